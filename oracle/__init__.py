@@ -1,0 +1,202 @@
+"""Float64 CPU oracle for the HedgeSpec drafter-evaluation path.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the bench's CPU-baseline
+leg may import this package; the product library never does. It shares no code
+with the GPU path; both sides read the same bytes from the seeded generator.
+
+The arithmetic lives in ``hs_oracle.c`` (plain fp64 loops, one function per
+definition in the paper); this module only marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "hs_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, no fast-math, no fused multiply-add, OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-fno-fast-math",
+                               "-ffp-contract=off", "-std=c11", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        P, I, I64, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        lib.or_row_stats.argtypes = [P, I, I64, D, P, P, P]
+        lib.or_row_stats.restype = None
+        lib.or_alpha.argtypes = [P, P, I, I64, D, D, D]
+        lib.or_alpha.restype = D
+        lib.or_eval.argtypes = [P, I, I64, I, I64, I64, D, I, P, P, P, P, P]
+        lib.or_eval.restype = I
+        lib.or_softmax_stats.argtypes = [P, I, I64, I64, I64, D, P, P, P]
+        lib.or_softmax_stats.restype = I
+        lib.or_path.argtypes = [P, I, I, P]
+        lib.or_path.restype = I
+        lib.or_eal_path.argtypes = [P, I]
+        lib.or_eal_path.restype = D
+        lib.or_accept_len.argtypes = [P, I, I, I, P, P, P, P, I, P]
+        lib.or_accept_len.restype = I
+        lib.or_hedge.argtypes = [P, P, I, I, I, D]
+        lib.or_hedge.restype = None
+        lib.or_normalhedge.argtypes = [P, P, P, P, I, I, I]
+        lib.or_normalhedge.restype = None
+        lib.or_normalhedge_residual.argtypes = [P, I, D]
+        lib.or_normalhedge_residual.restype = D
+        _lib = lib
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dtype_of(x: np.ndarray) -> int:
+    if x.dtype == np.float32:
+        return F32
+    if x.dtype == np.uint16:
+        return BF16
+    raise TypeError("logits must be float32 or uint16 (bf16 bit patterns), got %s" % x.dtype)
+
+
+def set_threads(n: int) -> None:
+    """Limit the OpenMP threads the oracle uses (for single-thread timing)."""
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+        gomp.omp_set_num_threads(ctypes.c_int(int(n)))
+    except OSError:
+        pass
+
+
+def row_stats(row: np.ndarray, T: float = 1.0):
+    """(max, argmax, lse) of one row of stored logits (float32 or bf16 bits)."""
+    row = np.ascontiguousarray(row)
+    m, a, l = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
+    _load().or_row_stats(_p(row), _dtype_of(row), row.shape[-1], T, ctypes.byref(m),
+                         ctypes.byref(a), ctypes.byref(l))
+    return m.value, a.value, l.value
+
+
+def alpha_pair(zt: np.ndarray, zi: np.ndarray, T: float = 1.0) -> float:
+    """Theorem 1: sum_v min(p_v, q_v) for two rows of stored logits."""
+    zt, zi = np.ascontiguousarray(zt), np.ascontiguousarray(zi)
+    _, _, lt = row_stats(zt, T)
+    _, _, li = row_stats(zi, T)
+    return _load().or_alpha(_p(zt), _p(zi), _dtype_of(zt), zt.shape[-1], T, lt, li)
+
+
+def evaluate(logits: np.ndarray, V: Optional[int] = None, T: float = 1.0, want_alpha: bool = True):
+    """Evaluate every drafter on every (query, position) group.
+
+    logits: [R][G][ld] (R = N + 1, row 0 = target) stored logits; any leading group shape
+    between R and ld is flattened, e.g. [R][B][K][ld].
+    Returns dict with alpha [G..][N], agree [G..][N] (uint8), argmax [G..][R] (int64),
+    rmax, rlse [G..][R].
+    """
+    R = logits.shape[0]
+    gshape = logits.shape[1:-1]
+    ld = logits.shape[-1]
+    V = ld if V is None else V
+    G = int(np.prod(gshape)) if gshape else 1
+    x = np.ascontiguousarray(logits).reshape(R, G, ld)
+    N = R - 1
+    alpha = np.full((G, N), np.nan)
+    agree = np.zeros((G, N), dtype=np.uint8)
+    argmax = np.zeros((G, R), dtype=np.int64)
+    rmax = np.zeros((G, R))
+    rlse = np.zeros((G, R))
+    rc = _load().or_eval(_p(x), _dtype_of(x), ld, R, G, V, T, 1 if want_alpha else 0,
+                         _p(alpha), _p(agree), _p(argmax), _p(rmax), _p(rlse))
+    if rc != 0:
+        raise ValueError("or_eval failed: %d" % rc)
+    return {"alpha": alpha.reshape(gshape + (N,)), "agree": agree.reshape(gshape + (N,)),
+            "argmax": argmax.reshape(gshape + (R,)), "rmax": rmax.reshape(gshape + (R,)),
+            "rlse": rlse.reshape(gshape + (R,))}
+
+
+def softmax_stats(x: np.ndarray, V: Optional[int] = None, T: float = 1.0):
+    """Row (max, argmax, lse) for a [rows][ld] tensor of stored logits."""
+    x = np.ascontiguousarray(x)
+    rows, ld = x.shape
+    V = ld if V is None else V
+    m = np.zeros(rows)
+    a = np.zeros(rows, dtype=np.int64)
+    l = np.zeros(rows)
+    rc = _load().or_softmax_stats(_p(x), _dtype_of(x), rows, V, ld, T, _p(m), _p(a), _p(l))
+    if rc != 0:
+        raise ValueError("or_softmax_stats failed: %d" % rc)
+    return m, a, l
+
+
+def eal_path(gamma) -> float:
+    """Theorem 3's estimator for the gamma sequence gamma_1..gamma_K along one path."""
+    g = np.ascontiguousarray(np.asarray(gamma, dtype=np.float64))
+    return _load().or_eal_path(_p(g), len(g))
+
+
+def path(parent, end: int) -> np.ndarray:
+    par = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    out = np.zeros(len(par) + 1, dtype=np.int32)
+    n = _load().or_path(_p(par), len(par), int(end), _p(out))
+    if n < 0:
+        raise ValueError("bad path")
+    return out[:n]
+
+
+def accept_len(gamma: np.ndarray, parent=None, path_end=None, loss_kind: int = LOSS_LENGTH,
+               want_prefix: bool = False):
+    """EAL [B][N], optional prefix [B][N][M], and loss [L][B][N] from gamma [B][N][M]."""
+    g = np.ascontiguousarray(gamma, dtype=np.float64)
+    B, N, M = g.shape
+    par = None if parent is None else np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    pe = None if path_end is None else np.ascontiguousarray(np.asarray(path_end, dtype=np.int32))
+    eal = np.zeros((B, N))
+    prefix = np.zeros((B, N, M)) if want_prefix else None
+    L = M if loss_kind == LOSS_ACCEPT_TOKEN else 1
+    loss = np.zeros((L, B, N))
+    rc = _load().or_accept_len(_p(g), B, N, M, _p(par), _p(pe), _p(eal), _p(prefix), loss_kind,
+                               _p(loss))
+    return {"eal": eal, "prefix": prefix, "loss": loss, "ok": rc == 0}
+
+
+def hedge(w: np.ndarray, loss: np.ndarray, eta: float) -> np.ndarray:
+    """Hedge update of normalised weights w [B][N] with loss [L][B][N]; returns new w."""
+    w = np.array(w, dtype=np.float64, order="C", copy=True)
+    loss = np.ascontiguousarray(loss, dtype=np.float64)
+    L, B, N = loss.shape
+    _load().or_hedge(_p(w), _p(loss), L, B, N, eta)
+    return w
+
+
+def normalhedge(R: np.ndarray, p: np.ndarray, loss: np.ndarray):
+    """NormalHedge update; returns (R, p, c) after the L loss vectors."""
+    R = np.array(R, dtype=np.float64, order="C", copy=True)
+    p = np.array(p, dtype=np.float64, order="C", copy=True)
+    loss = np.ascontiguousarray(loss, dtype=np.float64)
+    L, B, N = loss.shape
+    c = np.zeros(B)
+    _load().or_normalhedge(_p(R), _p(p), _p(c), _p(loss), L, B, N)
+    return R, p, c
+
+
+def normalhedge_residual(R_row: np.ndarray, c: float) -> float:
+    r = np.ascontiguousarray(R_row, dtype=np.float64)
+    return _load().or_normalhedge_residual(_p(r), len(r), c)

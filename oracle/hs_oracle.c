@@ -1,0 +1,346 @@
+/*
+ * Float64 CPU oracle for the HedgeSpec drafter-evaluation path.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product path may link, load or call
+ * this file; only the tests, the smoke check and the bench's CPU-baseline leg do.
+ * It shares no code, header or constant with the GPU library: the only thing
+ * both sides share is the input bytes written by the seeded generator.
+ *
+ * Every routine is the plain definition from the paper (arXiv 2510.20064),
+ * evaluated in fp64 with straightforward loops, no blocking and no reordering
+ * beyond what the definition states. Each routine names the passage it follows.
+ * Built with -O2 -fno-fast-math -ffp-contract=off.
+ *
+ * Parity status of each routine (pins live in the CPU test suite):
+ *   or_row_stats, or_alpha  : pinned (identities of Theorem 1, closed form for a
+ *                             boosted token, brute-force enumeration of the
+ *                             speculative-decoding box, disjoint supports).
+ *   or_eal_path, or_accept_len : pinned (Theorem 3 against brute force,
+ *                             worked example of the censoring appendix, constant-gamma
+ *                             closed form, range [1, K+1]).
+ *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
+ *   or_normalhedge          : pinned (closed-form c for one or m equal positive
+ *                             regrets, scale covariance, sum_i p_i dR_i = 0).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OR_F32 0
+#define OR_BF16 1
+
+#define OR_LOSS_LENGTH 0
+#define OR_LOSS_ACCEPT_TOKEN 1
+#define OR_LOSS_ACCEPT_CHUNK 2
+
+/* Exact decode of one stored logit to fp64: bf16 is the top half of an fp32. */
+static double or_decode(const void* base, int dtype, int64_t idx) {
+  if (dtype == OR_F32) return (double)((const float*)base)[idx];
+  uint32_t u = (uint32_t)((const uint16_t*)base)[idx] << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+/*
+ * Row statistics of a temperature softmax p = softmax(z / T).
+ *   max    : max_v z_v
+ *   argmax : the lowest v with z_v = max (left-to-right scan, strict >)
+ *   lse    : log sum_v exp(z_v / T) = max/T + log sum_v exp((z_v - max)/T)
+ * Greedy decoding picks the argmax of the raw logits, so the argmax does not
+ * depend on T. A row whose entries are all -inf has no distribution (lse = NaN).
+ */
+void or_row_stats(const void* row, int dtype, int64_t V, double T, double* max_out,
+                  int64_t* argmax_out, double* lse_out) {
+  double m = -INFINITY;
+  int64_t am = 0;
+  for (int64_t v = 0; v < V; ++v) {
+    double z = or_decode(row, dtype, v);
+    if (z > m) {
+      m = z;
+      am = v;
+    }
+  }
+  double s = 0.0;
+  for (int64_t v = 0; v < V; ++v) s += exp((or_decode(row, dtype, v) - m) / T);
+  if (max_out) *max_out = m;
+  if (argmax_out) *argmax_out = am;
+  if (lse_out) *lse_out = (m == -INFINITY) ? NAN : m / T + log(s);
+}
+
+/*
+ * Acceptance probability of speculative sampling (Theorem 1, Leviathan et al.
+ * Thm 3.5, restated in Section 2.2): alpha = sum_v min(p(v), q(v)) = 1 - TV(p, q),
+ * with p = softmax(z_t / T) and q = softmax(z_i / T). Clamped to [0, 1].
+ * lse_t / lse_i are the row log-normalisers from or_row_stats.
+ */
+double or_alpha(const void* zt, const void* zi, int dtype, int64_t V, double T, double lse_t,
+                double lse_i) {
+  double a = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    double p = exp(or_decode(zt, dtype, v) / T - lse_t);
+    double q = exp(or_decode(zi, dtype, v) / T - lse_i);
+    a += (p < q) ? p : q;
+  }
+  if (a < 0.0) a = 0.0;
+  if (a > 1.0) a = 1.0;
+  return a;
+}
+
+/*
+ * Evaluation of all drafters on G (query, position) groups.
+ * logits : [R][G][ld] stored logits, R = N + 1, row 0 = target, row 1 + i = drafter i.
+ * Outputs (any may be NULL):
+ *   alpha  [G][N]  : or_alpha of (target, drafter i)            (Theorem 1)
+ *   agree  [G][N]  : 1 if argmax target == argmax drafter i       (greedy form of Theorem 1)
+ *   argmax [G][R]  : argmax of every row
+ *   rmax, rlse [G][R] : row max and log-normaliser
+ * want_alpha = 0 skips the softmax work (greedy indicators only).
+ */
+int or_eval(const void* logits, int dtype, int64_t ld, int R, int64_t G, int64_t V, double T,
+            int want_alpha, double* alpha, uint8_t* agree, int64_t* argmax, double* rmax,
+            double* rlse) {
+  if (R < 2 || G < 1 || V < 1 || ld < V) return -1;
+  if (want_alpha && !(T > 0.0)) return -2;
+  int N = R - 1;
+  double* lse = (double*)malloc(sizeof(double) * (size_t)(R * G));
+  double* mx = (double*)malloc(sizeof(double) * (size_t)(R * G));
+  int64_t* am = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R * G));
+  double Ts = want_alpha ? T : 1.0;
+  size_t es = (dtype == OR_F32) ? 4 : 2;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t x = 0; x < (int64_t)R * G; ++x) {
+    int64_t r = x / G, g = x % G;
+    const char* row = (const char*)logits + (size_t)((r * G + g) * ld) * es;
+    or_row_stats(row, dtype, V, Ts, &mx[g * R + r], &am[g * R + r], &lse[g * R + r]);
+  }
+  if (want_alpha && alpha) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t x = 0; x < (int64_t)N * G; ++x) {
+      int64_t g = x / N;
+      int i = (int)(x % N);
+      const char* zt = (const char*)logits + (size_t)((0 * G + g) * ld) * es;
+      const char* zi = (const char*)logits + (size_t)(((1 + i) * G + g) * ld) * es;
+      alpha[g * N + i] = or_alpha(zt, zi, dtype, V, T, lse[g * R + 0], lse[g * R + 1 + i]);
+    }
+  }
+  for (int64_t g = 0; g < G; ++g) {
+    for (int r = 0; r < R; ++r) {
+      if (argmax) argmax[g * R + r] = am[g * R + r];
+      if (rmax) rmax[g * R + r] = mx[g * R + r];
+      if (rlse) rlse[g * R + r] = want_alpha ? lse[g * R + r] : NAN;
+    }
+    if (agree)
+      for (int i = 0; i < N; ++i) agree[g * N + i] = (uint8_t)(am[g * R + 0] == am[g * R + 1 + i]);
+  }
+  free(lse);
+  free(mx);
+  free(am);
+  return 0;
+}
+
+/* Row statistics of `rows` rows of a [rows][ld] tensor (one temperature softmax each). */
+int or_softmax_stats(const void* x, int dtype, int64_t rows, int64_t V, int64_t ld, double T,
+                     double* rmax, int64_t* rargmax, double* rlse) {
+  if (rows < 1 || V < 1 || ld < V || !(T > 0.0)) return -1;
+  size_t es = (dtype == OR_F32) ? 4 : 2;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < rows; ++r)
+    or_row_stats((const char*)x + (size_t)(r * ld) * es, dtype, V, T, &rmax[r], &rargmax[r],
+                 &rlse[r]);
+  return 0;
+}
+
+/*
+ * The node path root -> end of a draft tree given by parent pointers
+ * (parent[0] = -1, parent[n] < n). Node n carries the feedback gamma of the
+ * token that follows the prefix ending at n (Section 3.2: gamma_{j,i} for the
+ * j-th verified position). Writes the path root first; returns its length.
+ */
+int or_path(const int32_t* parent, int M, int end, int32_t* path) {
+  int len = 0;
+  int32_t tmp[4096];
+  for (int n = end; n >= 0; n = parent[n]) {
+    if (len >= 4096 || n >= M) return -1;
+    tmp[len++] = n;
+  }
+  for (int j = 0; j < len; ++j) path[j] = tmp[len - 1 - j];
+  return len;
+}
+
+/*
+ * Theorem 3 (one-step counterfactual AcceptLength estimator), taken literally:
+ *   EAL = sum_{k=1}^{K+1} k (1 - gamma_k) prod_{j=1}^{k-1} gamma_j,  gamma_{K+1} = 0.
+ * gamma[0..K-1] holds gamma_1..gamma_K. The value lies in [1, K+1] (Section 3.2).
+ */
+double or_eal_path(const double* gamma, int K) {
+  double eal = 0.0;
+  for (int k = 1; k <= K + 1; ++k) {
+    double gk = (k <= K) ? gamma[k - 1] : 0.0;
+    double prod = 1.0;
+    for (int j = 1; j <= k - 1; ++j) prod *= gamma[j - 1];
+    eal += (double)k * (1.0 - gk) * prod;
+  }
+  return eal;
+}
+
+/*
+ * Expected acceptance length and losses for B queries and N drafters.
+ * gamma   : [B][N][M] feedback per node (chain: M = K positions).
+ * parent  : [M] or NULL for a chain (parent[k] = k - 1).
+ * path_end: [B] or NULL (node M - 1).
+ * eal     : [B][N] Theorem 3 along the path root -> path_end[b].
+ * prefix  : [B][N][M] or NULL: product of gamma over the path root -> n, for every node n.
+ * loss    : [L][B][N] or NULL, by loss_kind:
+ *   LENGTH        : 1 - EAL / (K_path + 1)                      (chunk length loss, Appendix "Chunk-Level Games")
+ *   ACCEPT_TOKEN  : L = M vectors, l_k = 1 - gamma_k (chain only) (acceptance-probability loss, Section 3.3)
+ *   ACCEPT_CHUNK  : (1/K_path) sum_k (1 - gamma_k)               (chunk acceptance loss, Appendix "Chunk-Level Games")
+ * Returns 0, or -1 on an invalid path.
+ */
+int or_accept_len(const double* gamma, int B, int N, int M, const int32_t* parent,
+                  const int32_t* path_end, double* eal, double* prefix, int loss_kind,
+                  double* loss) {
+  int32_t* chainpar = NULL;
+  if (!parent) {
+    chainpar = (int32_t*)malloc(sizeof(int32_t) * (size_t)M);
+    for (int k = 0; k < M; ++k) chainpar[k] = k - 1;
+    parent = chainpar;
+  }
+  int bad = 0;
+  for (int b = 0; b < B; ++b) {
+    int end = path_end ? path_end[b] : M - 1;
+    int32_t path[4096];
+    int len = (end >= 0 && end < M) ? or_path(parent, M, end, path) : -1;
+    for (int i = 0; i < N; ++i) {
+      const double* g = gamma + ((size_t)b * N + i) * M;
+      if (len < 1) {
+        bad = 1;
+        eal[b * N + i] = NAN;
+        if (loss) loss[b * N + i] = NAN;
+        continue;
+      }
+      double gp[4096];
+      for (int j = 0; j < len; ++j) gp[j] = g[path[j]];
+      double e = or_eal_path(gp, len);
+      eal[b * N + i] = e;
+      if (prefix) {
+        for (int n = 0; n < M; ++n) {
+          int32_t pn[4096];
+          int ln = or_path(parent, M, n, pn);
+          double pr = 1.0;
+          for (int j = 0; j < ln; ++j) pr *= g[pn[j]];
+          prefix[((size_t)b * N + i) * M + n] = pr;
+        }
+      }
+      if (loss) {
+        if (loss_kind == OR_LOSS_LENGTH) {
+          loss[b * N + i] = 1.0 - e / (double)(len + 1);
+        } else if (loss_kind == OR_LOSS_ACCEPT_CHUNK) {
+          double s = 0.0;
+          for (int j = 0; j < len; ++j) s += 1.0 - gp[j];
+          loss[b * N + i] = s / (double)len;
+        } else {
+          for (int k = 0; k < M; ++k) loss[((size_t)k * B + b) * N + i] = 1.0 - g[k];
+        }
+      }
+    }
+  }
+  free(chainpar);
+  return bad ? -1 : 0;
+}
+
+/*
+ * Hedge (Appendix "Online Learning with Delayed Feedback", remark on Hedge):
+ * Update applies w_i <- w_i exp(-eta l_i) for each of the L loss vectors in
+ * FIFO order; Predict returns the normalised weights. w is [B][N], one learner
+ * per query, and holds normalised weights on entry and exit.
+ */
+void or_hedge(double* w, const double* loss, int L, int B, int N, double eta) {
+  for (int b = 0; b < B; ++b) {
+    double* wb = w + (size_t)b * N;
+    for (int l = 0; l < L; ++l) {
+      const double* lb = loss + ((size_t)l * B + b) * N;
+      double s = 0.0;
+      for (int i = 0; i < N; ++i) {
+        wb[i] = wb[i] * exp(-eta * lb[i]);
+        s += wb[i];
+      }
+      for (int i = 0; i < N; ++i) wb[i] /= s;
+    }
+  }
+}
+
+/* (1/N) sum_i exp(r_i^2 / (2c)), the left side of NormalHedge's scale equation. */
+static double nh_g(const double* r, int N, double c) {
+  double s = 0.0;
+  for (int i = 0; i < N; ++i) s += exp(r[i] * r[i] / (2.0 * c));
+  return s / (double)N;
+}
+
+/*
+ * NormalHedge (Appendix "Variants of Hedging Algorithmic choice", figure
+ * "The workflow of NormalHedge"), one learner per query, for each of the L loss
+ * vectors in order:
+ *   l_A = sum_i p_i l_i
+ *   R_i <- R_i + (l_A - l_i)
+ *   find c > 0 with (1/N) sum_i exp([R_i]_+^2 / (2c)) = e
+ *   p_i <- ([R_i]_+ / c) exp([R_i]_+^2 / (2c)), normalised.
+ * The left side decreases strictly in c; with M = max_i [R_i]_+^2 it is <= e at
+ * c = M/2 and >= e at c = M/(2(1 + ln N)), so the root is found by bisection on
+ * that bracket, run until the bracket's relative width is below 1e-15.
+ * When every [R_i]_+ is 0 the equation has no root; p is then uniform and c = 0.
+ * R, p: [B][N] in/out; c: [B] out (value of the last update).
+ */
+void or_normalhedge(double* R, double* p, double* c, const double* loss, int L, int B, int N) {
+  const double E = exp(1.0);
+  double* r = (double*)malloc(sizeof(double) * (size_t)N);
+  for (int b = 0; b < B; ++b) {
+    double* Rb = R + (size_t)b * N;
+    double* pb = p + (size_t)b * N;
+    double cb = 0.0;
+    for (int l = 0; l < L; ++l) {
+      const double* lb = loss + ((size_t)l * B + b) * N;
+      double la = 0.0;
+      for (int i = 0; i < N; ++i) la += pb[i] * lb[i];
+      double M = 0.0;
+      for (int i = 0; i < N; ++i) {
+        Rb[i] = Rb[i] + (la - lb[i]);
+        r[i] = Rb[i] > 0.0 ? Rb[i] : 0.0;
+        if (r[i] * r[i] > M) M = r[i] * r[i];
+      }
+      if (M == 0.0) {
+        for (int i = 0; i < N; ++i) pb[i] = 1.0 / (double)N;
+        cb = 0.0;
+        continue;
+      }
+      double lo = M / (2.0 * (1.0 + log((double)N))), hi = M / 2.0;
+      for (int it = 0; it < 4000 && hi - lo > 1e-15 * hi; ++it) {
+        double mid = 0.5 * (lo + hi);
+        if (mid <= lo || mid >= hi) break;
+        if (nh_g(r, N, mid) > E)
+          lo = mid;
+        else
+          hi = mid;
+      }
+      cb = 0.5 * (lo + hi);
+      double s = 0.0;
+      for (int i = 0; i < N; ++i) {
+        pb[i] = (r[i] / cb) * exp(r[i] * r[i] / (2.0 * cb));
+        s += pb[i];
+      }
+      for (int i = 0; i < N; ++i) pb[i] /= s;
+    }
+    c[b] = cb;
+  }
+  free(r);
+}
+
+/* Residual (1/N) sum exp(r^2/2c) - e for a given regret row; exposed for the pins. */
+double or_normalhedge_residual(const double* R, int N, double c) {
+  double* r = (double*)malloc(sizeof(double) * (size_t)N);
+  for (int i = 0; i < N; ++i) r[i] = R[i] > 0.0 ? R[i] : 0.0;
+  double g = nh_g(r, N, c) - exp(1.0);
+  free(r);
+  return g;
+}

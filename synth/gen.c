@@ -1,0 +1,174 @@
+/*
+ * Seeded synthetic logits for the drafter-evaluation workloads.
+ *
+ * This file is input plumbing only: it draws numbers and rounds them to the
+ * storage type. It contains none of the arithmetic of the method being tested
+ * (no softmax, no acceptance probability, no learner). Both the oracle and the
+ * GPU path consume the bytes it writes.
+ *
+ * Generator (counter based, so any row can be produced on its own):
+ *   mix64      : the splitmix64 output finaliser (Steele, Lea, Flood 2014).
+ *   row key    : mix64-chained over (seed, round, tensor, query b, position k).
+ *   element v  : two 64-bit draws h1 = mix64(key + (2v+1)*G), h2 = mix64(key + (2v+2)*G),
+ *                G = 0x9E3779B97F4A7C15. Their eight 16-bit fields c_j are
+ *                summed; Z = (sum c_j - 262140) * sqrt(1.5) / 65536 is the
+ *                standardised Irwin-Hall(8) variate (mean 0, variance 1,
+ *                support +-4.9). It needs only integer work plus one fp64
+ *                multiply, so it is bit-reproducible on any IEEE machine.
+ *   target     : t = sigma_t * Z (+ boost on nboost distinct seeded indices of
+ *                the row), rounded to the storage type.
+ *   drafter i  : d = decode(stored t) + s * Z_i, rounded (the noise is added to
+ *                exactly what the kernel reads).
+ *   rounding   : fp64 -> fp32 round-to-nearest-even, then (bf16 storage)
+ *                fp32 -> bf16 round-to-nearest-even on the bit pattern.
+ * Build with -ffp-contract=off so that no multiply-add is fused.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+#define SYN_F32 0
+#define SYN_BF16 1
+
+static const uint64_t GOLD = 0x9E3779B97F4A7C15ULL;
+
+static inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+static inline uint64_t chain(uint64_t key, uint64_t x) { return mix64(key ^ mix64(x + GOLD)); }
+
+uint64_t synth_row_key(uint64_t seed, int64_t round, int64_t tensor, int64_t b, int64_t k) {
+  uint64_t h = mix64(seed + GOLD);
+  h = chain(h, (uint64_t)round);
+  h = chain(h, (uint64_t)tensor);
+  h = chain(h, (uint64_t)b);
+  h = chain(h, (uint64_t)k);
+  return h;
+}
+
+static inline double normal_at(uint64_t key, int64_t v) {
+  uint64_t h1 = mix64(key + (uint64_t)(2 * v + 1) * GOLD);
+  uint64_t h2 = mix64(key + (uint64_t)(2 * v + 2) * GOLD);
+  int64_t s = 0;
+  for (int j = 0; j < 4; ++j) {
+    s += (int64_t)((h1 >> (16 * j)) & 0xFFFF);
+    s += (int64_t)((h2 >> (16 * j)) & 0xFFFF);
+  }
+  return (double)(s - 262140) * (1.2247448713915890491 / 65536.0);
+}
+
+double synth_normal(uint64_t key, int64_t v) { return normal_at(key, v); }
+
+static inline uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+static inline float bf16_to_f32(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* Round an fp64 value to the storage type; returns the stored value decoded back. */
+static inline double store_one(double x, int dtype, void* out, int64_t idx) {
+  float f = (float)x;
+  if (dtype == SYN_F32) {
+    ((float*)out)[idx] = f;
+    return (double)f;
+  }
+  uint16_t h = f32_to_bf16_rne(f);
+  ((uint16_t*)out)[idx] = h;
+  return (double)bf16_to_f32(h);
+}
+
+/* nboost distinct indices in [0, V), drawn by hashing with rejection of repeats. */
+int synth_boost_indices(uint64_t seed, int64_t round, int64_t b, int64_t k, int64_t V, int nboost,
+                        int64_t* idx) {
+  if (nboost > V) return -1;
+  uint64_t key = synth_row_key(seed, round, 0x626F6F7374LL /* "boost" */, b, k);
+  int n = 0;
+  for (uint64_t ctr = 0; n < nboost; ++ctr) {
+    int64_t cand = (int64_t)(mix64(key + (ctr + 1) * GOLD) % (uint64_t)V);
+    int dup = 0;
+    for (int j = 0; j < n; ++j) dup |= (idx[j] == cand);
+    if (!dup) idx[n++] = cand;
+  }
+  return 0;
+}
+
+/*
+ * Fill rows of the [R][B][K][V] logits tensor, R = N + 1 (row 0 = target,
+ * row 1 + i = drafter i).
+ *   rows      : tensor rows to produce (values in [0, N]), nrows of them.
+ *   bk        : (b, k) pairs to produce, nbk of them (b-major pairs), or NULL for all B*K in order.
+ *   scale     : [B][N] noise scale of drafter i at query b.
+ *   out       : [nrows][nbk][ld] elements of the storage type; only the first V of each row are written.
+ */
+int synth_fill(int dtype, int64_t V, int64_t ld, int B, int K, int N, uint64_t seed, int64_t round,
+               double sigma_t, int nboost, double boost, const double* scale, const int32_t* rows,
+               int nrows, const int32_t* bk, int64_t nbk, void* out) {
+  if (dtype != SYN_F32 && dtype != SYN_BF16) return -1;
+  if (V < 1 || ld < V || B < 1 || K < 1 || N < 1 || nboost < 0 || nboost > V) return -2;
+  int64_t nitems = (bk ? nbk : (int64_t)B * K);
+  int64_t total = nitems * nrows;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t it = 0; it < total; ++it) {
+    int64_t ri = it / nitems, p = it % nitems;
+    int row = rows[ri];
+    int64_t b = bk ? bk[2 * p] : p / K;
+    int64_t k = bk ? bk[2 * p + 1] : p % K;
+    int64_t base = (ri * nitems + p) * ld;
+    uint64_t tkey = synth_row_key(seed, round, 0, b, k);
+    int64_t bidx[64];
+    int nb = nboost < 64 ? nboost : 64;
+    if (nb > 0) synth_boost_indices(seed, round, b, k, V, nb, bidx);
+    if (row == 0) {
+      for (int64_t v = 0; v < V; ++v) {
+        double t = sigma_t * normal_at(tkey, v);
+        for (int j = 0; j < nb; ++j)
+          if (bidx[j] == v) t = t + boost;
+        store_one(t, dtype, out, base + v);
+      }
+    } else {
+      double s = scale[b * N + (row - 1)];
+      uint64_t dkey = synth_row_key(seed, round, row, b, k);
+      float tmpf;
+      uint16_t tmph;
+      for (int64_t v = 0; v < V; ++v) {
+        double t = sigma_t * normal_at(tkey, v);
+        for (int j = 0; j < nb; ++j)
+          if (bidx[j] == v) t = t + boost;
+        double ts = (dtype == SYN_F32) ? store_one(t, dtype, &tmpf, 0) : store_one(t, dtype, &tmph, 0);
+        double d = ts + s * normal_at(dkey, v);
+        store_one(d, dtype, out, base + v);
+      }
+    }
+  }
+  return 0;
+}
+
+/* Seeded Fisher-Yates shuffle of 0..n-1 keyed by (seed, tag, b). */
+void synth_permutation(uint64_t seed, int64_t tag, int64_t b, int n, int32_t* perm) {
+  uint64_t key = synth_row_key(seed, 0, tag, b, 0);
+  for (int i = 0; i < n; ++i) perm[i] = i;
+  for (int i = n - 1; i > 0; --i) {
+    int j = (int)(mix64(key + (uint64_t)(i + 1) * GOLD) % (uint64_t)(i + 1));
+    int32_t t = perm[i];
+    perm[i] = perm[j];
+    perm[j] = t;
+  }
+}
+
+/* Uniform integer in [0, n) keyed by (seed, tag, a, c); used for seeded tree descents. */
+int64_t synth_uniform_int(uint64_t seed, int64_t tag, int64_t a, int64_t c, int64_t n) {
+  uint64_t key = synth_row_key(seed, 0, tag, a, c);
+  return (int64_t)(mix64(key + GOLD) % (uint64_t)n);
+}

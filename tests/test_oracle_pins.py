@@ -1,0 +1,369 @@
+"""Pins that tie the float64 oracle to the paper and to mathematics, not to itself.
+
+Each test checks the oracle against something fixed independently of its code:
+identities of Theorem 1, closed forms, the paper's worked example, exact
+enumeration of the speculative-decoding procedure on tiny vocabularies, and
+invariants of Hedge / NormalHedge. A plausible slip in the oracle (a dropped
+term, a wrong sign or index, T applied the wrong way, the wrong p used for the
+learner's loss) fails at least one of them.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bf16(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round to nearest even (test-side helper)."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = u + 0x7FFF + ((u >> 16) & 1)
+    return (u >> 16).astype(np.uint16)
+
+
+def _softmax(z: np.ndarray, T: float) -> np.ndarray:
+    x = z.astype(np.float64) / T
+    x = x - x.max()
+    e = np.exp(x)
+    return e / e.sum()
+
+
+# ------------------------------------------------------------------------------------------
+# Theorem 1: alpha = sum min(p, q) = 1 - TV(p, q)
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T", [1.0, 0.7, 0.05, 20.0])
+def test_alpha_of_identical_rows_is_one(T):
+    rng = np.random.default_rng(1)
+    z = rng.normal(0, 3, 5000).astype(np.float32)
+    assert abs(oracle.alpha_pair(z, z, T) - 1.0) < 1e-12
+    zb = _bf16(z)
+    assert abs(oracle.alpha_pair(zb, zb, T) - 1.0) < 1e-12
+
+
+def test_alpha_disjoint_supports_is_exactly_zero():
+    rng = np.random.default_rng(2)
+    V = 4096
+    zt = rng.normal(0, 2, V).astype(np.float32)
+    zi = rng.normal(0, 2, V).astype(np.float32)
+    mask = rng.random(V) < 0.5
+    zt[mask] = -np.inf
+    zi[~mask] = -np.inf
+    assert oracle.alpha_pair(zt, zi, 1.0) == 0.0
+
+
+@pytest.mark.parametrize("T", [1.0, 0.5, 3.0])
+def test_alpha_symmetric_bounded_and_equals_one_minus_tv(T):
+    rng = np.random.default_rng(3)
+    for V in [2, 17, 1000, 32000]:
+        zt = rng.normal(0, 2, V).astype(np.float32)
+        zi = (zt + rng.normal(0, 1.5, V)).astype(np.float32)
+        a = oracle.alpha_pair(zt, zi, T)
+        assert 0.0 <= a <= 1.0
+        assert abs(a - oracle.alpha_pair(zi, zt, T)) < 1e-13
+        p, q = _softmax(zt, T), _softmax(zi, T)
+        tv = 0.5 * np.abs(p - q).sum()
+        assert abs(a - (1.0 - tv)) < 1e-12
+        # acceptance-rule form of the speculative-decoding box: sum_v q_v min(1, p_v / q_v)
+        assert abs(a - np.sum(q * np.minimum(1.0, p / q))) < 1e-12
+
+
+@pytest.mark.parametrize("T", [1.0, 0.5, 2.0])
+@pytest.mark.parametrize("delta", [0.5, 3.0, 9.0])
+def test_alpha_closed_form_one_boosted_token_full_vocab(T, delta):
+    # p uniform over V; q uniform except one token boosted by delta:
+    # alpha = 1/V + (V - 1) / (e^{delta/T} + V - 1)
+    V = 151936
+    zt = np.zeros(V, dtype=np.float32)
+    zi = np.zeros(V, dtype=np.float32)
+    zi[12345] = delta
+    want = 1.0 / V + (V - 1) / (math.exp(delta / T) + V - 1)
+    assert abs(oracle.alpha_pair(zt, zi, T) - want) < 1e-11
+    assert abs(oracle.alpha_pair(zi, zt, T) - want) < 1e-11
+    # the same in bf16 storage (0 and delta are exact in bf16)
+    assert abs(oracle.alpha_pair(_bf16(zt), _bf16(zi), T) - want) < 1e-11
+
+
+def test_alpha_single_token_vocab_is_one():
+    assert oracle.alpha_pair(np.array([3.0], np.float32), np.array([-7.0], np.float32), 1.0) == 1.0
+
+
+def test_alpha_temperature_to_zero_gives_greedy_indicator():
+    rng = np.random.default_rng(4)
+    V = 64
+    for _ in range(20):
+        zt = rng.normal(0, 1, V).astype(np.float32)
+        zi = (zt + rng.normal(0, 1, V)).astype(np.float32)
+        st, si = np.sort(zt), np.sort(zi)
+        if st[-1] - st[-2] < 0.05 or si[-1] - si[-2] < 0.05:
+            continue
+        a = oracle.alpha_pair(zt, zi, 1e-3)
+        g = float(np.argmax(zt) == np.argmax(zi))
+        assert abs(a - g) < 1e-9
+
+
+def test_row_stats_argmax_lowest_index_and_lse():
+    z = np.array([0.5, 2.0, -1.0, 2.0, 2.0, 1.0], dtype=np.float32)
+    m, a, l = oracle.row_stats(z, 0.5)
+    assert m == 2.0 and a == 1
+    want = math.log(sum(math.exp(float(v) / 0.5) for v in z))
+    assert abs(l - want) < 1e-13
+    # bf16 ties (0x4000 == 2.0), and a -inf entry
+    zb = np.array([0x3F80, 0x4000, 0xFF80, 0x4000], dtype=np.uint16)
+    m, a, l = oracle.row_stats(zb, 1.0)
+    assert m == 2.0 and a == 1
+    assert abs(l - math.log(math.e + 2 * math.e ** 2)) < 1e-13
+
+
+def test_evaluate_greedy_indicators_and_shapes():
+    # target argmax 3 (tie with 7 resolved to the lowest index)
+    V = 10
+    t = np.zeros(V, np.float32)
+    t[3] = t[7] = 5.0
+    d1 = np.zeros(V, np.float32)
+    d1[3] = 1.0
+    d2 = np.zeros(V, np.float32)
+    d2[7] = 1.0
+    d3 = t.copy()
+    x = np.stack([t, d1, d2, d3])[:, None, :]  # [R][G=1][V]
+    out = oracle.evaluate(x, T=1.0)
+    assert list(out["argmax"][0]) == [3, 3, 7, 3]
+    assert list(out["agree"][0]) == [1, 0, 1]
+    assert abs(out["alpha"][0, 2] - 1.0) < 1e-12
+
+
+# ------------------------------------------------------------------------------------------
+# Speculative-decoding box (Section 2.2), enumerated exactly on tiny vocabularies
+# ------------------------------------------------------------------------------------------
+
+def _sd_box_enumeration(P, Q):
+    """Exact expectation of the number of tokens one chunk emits, and the law of its first token,
+    for the speculative-decoding procedure with position-wise distributions P[k], Q[k]."""
+    K, V = len(P), len(P[0])
+    expected = 0.0
+    first = np.zeros(V)
+    res0 = np.maximum(P[0] - Q[0], 0.0)
+    for drafts in itertools.product(range(V), repeat=K):
+        reach = float(np.prod([Q[k][d] for k, d in enumerate(drafts)]))
+        if reach == 0.0:
+            continue
+        for k, d in enumerate(drafts):
+            acc = min(1.0, P[k][d] / Q[k][d])
+            rej = reach * (1.0 - acc)
+            expected += rej * (k + 1)  # k accepted drafts + the resampled token
+            if k == 0:
+                first[d] += reach * acc
+                if res0.sum() > 0:
+                    first += rej * res0 / res0.sum()
+            reach *= acc
+        expected += reach * (K + 1)  # all K accepted + the bonus token
+    return expected, first
+
+
+@pytest.mark.parametrize("V,K,T", [(2, 1, 1.0), (3, 2, 1.0), (4, 3, 0.7), (5, 3, 1.6), (3, 3, 0.3)])
+def test_bruteforce_sd_box_matches_alpha_and_eal(V, K, T):
+    rng = np.random.default_rng(100 + 10 * V + K)
+    for trial in range(3):
+        zt = rng.normal(0, 1.5, (K, V)).astype(np.float32)
+        zq = (zt + rng.normal(0, 1.0, (K, V))).astype(np.float32)
+        if trial == 2:
+            zq[0, 0] = -np.inf  # a token the drafter never proposes
+        P = [_softmax(zt[k], T) for k in range(K)]
+        Q = [_softmax(zq[k], T) for k in range(K)]
+        expected, first = _sd_box_enumeration(P, Q)
+        # Theorem 1: the first emitted token is distributed as p
+        assert np.allclose(first, P[0], atol=1e-13)
+        gam = [oracle.alpha_pair(zt[k], zq[k], T) for k in range(K)]
+        # Theorem 3 with position-wise fixed distributions is exact
+        assert abs(oracle.eal_path(gam) - expected) < 1e-12
+
+
+def test_bruteforce_greedy_is_one_plus_leading_agreement_run():
+    for bits in itertools.product([0.0, 1.0], repeat=5):
+        run = 0
+        for g in bits:
+            if g == 0.0:
+                break
+            run += 1
+        assert oracle.eal_path(list(bits)) == 1.0 + run
+
+
+# ------------------------------------------------------------------------------------------
+# Theorem 3 estimator
+# ------------------------------------------------------------------------------------------
+
+def test_worked_example_censoring_appendix():
+    with open(os.path.join(GOLDEN, "censoring_example.json")) as f:
+        gold = json.load(f)
+    for case in gold["cases"]:
+        assert len(case["gamma"]) == case["K"]
+        assert abs(oracle.eal_path(case["gamma"]) - case["eal"]) < 1e-12, case["name"]
+
+
+@pytest.mark.parametrize("K", [1, 2, 4, 8, 9])
+def test_eal_constant_gamma_closed_form(K):
+    for a in [0.0, 0.25, 0.6, 0.9, 0.999]:
+        want = (1 - a ** (K + 1)) / (1 - a)
+        assert abs(oracle.eal_path([a] * K) - want) < 1e-12
+    assert abs(oracle.eal_path([1.0] * K) - (K + 1)) < 1e-12
+    assert oracle.eal_path([0.3] + [1.0] * (K - 1)) == pytest.approx(1 + 0.3 * K, abs=1e-12)
+
+
+def test_eal_range_is_one_to_k_plus_one():
+    rng = np.random.default_rng(5)
+    for K in [1, 3, 8, 20]:
+        for _ in range(50):
+            e = oracle.eal_path(rng.random(K))
+            assert 1.0 - 1e-12 <= e <= K + 1 + 1e-12
+
+
+def test_tree_prefix_products_and_path_eal_hand_computed():
+    parent = [-1, 0, 0, 1, 1, 2]
+    gam = np.array([0.9, 0.8, 0.7, 0.6, 0.5, 0.4])[None, None, :]  # [B=1][N=1][M=6]
+    out = oracle.accept_len(gam, parent=parent, path_end=[4], want_prefix=True)
+    # path 0 -> 1 -> 4; prefix products by hand
+    assert np.allclose(out["prefix"][0, 0], [0.9, 0.72, 0.63, 0.432, 0.36, 0.252], atol=1e-15)
+    assert abs(out["eal"][0, 0] - (1 + 0.9 + 0.72 + 0.36)) < 1e-12
+    assert list(oracle.path(parent, 5)) == [0, 2, 5]
+    # a path through the tree equals the chain of its gammas
+    out = oracle.accept_len(gam, parent=parent, path_end=[5])
+    assert abs(out["eal"][0, 0] - oracle.eal_path([0.9, 0.7, 0.4])) < 1e-15
+    # length loss 1 - EAL / (K_path + 1) with K_path = 3
+    assert abs(out["loss"][0, 0, 0] - (1 - out["eal"][0, 0] / 4)) < 1e-15
+
+
+def test_chain_equals_tree_with_chain_parents():
+    rng = np.random.default_rng(6)
+    g = rng.random((3, 5, 8))
+    a = oracle.accept_len(g)
+    b = oracle.accept_len(g, parent=np.arange(-1, 7), path_end=[7, 7, 7])
+    assert np.array_equal(a["eal"], b["eal"])
+
+
+def test_loss_kinds_on_worked_example():
+    g = np.array([1.0, 0.0])[None, None, :]
+    assert abs(oracle.accept_len(g, loss_kind=oracle.LOSS_LENGTH)["loss"][0, 0, 0] - 1 / 3) < 1e-15
+    tok = oracle.accept_len(g, loss_kind=oracle.LOSS_ACCEPT_TOKEN)["loss"]
+    assert tok.shape == (2, 1, 1) and list(tok[:, 0, 0]) == [0.0, 1.0]
+    assert oracle.accept_len(g, loss_kind=oracle.LOSS_ACCEPT_CHUNK)["loss"][0, 0, 0] == 0.5
+    # all-accept gives zero loss; all-reject gives K/(K+1) length loss
+    assert oracle.accept_len(np.ones((1, 1, 4)))["loss"][0, 0, 0] == 0.0
+    assert abs(oracle.accept_len(np.zeros((1, 1, 4)))["loss"][0, 0, 0] - 0.8) < 1e-15
+
+
+def test_out_of_range_path_end_gives_nan():
+    out = oracle.accept_len(np.ones((1, 2, 4)), path_end=[9])
+    assert not out["ok"] and np.isnan(out["eal"]).all()
+
+
+# ------------------------------------------------------------------------------------------
+# Hedge
+# ------------------------------------------------------------------------------------------
+
+def test_hedge_eta_zero_stays_uniform_and_sums_to_one():
+    rng = np.random.default_rng(7)
+    w = np.full((3, 6), 1 / 6)
+    loss = rng.random((5, 3, 6))
+    assert np.allclose(oracle.hedge(w, loss, 0.0), 1 / 6, atol=1e-15)
+    w2 = oracle.hedge(w, loss, 0.7)
+    assert np.allclose(w2.sum(axis=1), 1.0, atol=1e-14)
+
+
+def test_hedge_closed_form_cumulative_loss_and_shift_invariance():
+    rng = np.random.default_rng(8)
+    B, N, steps, eta = 4, 9, 40, 0.3
+    loss = rng.random((steps, 1, B, N))
+    w = np.full((B, N), 1 / N)
+    for t in range(steps):
+        w = oracle.hedge(w, loss[t], eta)
+    cum = loss.sum(axis=(0, 1))
+    logits = -eta * cum
+    want = np.exp(logits - logits.max(axis=1, keepdims=True))
+    want /= want.sum(axis=1, keepdims=True)
+    assert np.allclose(w, want, atol=1e-13)
+    # adding a constant to every expert's loss changes nothing
+    w_shift = np.full((B, N), 1 / N)
+    for t in range(steps):
+        w_shift = oracle.hedge(w_shift, loss[t] + 0.37, eta)
+    assert np.allclose(w_shift, w, atol=1e-13)
+    # L vectors in one call == L calls
+    w_one = oracle.hedge(np.full((B, N), 1 / N), loss[:, 0], eta)
+    assert np.allclose(w_one, w, atol=1e-13)
+
+
+# ------------------------------------------------------------------------------------------
+# NormalHedge
+# ------------------------------------------------------------------------------------------
+
+def test_normalhedge_single_positive_regret_closed_form():
+    N = 4
+    R0 = np.zeros((1, N))
+    p0 = np.full((1, N), 1 / N)
+    loss = np.array([[[0.0, 1.0, 1.0, 1.0]]])  # l_A = 0.75 -> R = (0.75, -0.25, -0.25, -0.25)
+    R, p, c = oracle.normalhedge(R0, p0, loss)
+    assert np.allclose(R, [[0.75, -0.25, -0.25, -0.25]], atol=1e-15)
+    want_c = 0.75 ** 2 / (2 * math.log(N * (math.e - 1) + 1))
+    assert abs(c[0] - want_c) < 1e-14 * want_c
+    assert np.allclose(p, [[1.0, 0.0, 0.0, 0.0]], atol=1e-15)
+
+
+def test_normalhedge_m_equal_positive_regrets_closed_form():
+    N, m = 5, 2
+    loss = np.array([[[0.0, 0.0, 1.0, 1.0, 1.0]]])  # l_A = 0.6 -> R = (.6, .6, -.4, -.4, -.4)
+    R, p, c = oracle.normalhedge(np.zeros((1, N)), np.full((1, N), 1 / N), loss)
+    want_c = 0.36 / (2 * math.log((N * (math.e - 1) + m) / m))
+    assert abs(c[0] - want_c) < 1e-14 * want_c
+    assert np.allclose(p, [[0.5, 0.5, 0, 0, 0]], atol=1e-15)
+
+
+def test_normalhedge_all_nonpositive_regret_is_uniform():
+    R, p, c = oracle.normalhedge(np.zeros((2, 3)), np.full((2, 3), 1 / 3), np.full((1, 2, 3), 0.4))
+    assert np.allclose(p, 1 / 3) and np.all(c == 0.0)
+
+
+def test_normalhedge_stream_invariants():
+    rng = np.random.default_rng(9)
+    B, N = 3, 16
+    R = np.zeros((B, N))
+    p = np.full((B, N), 1 / N)
+    base = rng.random((B, N))
+    cum = np.zeros((B, N))
+    for t in range(200):
+        loss = np.clip(base + rng.uniform(-0.3, 0.3, (B, N)), 0, 1)[None]
+        cum += loss[0]
+        R_new, p_new, c = oracle.normalhedge(R, p, loss)
+        # the learner's loss uses the distribution before the update: sum_i p_i dR_i = 0
+        assert np.all(np.abs(((R_new - R) * p).sum(axis=1)) < 1e-13)
+        assert np.allclose(p_new.sum(axis=1), 1.0, atol=1e-13)
+        for b in range(B):
+            if c[b] > 0:
+                assert abs(oracle.normalhedge_residual(R_new[b], c[b])) < 1e-12
+            assert np.all(p_new[b][R_new[b] <= 0] == 0.0) or c[b] == 0
+        R, p = R_new, p_new
+    # p is increasing in the regret, so the best expert in hindsight carries the largest weight
+    assert np.all(np.argmax(p, axis=1) == np.argmin(cum, axis=1))
+    for b in range(B):
+        order = np.argsort(R[b])
+        assert np.all(np.diff(p[b][order]) >= -1e-15)
+
+
+def test_normalhedge_scale_covariance_and_permutation():
+    rng = np.random.default_rng(10)
+    N = 7
+    R0 = rng.normal(0, 1, (1, N))
+    zero = np.zeros((1, 1, N))  # a zero loss leaves R unchanged and re-solves c
+    _, p1, c1 = oracle.normalhedge(R0, np.full((1, N), 1 / N), zero)
+    for lam in [0.01, 3.0, 250.0]:
+        _, p2, c2 = oracle.normalhedge(lam * R0, np.full((1, N), 1 / N), zero)
+        assert abs(c2[0] - lam ** 2 * c1[0]) < 1e-12 * lam ** 2 * c1[0]
+        assert np.allclose(p2, p1, atol=1e-12)
+    perm = rng.permutation(N)
+    _, p3, c3 = oracle.normalhedge(R0[:, perm], np.full((1, N), 1 / N), zero)
+    assert abs(c3[0] - c1[0]) < 1e-13 * c1[0]
+    assert np.allclose(p3, p1[:, perm], atol=1e-13)
