@@ -1,0 +1,217 @@
+/*
+ * hedgespec.h - C ABI of libhedgespec.so, the MI355X (gfx950) drafter-evaluation
+ * hot path of HedgeSpec (arXiv 2510.20064, "Not-a-Bandit: Provably No-Regret
+ * Drafter Selection in Speculative Decoding for LLMs").
+ *
+ * One verification round of the full-information evaluation phase (Section 3.2):
+ * for B queries, K verified positions (or M draft-tree nodes) and N drafters, the
+ * target's and every drafter's logits become temperature softmaxes; every
+ * (query, drafter, position) gets its acceptance probability and greedy
+ * agreement; every (query, drafter) gets Theorem 3's expected acceptance length
+ * and a loss; per-query Hedge and NormalHedge learners are updated.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless the name ends in _host.
+ *   - Every call is asynchronous: it validates its arguments on the host, then
+ *     enqueues its kernels on `stream` (a hipStream_t; NULL = the null stream)
+ *     and returns without synchronising.
+ *   - The caller owns every buffer and keeps it alive until the stream work has
+ *     completed. The library keeps no pointer after a call returns and
+ *     allocates no memory; scratch space is a caller-provided workspace.
+ *   - Validation is complete and happens before any HIP call: on an error code
+ *     nothing has been enqueued and no output has been touched.
+ *   - Device-side faults surface at the caller's next synchronisation.
+ *   - Calls that share a workspace must not overlap in time (same stream, or
+ *     ordered by events).
+ */
+#ifndef HEDGESPEC_H
+#define HEDGESPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes (every entry point returns one) ---------------------------------------- */
+#define HS_OK 0
+#define HS_ERR_NULL 1        /* a required pointer is NULL                                   */
+#define HS_ERR_SHAPE 2       /* B, N, K, V, L or a stride out of range                       */
+#define HS_ERR_DTYPE 3       /* unknown storage type                                         */
+#define HS_ERR_ALIGN 4       /* a logits row is not 16-byte aligned                          */
+#define HS_ERR_TEMPERATURE 5 /* temperature not finite and > 0 where a softmax is needed     */
+#define HS_ERR_TREE 6        /* invalid parent array, or a loss kind a tree does not support */
+#define HS_ERR_WORKSPACE 7   /* workspace NULL or smaller than the queried size              */
+#define HS_ERR_LIMIT 8       /* a size above the library's limits                            */
+#define HS_ERR_HIP 9         /* the HIP runtime refused a launch                             */
+#define HS_ERR_ARG 10        /* unknown mode or loss kind                                    */
+
+/* ---- limits ------------------------------------------------------------------------------- */
+#define HS_MAX_DRAFTERS 64 /* N: one wave64 lane per drafter in the learner kernel  */
+#define HS_MAX_POSITIONS 64 /* K (chain positions) or M (tree nodes)                */
+#define HS_MAX_QUERIES 65535
+
+/* ---- enumerations ------------------------------------------------------------------------- */
+#define HS_F32 0  /* fp32 logits                            */
+#define HS_BF16 1 /* bf16 logits (upper half of an fp32)    */
+
+#define HS_SAMPLE 0 /* gamma = alpha, speculative sampling at temperature T (Theorem 1)        */
+#define HS_GREEDY 1 /* gamma = argmax agreement, Theorem 1 with one-hot p and q (greedy)       */
+
+#define HS_LOSS_LENGTH 0       /* 1 - EAL/(K_path + 1): chunk length loss (Appendix "Chunk-Level Games") */
+#define HS_LOSS_ACCEPT_TOKEN 1 /* K vectors 1 - gamma_k, in order (Section 3.3, acceptance loss)         */
+#define HS_LOSS_ACCEPT_CHUNK 2 /* (1/K_path) sum_k (1 - gamma_k) (Appendix "Chunk-Level Games")           */
+
+/*
+ * A [B][K][V] logits tensor: element (b, k, v) is at
+ * ptr + (b * stride_b + k * stride_k + v) * element_size. V is contiguous.
+ * Strides are in elements. ptr and every row start must be 16-byte aligned
+ * (strides multiples of 4 for fp32 and of 8 for bf16).
+ */
+typedef struct hs_view {
+  const void* ptr;
+  int64_t stride_b;
+  int64_t stride_k;
+} hs_view;
+
+/*
+ * hs_softmax_stats - statistics of `rows` temperature softmaxes p = softmax(z/T).
+ * The softmax of the target and of every drafter is the first step of Theorem 1
+ * (Section 2.2); the temperature form follows the non-greedy experiments (T = 0.5,
+ * Appendix "Non-greedy results").
+ *   logits     : [rows][ld] of `dtype`, V <= ld, row starts 16-byte aligned.
+ *   row_max    : [rows] max_v z_v (raw logits), or NULL.
+ *   row_lse    : [rows] natural-log normaliser log sum_v exp(z_v / T), or NULL.
+ *   row_argmax : [rows] lowest v with z_v = max (raw logits, so independent of T), or NULL.
+ * Needs T finite and > 0. A row whose entries are all -inf yields lse = NaN.
+ */
+int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t V, int64_t ld,
+                     float temperature, float* row_max, float* row_lse, int32_t* row_argmax,
+                     void* stream);
+
+/* Bytes of device workspace hs_eval_alpha needs for this shape (0 on invalid shapes). */
+size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
+
+/*
+ * hs_eval_alpha - full-information evaluation of N drafters (Section 3.2).
+ * For every query b, position k and drafter i:
+ *   alpha[b][i][k] = sum_v min(p(v), q_i(v)) = 1 - TV(p, q_i)      (Theorem 1)
+ *     with p = softmax(target[b][k] / T), q_i = softmax(drafter_i[b][k] / T),
+ *     accumulated in fp32 and clamped to [0, 1];
+ *   agree[b][i][k]  = 1 if argmax target[b][k] == argmax drafter_i[b][k] else 0;
+ *   argmax_t[b][k], argmax_d[b][i][k] = lowest index of the row maximum (raw logits).
+ * target       : host pointer to one view; drafters_host: host array of N views.
+ * alpha        : [B][N][K] fp32 or NULL. Needs T finite and > 0 when non-NULL.
+ * agree        : [B][N][K] uint8 or NULL.
+ * argmax_t     : [B][K] int32 or NULL; argmax_d: [B][N][K] int32 or NULL.
+ * mode         : HS_SAMPLE or HS_GREEDY. Only selects which outputs are required:
+ *                HS_SAMPLE requires alpha, HS_GREEDY requires agree; any other
+ *                non-NULL output is filled as well.
+ * K            : positions per query (chain) or tree nodes M; 1 <= K <= 64.
+ * workspace    : at least hs_eval_alpha_workspace_size() bytes of device memory,
+ *                256-byte aligned; no initialisation needed.
+ * Each logit is read from HBM once per call. Results are deterministic (fixed
+ * reduction order) for a given shape.
+ */
+int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
+                  int64_t V, int dtype, float temperature, int mode, float* alpha, uint8_t* agree,
+                  int32_t* argmax_t, int32_t* argmax_d, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
+/*
+ * hs_accept_len - Theorem 3's one-step counterfactual acceptance-length
+ * estimator for every (query, drafter), and the learner's loss.
+ * gamma is alpha (HS_SAMPLE; `alpha` [B][N][K] fp32) or the agreement
+ * indicator (HS_GREEDY; `agree` [B][N][K] uint8).
+ * Chains (parent_host = NULL): EAL = sum_{k=1}^{K+1} k (1-gamma_k) prod_{j<k} gamma_j
+ *   = 1 + sum_{k=1}^{K} prod_{j<=k} gamma_j, with gamma_{K+1} = 0.
+ * Trees (parent_host = host int32[K], parent[0] = -1, 0 <= parent[n] < n):
+ *   node n carries the feedback of the token after its prefix (Section 3.2);
+ *   prefix[n] = gamma[n] * prefix[parent[n]] (root: gamma[0]); the path is
+ *   root -> path_end[b]; EAL = 1 + sum of prefix over the path's K_path nodes.
+ * path_end     : [B] int32 device array or NULL (node K-1). An index outside
+ *                [0, K) gives NaN for that query's EAL and loss.
+ * eal          : [B][N] fp64 (required).
+ * prefix       : [B][N][K] fp64 or NULL.
+ * loss         : [L][B][N] fp64 or NULL; L = K for HS_LOSS_ACCEPT_TOKEN (chains
+ *                only), else L = 1. See HS_LOSS_* for the definitions.
+ */
+int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
+                  const int32_t* parent_host, const int32_t* path_end, double* eal,
+                  double* prefix, int loss_kind, double* loss, void* stream);
+
+/*
+ * hs_hedge_update - Hedge, one learner per query (Appendix "Online Learning with
+ * Delayed Feedback", Hedge remark): for each of the L loss vectors in order,
+ * w_i <- w_i exp(-eta loss_i); Predict returns the normalised weights.
+ * Kept in the log domain: logw_i -= eta * loss_i, re-centred so max_i logw_i = 0,
+ * then w = softmax(logw).
+ * logw : [B][N] fp64 in/out (initialise to 0); w: [B][N] fp64 out.
+ * loss : [L][B][N] fp64, expected in [0, 1] (not checked: device data). L >= 1.
+ */
+int hs_hedge_update(double* logw, double* w, const double* loss, int L, int B, int N, double eta,
+                    void* stream);
+
+/*
+ * hs_normalhedge_update - NormalHedge, one learner per query (Appendix "Variants
+ * of Hedging Algorithmic choice", figure "The workflow of NormalHedge"). For each
+ * of the L loss vectors in order:
+ *   l_A = sum_i p_i l_i;  R_i += l_A - l_i;  r_i = max(R_i, 0);
+ *   c solves (1/N) sum_i exp(r_i^2 / (2c)) = e;
+ *   p_i = (r_i / c) exp(r_i^2 / (2c)) / normaliser.
+ * If every r_i is 0 the equation has no root: p = 1/N and c = 0.
+ * R : [B][N] fp64 in/out (initialise to 0); p: [B][N] fp64 in/out (initialise to 1/N);
+ * c : [B] fp64 out (value of the last update); loss: [L][B][N] fp64.
+ */
+int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, int L, int B,
+                          int N, void* stream);
+
+/*
+ * hs_round - one verification round of the whole path in two launches:
+ * hs_eval_alpha, then one learner kernel that does hs_accept_len's work, the
+ * loss, and the Hedge and NormalHedge updates with that loss. Arguments mean
+ * what they mean in the calls above. Learner state pointers may be NULL to
+ * skip that learner (logw and w together; R, p and c together). eal is
+ * required; alpha/agree as hs_eval_alpha requires them for `mode`.
+ */
+typedef struct hs_round_args {
+  hs_view target;
+  const hs_view* drafters_host; /* host array of N views */
+  int N, B, K;
+  int64_t V;
+  int dtype;
+  float temperature;
+  int mode;
+  float* alpha;
+  uint8_t* agree;
+  int32_t* argmax_t;
+  int32_t* argmax_d;
+  const int32_t* parent_host;
+  const int32_t* path_end;
+  double* eal;
+  double* prefix;
+  int loss_kind;
+  double* loss;
+  double* logw;
+  double* w;
+  double eta;
+  double* R;
+  double* p;
+  double* c;
+  void* workspace;
+  size_t workspace_bytes;
+} hs_round_args;
+
+int hs_round(const hs_round_args* args, void* stream);
+
+/* Name of a status code; the thread's last error message; library version (major*10000+minor*100+patch). */
+const char* hs_status_string(int status);
+const char* hs_last_error(void);
+int hs_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HEDGESPEC_H */

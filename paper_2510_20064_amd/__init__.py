@@ -1,0 +1,320 @@
+"""Python binding of libhedgespec.so, the MI355X drafter-evaluation hot path of HedgeSpec.
+
+Argument marshalling only: every step runs in the library's HIP kernels. PyTorch supplies
+device memory and the current HIP stream. The function names match the C ABI declared in
+include/hedgespec.h (hs_softmax_stats, hs_eval_alpha, hs_accept_len, hs_hedge_update,
+hs_normalhedge_update, hs_round). There is no CPU fallback: if the library is not built,
+loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhedgespec.so")
+
+HS_OK = 0
+HS_F32, HS_BF16 = 0, 1
+SAMPLE, GREEDY = 0, 1
+LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
+MAX_DRAFTERS = 64
+MAX_POSITIONS = 64
+
+
+class HsError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s: %s" % (_status_name(code), msg))
+        self.code = code
+
+
+class hs_view(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_void_p), ("stride_b", ctypes.c_int64),
+                ("stride_k", ctypes.c_int64)]
+
+
+class hs_round_args(ctypes.Structure):
+    _fields_ = [
+        ("target", hs_view), ("drafters_host", ctypes.POINTER(hs_view)),
+        ("N", ctypes.c_int), ("B", ctypes.c_int), ("K", ctypes.c_int), ("V", ctypes.c_int64),
+        ("dtype", ctypes.c_int), ("temperature", ctypes.c_float), ("mode", ctypes.c_int),
+        ("alpha", ctypes.c_void_p), ("agree", ctypes.c_void_p), ("argmax_t", ctypes.c_void_p),
+        ("argmax_d", ctypes.c_void_p), ("parent_host", ctypes.c_void_p),
+        ("path_end", ctypes.c_void_p), ("eal", ctypes.c_void_p), ("prefix", ctypes.c_void_p),
+        ("loss_kind", ctypes.c_int), ("loss", ctypes.c_void_p), ("logw", ctypes.c_void_p),
+        ("w", ctypes.c_void_p), ("eta", ctypes.c_double), ("R", ctypes.c_void_p),
+        ("p", ctypes.c_void_p), ("c", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libhedgespec.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libhedgespec.so is not built (%s); run __graft_entry__.build() or "
+                           "python -m paper_2510_20064_amd.build" % path)
+    lib = ctypes.CDLL(path)
+    P, I, I64, F, D, SZ = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float,
+                           ctypes.c_double, ctypes.c_size_t)
+    VP = ctypes.POINTER(hs_view)
+    lib.hs_softmax_stats.argtypes = [P, I, I64, I64, I64, F, P, P, P, P]
+    lib.hs_eval_alpha_workspace_size.argtypes = [I, I, I, I64, I]
+    lib.hs_eval_alpha_workspace_size.restype = SZ
+    lib.hs_eval_alpha.argtypes = [VP, VP, I, I, I, I64, I, F, I, P, P, P, P, P, SZ, P]
+    lib.hs_accept_len.argtypes = [P, P, I, I, I, I, P, P, P, P, I, P, P]
+    lib.hs_hedge_update.argtypes = [P, P, P, I, I, I, D, P]
+    lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
+    lib.hs_round.argtypes = [ctypes.POINTER(hs_round_args), P]
+    lib.hs_status_string.argtypes = [I]
+    lib.hs_status_string.restype = ctypes.c_char_p
+    lib.hs_last_error.restype = ctypes.c_char_p
+    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_accept_len", "hs_hedge_update",
+                 "hs_normalhedge_update", "hs_round", "hs_version"]:
+        getattr(lib, name).restype = I
+    _lib = lib
+    return lib
+
+
+def _status_name(code: int) -> str:
+    try:
+        return load_library().hs_status_string(code).decode()
+    except Exception:  # pragma: no cover
+        return "status %d" % code
+
+
+def _check(code: int) -> None:
+    if code != HS_OK:
+        raise HsError(code, load_library().hs_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return HS_F32
+    if t.dtype in (torch.bfloat16, torch.uint16, torch.int16):
+        return HS_BF16
+    raise TypeError("logits must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _view(t: torch.Tensor) -> hs_view:
+    if t.dim() != 3 or t.stride(2) != 1:
+        raise ValueError("a logits view must be [B][K][V] with V contiguous")
+    return hs_view(t.data_ptr(), t.stride(0), t.stride(1))
+
+
+# --------------------------------------------------------------------------------------------
+
+def softmax_stats(x: torch.Tensor, V: Optional[int] = None, temperature: float = 1.0,
+                  stream=None):
+    """hs_softmax_stats on a [rows][ld] tensor: returns (row_max f32, row_lse f32, row_argmax i32)."""
+    lib = load_library()
+    rows, ld = x.shape
+    V = ld if V is None else V
+    if x.stride(1) != 1:
+        raise ValueError("rows must be contiguous")
+    mx = torch.empty(rows, dtype=torch.float32, device=x.device)
+    lse = torch.empty(rows, dtype=torch.float32, device=x.device)
+    am = torch.empty(rows, dtype=torch.int32, device=x.device)
+    _check(lib.hs_softmax_stats(_ptr(x), _dtype_code(x), rows, V, x.stride(0), temperature,
+                                _ptr(mx), _ptr(lse), _ptr(am), _stream(stream)))
+    return mx, lse, am
+
+
+def eval_workspace_size(B: int, N: int, K: int, V: int, dtype: int) -> int:
+    return int(load_library().hs_eval_alpha_workspace_size(B, N, K, V, dtype))
+
+
+def alloc_workspace(B: int, N: int, K: int, V: int, dtype: int, device) -> torch.Tensor:
+    n = eval_workspace_size(B, N, K, V, dtype)
+    if n == 0:
+        raise ValueError("invalid shape for the evaluation workspace")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _split_logits(target: torch.Tensor, drafters):
+    """Accept a [N+1][B][K][V] tensor (row 0 target) or (target [B][K][V], drafters list/tensor)."""
+    if drafters is None:
+        return target[0], [target[1 + i] for i in range(target.shape[0] - 1)]
+    if isinstance(drafters, torch.Tensor):
+        return target, [drafters[i] for i in range(drafters.shape[0])]
+    return target, list(drafters)
+
+
+def eval_alpha(target: torch.Tensor, drafters=None, V: Optional[int] = None,
+               temperature: float = 1.0, mode: int = SAMPLE, want_alpha: Optional[bool] = None,
+               want_agree: Optional[bool] = None, want_argmax: bool = False,
+               workspace: Optional[torch.Tensor] = None, out: Optional[dict] = None, stream=None):
+    """hs_eval_alpha. Returns a dict of device tensors: alpha [B][N][K] f32, agree [B][N][K] u8,
+    argmax_t [B][K] i32, argmax_d [B][N][K] i32 (those requested)."""
+    lib = load_library()
+    t, ds = _split_logits(target, drafters)
+    B, K, ld = t.shape
+    N = len(ds)
+    V = ld if V is None else V
+    dt = _dtype_code(t)
+    dev = t.device
+    want_alpha = (mode == SAMPLE) if want_alpha is None else want_alpha
+    want_agree = (mode == GREEDY) if want_agree is None else want_agree
+    o = {} if out is None else out
+    if want_alpha and "alpha" not in o:
+        o["alpha"] = torch.empty((B, N, K), dtype=torch.float32, device=dev)
+    if want_agree and "agree" not in o:
+        o["agree"] = torch.empty((B, N, K), dtype=torch.uint8, device=dev)
+    if want_argmax:
+        o.setdefault("argmax_t", torch.empty((B, K), dtype=torch.int32, device=dev))
+        o.setdefault("argmax_d", torch.empty((B, N, K), dtype=torch.int32, device=dev))
+    if workspace is None:
+        workspace = alloc_workspace(B, N, K, V, dt, dev)
+    tv = _view(t)
+    dv = (hs_view * N)(*[_view(d) for d in ds])
+    _check(lib.hs_eval_alpha(ctypes.byref(tv), dv, N, B, K, V, dt, temperature, mode,
+                             _ptr(o.get("alpha")), _ptr(o.get("agree")), _ptr(o.get("argmax_t")),
+                             _ptr(o.get("argmax_d")), _ptr(workspace), workspace.numel(),
+                             _stream(stream)))
+    return o
+
+
+def _parent_host(parent):
+    if parent is None:
+        return None, None
+    arr = (ctypes.c_int32 * len(parent))(*[int(x) for x in parent])
+    return arr, ctypes.cast(arr, ctypes.c_void_p)
+
+
+def accept_len(gamma: torch.Tensor, mode: int = SAMPLE, parent: Optional[Sequence[int]] = None,
+               path_end: Optional[torch.Tensor] = None, loss_kind: int = LOSS_LENGTH,
+               want_prefix: bool = False, want_loss: bool = True, stream=None):
+    """hs_accept_len. gamma: alpha [B][N][K] f32 (SAMPLE) or agree [B][N][K] u8 (GREEDY)."""
+    lib = load_library()
+    B, N, K = gamma.shape
+    dev = gamma.device
+    eal = torch.empty((B, N), dtype=torch.float64, device=dev)
+    prefix = torch.empty((B, N, K), dtype=torch.float64, device=dev) if want_prefix else None
+    L = K if loss_kind == LOSS_ACCEPT_TOKEN else 1
+    loss = torch.empty((L, B, N), dtype=torch.float64, device=dev) if want_loss else None
+    keep, par = _parent_host(parent)
+    alpha = gamma if mode == SAMPLE else None
+    agree = gamma if mode == GREEDY else None
+    _check(lib.hs_accept_len(_ptr(alpha), _ptr(agree), mode, B, N, K, par, _ptr(path_end),
+                             _ptr(eal), _ptr(prefix), loss_kind, _ptr(loss), _stream(stream)))
+    del keep
+    return {"eal": eal, "prefix": prefix, "loss": loss}
+
+
+def hedge_update(logw: torch.Tensor, w: torch.Tensor, loss: torch.Tensor, eta: float,
+                 stream=None) -> None:
+    """hs_hedge_update in place: logw [B][N] in/out, w [B][N] out, loss [L][B][N]."""
+    L, B, N = loss.shape
+    _check(load_library().hs_hedge_update(_ptr(logw), _ptr(w), _ptr(loss), L, B, N, eta,
+                                          _stream(stream)))
+
+
+def normalhedge_update(R: torch.Tensor, p: torch.Tensor, c: torch.Tensor, loss: torch.Tensor,
+                       stream=None) -> None:
+    """hs_normalhedge_update in place: R, p [B][N] in/out, c [B] out, loss [L][B][N]."""
+    L, B, N = loss.shape
+    _check(load_library().hs_normalhedge_update(_ptr(R), _ptr(p), _ptr(c), _ptr(loss), L, B, N,
+                                                _stream(stream)))
+
+
+class LearnerState:
+    """Device-resident per-query learner state: Hedge (logw, w) and NormalHedge (R, p, c)."""
+
+    def __init__(self, B: int, N: int, device):
+        self.logw = torch.zeros((B, N), dtype=torch.float64, device=device)
+        self.w = torch.full((B, N), 1.0 / N, dtype=torch.float64, device=device)
+        self.R = torch.zeros((B, N), dtype=torch.float64, device=device)
+        self.p = torch.full((B, N), 1.0 / N, dtype=torch.float64, device=device)
+        self.c = torch.zeros((B,), dtype=torch.float64, device=device)
+
+
+class Round:
+    """Pre-marshalled hs_round call: eval + learner kernel for fixed buffers.
+
+    Build once, then call run() per verification round (optionally switching the logits
+    buffer with set_logits) - the ctypes structure is reused, so a call costs only the
+    launches."""
+
+    def __init__(self, target: torch.Tensor, drafters=None, V: Optional[int] = None,
+                 temperature: float = 1.0, mode: int = SAMPLE, loss_kind: int = LOSS_LENGTH,
+                 eta: float = 0.5, parent: Optional[Sequence[int]] = None,
+                 path_end: Optional[torch.Tensor] = None, hedge: bool = True,
+                 normalhedge: bool = True, want_prefix: bool = False, want_argmax: bool = False,
+                 want_loss: bool = True, want_agree: Optional[bool] = None,
+                 state: Optional[LearnerState] = None):
+        self.lib = load_library()
+        t, ds = _split_logits(target, drafters)
+        B, K, ld = t.shape
+        N = len(ds)
+        self.B, self.N, self.K = B, N, K
+        self.V = ld if V is None else V
+        dev = t.device
+        self.dtype = _dtype_code(t)
+        self.mode = mode
+        self.alpha = torch.empty((B, N, K), dtype=torch.float32, device=dev)
+        self.agree = torch.empty((B, N, K), dtype=torch.uint8, device=dev)
+        self.argmax_t = torch.empty((B, K), dtype=torch.int32, device=dev) if want_argmax else None
+        self.argmax_d = (torch.empty((B, N, K), dtype=torch.int32, device=dev)
+                         if want_argmax else None)
+        self.eal = torch.empty((B, N), dtype=torch.float64, device=dev)
+        self.prefix = torch.empty((B, N, K), dtype=torch.float64, device=dev) if want_prefix else None
+        L = K if loss_kind == LOSS_ACCEPT_TOKEN else 1
+        self.loss = torch.empty((L, B, N), dtype=torch.float64, device=dev) if want_loss else None
+        self.state = state if state is not None else LearnerState(B, N, dev)
+        self.workspace = alloc_workspace(B, N, K, self.V, self.dtype, dev)
+        self._par_keep, par = _parent_host(parent)
+        self.path_end = path_end
+        self._views = (hs_view * N)()
+        a = hs_round_args()
+        a.drafters_host = ctypes.cast(self._views, ctypes.POINTER(hs_view))
+        a.N, a.B, a.K, a.V = N, B, K, self.V
+        a.dtype, a.temperature, a.mode = self.dtype, temperature, mode
+        want_agree = (mode == GREEDY) if want_agree is None else want_agree
+        a.alpha = self.alpha.data_ptr() if mode == SAMPLE else None
+        a.agree = self.agree.data_ptr() if want_agree else None
+        a.argmax_t = None if self.argmax_t is None else self.argmax_t.data_ptr()
+        a.argmax_d = None if self.argmax_d is None else self.argmax_d.data_ptr()
+        a.parent_host = par
+        a.path_end = None if path_end is None else path_end.data_ptr()
+        a.eal = self.eal.data_ptr()
+        a.prefix = None if self.prefix is None else self.prefix.data_ptr()
+        a.loss_kind = loss_kind
+        a.loss = None if self.loss is None else self.loss.data_ptr()
+        st = self.state
+        if hedge:
+            a.logw, a.w, a.eta = st.logw.data_ptr(), st.w.data_ptr(), eta
+        if normalhedge:
+            a.R, a.p, a.c = st.R.data_ptr(), st.p.data_ptr(), st.c.data_ptr()
+        a.workspace = self.workspace.data_ptr()
+        a.workspace_bytes = self.workspace.numel()
+        self.args = a
+        self.set_logits(target, drafters)
+
+    def set_logits(self, target: torch.Tensor, drafters=None) -> None:
+        t, ds = _split_logits(target, drafters)
+        if len(ds) != self.N or tuple(t.shape[:2]) != (self.B, self.K):
+            raise ValueError("logits shape changed")
+        self._keep = (t, ds)
+        self.args.target = _view(t)
+        for i, d in enumerate(ds):
+            self._views[i] = _view(d)
+
+    def run(self, stream=None) -> None:
+        _check(self.lib.hs_round(ctypes.byref(self.args), _stream(stream)))

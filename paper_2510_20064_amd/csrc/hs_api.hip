@@ -1,0 +1,342 @@
+// C ABI of libhedgespec: host-side validation, launch geometry, workspace sizing.
+// Every argument is checked before the first HIP call; on an error nothing is enqueued.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "hs_internal.h"
+
+#define HS_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = 0;
+  return HS_OK;
+}
+
+int elem_bytes(int dtype) { return dtype == HS_F32 ? 4 : 2; }
+
+bool make_geom(int B, int N, int K, int64_t V, int dtype, hs::Geom* g) {
+  if (B < 1 || N < 1 || K < 1 || V < 1) return false;
+  if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS || K > HS_MAX_POSITIONS || V > INT32_MAX)
+    return false;
+  if (dtype != HS_F32 && dtype != HS_BF16) return false;
+  const int E = 16 / elem_bytes(dtype);
+  g->B = B;
+  g->N = N;
+  g->K = K;
+  g->R = N + 1;
+  g->G = B * K;
+  g->V = V;
+  g->dtype = dtype;
+  g->nvec = (V + E - 1) / E;
+  const int64_t per = (int64_t)hs::kSliceElems / E;
+  g->S = (int)((g->nvec + per - 1) / per);
+  g->vps = (g->nvec + g->S - 1) / g->S;
+  return true;
+}
+
+int check_shape(int B, int N, int K, int64_t V) {
+  if (B < 1 || N < 1 || K < 1 || V < 1)
+    return fail(HS_ERR_SHAPE, "B, N, K and V must be >= 1 (got B=%d N=%d K=%d V=%lld)", B, N, K,
+                (long long)V);
+  if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS || K > HS_MAX_POSITIONS || V > INT32_MAX)
+    return fail(HS_ERR_LIMIT, "limits: B <= %d, N <= %d, K <= %d, V <= 2^31-1 (got B=%d N=%d K=%d)",
+                HS_MAX_QUERIES, HS_MAX_DRAFTERS, HS_MAX_POSITIONS, B, N, K);
+  return HS_OK;
+}
+
+int check_view(const hs_view* v, int dtype, const char* what) {
+  if (!v || !v->ptr) return fail(HS_ERR_NULL, "%s: NULL view or pointer", what);
+  if (v->stride_b < 0 || v->stride_k < 0) return fail(HS_ERR_SHAPE, "%s: negative stride", what);
+  const int64_t es = elem_bytes(dtype);
+  if (((uintptr_t)v->ptr & 15) != 0 || ((v->stride_b * es) & 15) != 0 ||
+      ((v->stride_k * es) & 15) != 0)
+    return fail(HS_ERR_ALIGN, "%s: rows must start on 16-byte boundaries", what);
+  return HS_OK;
+}
+
+int check_parent(const int32_t* parent, int M) {
+  if (!parent) return HS_OK;
+  if (parent[0] != -1) return fail(HS_ERR_TREE, "parent[0] must be -1 (the root)");
+  for (int n = 1; n < M; ++n)
+    if (parent[n] < 0 || parent[n] >= n)
+      return fail(HS_ERR_TREE, "parent[%d] = %d: a parent must precede its child", n, parent[n]);
+  return HS_OK;
+}
+
+struct EvalReq {
+  const hs_view* target;
+  const hs_view* drafters;
+  int N, B, K;
+  int64_t V;
+  int dtype;
+  float T;
+  int mode;
+  float* alpha;
+  uint8_t* agree;
+  int32_t* argmax_t;
+  int32_t* argmax_d;
+  void* ws;
+  size_t ws_bytes;
+};
+
+int validate_eval(const EvalReq& q, hs::Geom* g, hs::RowTable* rows) {
+  int rc = check_shape(q.B, q.N, q.K, q.V);
+  if (rc) return rc;
+  if (q.dtype != HS_F32 && q.dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
+  if (q.mode != HS_SAMPLE && q.mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", q.mode);
+  if (!q.drafters) return fail(HS_ERR_NULL, "drafters_host is NULL");
+  if ((rc = check_view(q.target, q.dtype, "target"))) return rc;
+  for (int i = 0; i < q.N; ++i) {
+    char what[32];
+    snprintf(what, sizeof(what), "drafter %d", i);
+    if ((rc = check_view(&q.drafters[i], q.dtype, what))) return rc;
+  }
+  if (q.mode == HS_SAMPLE && !q.alpha) return fail(HS_ERR_NULL, "sample mode needs alpha");
+  if (q.mode == HS_GREEDY && !q.agree) return fail(HS_ERR_NULL, "greedy mode needs agree");
+  if (q.alpha && !(isfinite(q.T) && q.T > 0.0f))
+    return fail(HS_ERR_TEMPERATURE, "temperature must be finite and > 0 (got %g)", (double)q.T);
+  make_geom(q.B, q.N, q.K, q.V, q.dtype, g);
+  if ((int64_t)g->G * g->R * g->S >= ((int64_t)1 << 31))
+    return fail(HS_ERR_LIMIT, "too many row slices for one launch");
+  const size_t need = hs::ws_layout(*g).total;
+  if (!q.ws) return fail(HS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (q.ws_bytes < need)
+    return fail(HS_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", q.ws_bytes, need);
+  if (((uintptr_t)q.ws & 255) != 0) return fail(HS_ERR_ALIGN, "workspace must be 256-byte aligned");
+  rows->ptr[0] = q.target->ptr;
+  rows->sb[0] = q.target->stride_b;
+  rows->sk[0] = q.target->stride_k;
+  for (int i = 0; i < q.N; ++i) {
+    rows->ptr[1 + i] = q.drafters[i].ptr;
+    rows->sb[1 + i] = q.drafters[i].stride_b;
+    rows->sk[1 + i] = q.drafters[i].stride_k;
+  }
+  for (int r = q.N + 1; r < hs::kMaxRows; ++r) {
+    rows->ptr[r] = nullptr;
+    rows->sb[r] = rows->sk[r] = 0;
+  }
+  return HS_OK;
+}
+
+int run_eval(const EvalReq& q, const hs::Geom& g, const hs::RowTable& rows, hipStream_t s) {
+  const bool need_sum = q.alpha != nullptr;
+  const bool need_arg = q.agree || q.argmax_t || q.argmax_d;
+  const float c = need_sum ? (float)(1.4426950408889634 / (double)q.T) : 1.0f;
+  int rc = hs::launch_eval(g, rows, c, need_sum, need_arg, q.alpha, q.agree, q.argmax_t,
+                           q.argmax_d, reinterpret_cast<char*>(q.ws), s);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return HS_OK;
+}
+
+struct TailReq {
+  const float* alpha;
+  const uint8_t* agree;
+  int mode, B, N, K;
+  const int32_t* parent;
+  const int32_t* path_end;
+  double* eal;
+  double* prefix;
+  int loss_kind;
+  double* loss;
+};
+
+int validate_tail(const TailReq& q, hs::TailArgs* a) {
+  int rc = check_shape(q.B, q.N, q.K, 1);
+  if (rc) return rc;
+  if (q.mode != HS_SAMPLE && q.mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", q.mode);
+  if (q.mode == HS_SAMPLE && !q.alpha) return fail(HS_ERR_NULL, "sample mode needs alpha");
+  if (q.mode == HS_GREEDY && !q.agree) return fail(HS_ERR_NULL, "greedy mode needs agree");
+  if (!q.eal) return fail(HS_ERR_NULL, "eal is NULL");
+  if (q.loss_kind < HS_LOSS_LENGTH || q.loss_kind > HS_LOSS_ACCEPT_CHUNK)
+    return fail(HS_ERR_ARG, "unknown loss kind %d", q.loss_kind);
+  if ((rc = check_parent(q.parent, q.K))) return rc;
+  if (q.parent && q.loss_kind == HS_LOSS_ACCEPT_TOKEN)
+    return fail(HS_ERR_TREE, "token-level acceptance loss is defined for chains only");
+  memset(a, 0, sizeof(*a));
+  a->alpha = q.alpha;
+  a->agree = q.agree;
+  a->gamma_src = q.mode == HS_SAMPLE ? 1 : 2;
+  a->B = q.B;
+  a->N = q.N;
+  a->M = q.K;
+  a->tree = q.parent != nullptr;
+  for (int n = 0; n < HS_MAX_POSITIONS; ++n) a->parent[n] = (q.parent && n < q.K) ? q.parent[n] : n - 1;
+  a->path_end = q.path_end;
+  a->eal = q.eal;
+  a->prefix = q.prefix;
+  a->loss_kind = q.loss_kind;
+  a->loss_out = q.loss;
+  a->L = q.loss_kind == HS_LOSS_ACCEPT_TOKEN ? q.K : 1;
+  return HS_OK;
+}
+
+}  // namespace
+
+HS_API const char* hs_status_string(int status) {
+  switch (status) {
+    case HS_OK: return "HS_OK";
+    case HS_ERR_NULL: return "HS_ERR_NULL";
+    case HS_ERR_SHAPE: return "HS_ERR_SHAPE";
+    case HS_ERR_DTYPE: return "HS_ERR_DTYPE";
+    case HS_ERR_ALIGN: return "HS_ERR_ALIGN";
+    case HS_ERR_TEMPERATURE: return "HS_ERR_TEMPERATURE";
+    case HS_ERR_TREE: return "HS_ERR_TREE";
+    case HS_ERR_WORKSPACE: return "HS_ERR_WORKSPACE";
+    case HS_ERR_LIMIT: return "HS_ERR_LIMIT";
+    case HS_ERR_HIP: return "HS_ERR_HIP";
+    case HS_ERR_ARG: return "HS_ERR_ARG";
+    default: return "HS_ERR_UNKNOWN";
+  }
+}
+
+HS_API const char* hs_last_error(void) { return g_err; }
+
+HS_API int hs_version(void) { return 100; }
+
+HS_API int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t V, int64_t ld,
+                            float temperature, float* row_max, float* row_lse,
+                            int32_t* row_argmax, void* stream) {
+  if (!logits) return fail(HS_ERR_NULL, "logits is NULL");
+  if (dtype != HS_F32 && dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", dtype);
+  if (rows < 1 || V < 1 || ld < V) return fail(HS_ERR_SHAPE, "need rows >= 1, 1 <= V <= ld");
+  if (rows > INT32_MAX || V > INT32_MAX) return fail(HS_ERR_LIMIT, "rows and V must be < 2^31");
+  if (!(isfinite(temperature) && temperature > 0.0f))
+    return fail(HS_ERR_TEMPERATURE, "temperature must be finite and > 0");
+  const int64_t es = elem_bytes(dtype);
+  if (((uintptr_t)logits & 15) != 0 || ((ld * es) & 15) != 0)
+    return fail(HS_ERR_ALIGN, "rows must start on 16-byte boundaries");
+  if (!row_max && !row_lse && !row_argmax) return ok();
+  const float c = (float)(1.4426950408889634 / (double)temperature);
+  int rc = hs::launch_softmax_stats(logits, dtype, rows, V, ld, c, row_max, row_lse, row_argmax,
+                                    (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
+HS_API size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype) {
+  hs::Geom g;
+  if (!make_geom(B, N, K, V, dtype, &g)) return 0;
+  return hs::ws_layout(g).total;
+}
+
+HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
+                         int64_t V, int dtype, float temperature, int mode, float* alpha,
+                         uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  EvalReq q{target, drafters_host, N, B, K, V, dtype, temperature, mode, alpha, agree, argmax_t,
+            argmax_d, workspace, workspace_bytes};
+  hs::Geom g;
+  hs::RowTable rows;
+  int rc = validate_eval(q, &g, &rows);
+  if (rc) return rc;
+  rc = run_eval(q, g, rows, (hipStream_t)stream);
+  return rc ? rc : ok();
+}
+
+HS_API int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
+                         const int32_t* parent_host, const int32_t* path_end, double* eal,
+                         double* prefix, int loss_kind, double* loss, void* stream) {
+  TailReq q{alpha, agree, mode, B, N, K, parent_host, path_end, eal, prefix, loss_kind, loss};
+  hs::TailArgs a;
+  int rc = validate_tail(q, &a);
+  if (rc) return rc;
+  rc = hs::launch_tail(a, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
+static int learner_common(const double* loss, int L, int B, int N) {
+  if (!loss) return fail(HS_ERR_NULL, "loss is NULL");
+  if (L < 1 || B < 1 || N < 1) return fail(HS_ERR_SHAPE, "L, B and N must be >= 1");
+  if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS)
+    return fail(HS_ERR_LIMIT, "limits: B <= %d, N <= %d", HS_MAX_QUERIES, HS_MAX_DRAFTERS);
+  return HS_OK;
+}
+
+HS_API int hs_hedge_update(double* logw, double* w, const double* loss, int L, int B, int N,
+                           double eta, void* stream) {
+  if (!logw || !w) return fail(HS_ERR_NULL, "logw and w are required");
+  int rc = learner_common(loss, L, B, N);
+  if (rc) return rc;
+  if (!isfinite(eta)) return fail(HS_ERR_ARG, "eta must be finite");
+  hs::TailArgs a;
+  memset(&a, 0, sizeof(a));
+  a.gamma_src = 0;
+  a.B = B;
+  a.N = N;
+  a.M = 1;
+  a.loss_in = loss;
+  a.L = L;
+  a.logw = logw;
+  a.w = w;
+  a.eta = eta;
+  rc = hs::launch_tail(a, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
+HS_API int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, int L,
+                                 int B, int N, void* stream) {
+  if (!R || !p || !c) return fail(HS_ERR_NULL, "R, p and c are required");
+  int rc = learner_common(loss, L, B, N);
+  if (rc) return rc;
+  hs::TailArgs a;
+  memset(&a, 0, sizeof(a));
+  a.gamma_src = 0;
+  a.B = B;
+  a.N = N;
+  a.M = 1;
+  a.loss_in = loss;
+  a.L = L;
+  a.R = R;
+  a.p = p;
+  a.c = c;
+  rc = hs::launch_tail(a, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
+HS_API int hs_round(const hs_round_args* r, void* stream) {
+  if (!r) return fail(HS_ERR_NULL, "args is NULL");
+  EvalReq q{&r->target, r->drafters_host, r->N, r->B, r->K, r->V, r->dtype, r->temperature,
+            r->mode, r->alpha, r->agree, r->argmax_t, r->argmax_d, r->workspace,
+            r->workspace_bytes};
+  hs::Geom g;
+  hs::RowTable rows;
+  int rc = validate_eval(q, &g, &rows);
+  if (rc) return rc;
+  TailReq t{r->alpha, r->agree, r->mode, r->B, r->N, r->K, r->parent_host, r->path_end, r->eal,
+            r->prefix, r->loss_kind, r->loss};
+  hs::TailArgs a;
+  if ((rc = validate_tail(t, &a))) return rc;
+  if ((r->logw == nullptr) != (r->w == nullptr))
+    return fail(HS_ERR_NULL, "logw and w must be given together");
+  if (!((r->R == nullptr) == (r->p == nullptr) && (r->R == nullptr) == (r->c == nullptr)))
+    return fail(HS_ERR_NULL, "R, p and c must be given together");
+  if (r->logw && !isfinite(r->eta)) return fail(HS_ERR_ARG, "eta must be finite");
+  a.logw = r->logw;
+  a.w = r->w;
+  a.eta = r->eta;
+  a.R = r->R;
+  a.p = r->p;
+  a.c = r->c;
+  hipStream_t s = (hipStream_t)stream;
+  if ((rc = run_eval(q, g, rows, s))) return rc;
+  rc = hs::launch_tail(a, s);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}

@@ -1,0 +1,180 @@
+// Internal declarations of libhedgespec: kernel geometry, workspace layout and
+// device helpers shared by the evaluation, statistics and learner kernels.
+// gfx950 (CDNA4): wave64, 256-thread workgroups, 16-byte global loads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hedgespec.h"
+
+namespace hs {
+
+constexpr int kThreads = 256;          // workgroup size of the streaming kernels (4 waves)
+constexpr int kWaves = kThreads / 64;
+constexpr int kSliceElems = 8192;      // max logits of one row handled by one workgroup pass
+constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
+constexpr int kMinsumChunk = 8;        // drafters per min-sum work item
+
+// Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 logits.
+template <int DT>
+struct Vec;
+template <>
+struct Vec<HS_F32> {
+  static constexpr int kElems = 4;
+  static constexpr int kBytes = 4;
+  static constexpr int kU = kSliceElems / (kThreads * kElems);  // vectors per thread per slice
+  __device__ static inline void load(const char* rowp, int64_t vi, int64_t V, float* z) {
+    if ((vi + 1) * kElems <= V) {
+      float4 x = *reinterpret_cast<const float4*>(rowp + vi * 16);
+      z[0] = x.x; z[1] = x.y; z[2] = x.z; z[3] = x.w;
+    } else {
+      const float* p = reinterpret_cast<const float*>(rowp);
+#pragma unroll
+      for (int e = 0; e < kElems; ++e) {
+        int64_t idx = vi * kElems + e;
+        z[e] = idx < V ? p[idx] : -INFINITY;
+      }
+    }
+  }
+};
+template <>
+struct Vec<HS_BF16> {
+  static constexpr int kElems = 8;
+  static constexpr int kBytes = 2;
+  static constexpr int kU = kSliceElems / (kThreads * kElems);
+  __device__ static inline float lo(uint32_t w) { return __uint_as_float(w << 16); }
+  __device__ static inline float hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+  __device__ static inline void load(const char* rowp, int64_t vi, int64_t V, float* z) {
+    if ((vi + 1) * kElems <= V) {
+      uint4 x = *reinterpret_cast<const uint4*>(rowp + vi * 16);
+      z[0] = lo(x.x); z[1] = hi(x.x); z[2] = lo(x.y); z[3] = hi(x.y);
+      z[4] = lo(x.z); z[5] = hi(x.z); z[6] = lo(x.w); z[7] = hi(x.w);
+    } else {
+      const uint16_t* p = reinterpret_cast<const uint16_t*>(rowp);
+#pragma unroll
+      for (int e = 0; e < kElems; ++e) {
+        int64_t idx = vi * kElems + e;
+        z[e] = idx < V ? __uint_as_float((uint32_t)p[idx] << 16) : -INFINITY;
+      }
+    }
+  }
+};
+
+// The R = N + 1 logits rows of a (query, position) group: row 0 target, row 1 + i drafter i.
+struct RowTable {
+  const void* ptr[kMaxRows];
+  int64_t sb[kMaxRows];
+  int64_t sk[kMaxRows];
+};
+
+// Split of a row of V logits into S slices of `vps` 16-byte vectors (balanced; last may be shorter).
+struct Geom {
+  int B, N, K, R, G;  // G = B * K groups
+  int64_t V, nvec, vps;
+  int S;
+  int dtype;
+};
+
+// Statistics of one row slice, in log2 units: offset o = fl(m * c) with c = log2(e)/T and
+// s = sum_v exp2(z_v * c - o); every exponent is formed by one fused multiply-add against the
+// same offset, so slices and threads combine exactly whatever the rounding of o.
+struct SliceStat {
+  float m;   // max of the raw logits
+  int idx;   // lowest index attaining m
+  float o;   // offset
+  float s;   // sum of exp2(z c - o)
+};
+
+// Whole-row statistics: log2 of the normaliser is O + lS (as a double-float hi + lo).
+struct RowStat {
+  float Xhi;  // fl(O + lS)
+  float Xlo;  // (O + lS) - Xhi
+  int idx;    // argmax of the row
+  float m;    // max of the raw logits
+};
+
+// Workspace of hs_eval_alpha (byte offsets, 256-aligned).
+struct WsLayout {
+  size_t slice_stats;  // [G][R][S] SliceStat
+  size_t row_stats;    // [G][R] RowStat
+  size_t parts;        // [G][N][S] float min-sum partials
+  size_t counters;     // [G] p1 done, [G] ready, [G] p2 done, [16] queues
+  size_t total;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline WsLayout ws_layout(const Geom& g) {
+  WsLayout L;
+  size_t off = 0;
+  L.slice_stats = off;
+  off = align256(off + sizeof(SliceStat) * (size_t)g.G * g.R * g.S);
+  L.row_stats = off;
+  off = align256(off + sizeof(RowStat) * (size_t)g.G * g.R);
+  L.parts = off;
+  off = align256(off + sizeof(float) * (size_t)g.G * g.N * g.S);
+  L.counters = off;
+  off = align256(off + sizeof(uint32_t) * ((size_t)g.G * 3 + 64));
+  L.total = off;
+  return L;
+}
+
+// ---- device reductions -------------------------------------------------------------------
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Lexicographic (value descending, index ascending) argmax combine.
+__device__ inline void argmax_combine(float& m, int& idx, float m2, int idx2) {
+  if (m2 > m || (m2 == m && idx2 < idx)) {
+    m = m2;
+    idx = idx2;
+  }
+}
+
+// Combine two (offset, sum) pairs of exp2 sums: sum_a 2^(o_a - o) + sum_b 2^(o_b - o).
+__device__ inline void lse2_combine(float& o, float& s, float o2, float s2) {
+  float on = fmaxf(o, o2);
+  float a = (o == -INFINITY) ? 0.0f : s * __builtin_amdgcn_exp2f(o - on);
+  float b = (o2 == -INFINITY) ? 0.0f : s2 * __builtin_amdgcn_exp2f(o2 - on);
+  o = on;
+  s = a + b;
+}
+
+}  // namespace hs
+
+// Launchers (host side), defined next to their kernels.
+namespace hs {
+int launch_eval(const Geom& g, const RowTable& rows, float c, bool need_sum, bool need_argmax,
+                float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
+                hipStream_t stream);
+int launch_softmax_stats(const void* x, int dtype, int64_t rows, int64_t V, int64_t ld, float c,
+                         float* row_max, float* row_lse, int32_t* row_argmax, hipStream_t stream);
+
+struct TailArgs {
+  const float* alpha;
+  const uint8_t* agree;
+  int gamma_src;  // 0: losses come from loss_in; 1: gamma = alpha; 2: gamma = agree
+  int B, N, M;
+  int tree;
+  int32_t parent[HS_MAX_POSITIONS];
+  const int32_t* path_end;
+  double* eal;
+  double* prefix;
+  int loss_kind;
+  double* loss_out;
+  const double* loss_in;
+  int L;
+  double* logw;
+  double* w;
+  double eta;
+  double* R;
+  double* p;
+  double* c;
+};
+int launch_tail(const TailArgs& a, hipStream_t stream);
+}  // namespace hs

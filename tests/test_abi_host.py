@@ -1,0 +1,140 @@
+"""The C ABI on the host: the library loads, exports every declared symbol, and rejects
+invalid arguments before any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2510_20064_amd as hs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hedgespec.h")
+
+FAKE = 0x100000  # never dereferenced: validation fails before any device access
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hs_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = hs.load_library()
+    names = declared_functions()
+    assert "hs_eval_alpha" in names and "hs_round" in names and len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    lib = hs.load_library()
+    assert lib.hs_status_string(0) == b"HS_OK"
+    assert lib.hs_status_string(6) == b"HS_ERR_TREE"
+    assert lib.hs_status_string(99) == b"HS_ERR_UNKNOWN"
+    assert lib.hs_version() >= 100
+
+
+def test_workspace_size_query():
+    lib = hs.load_library()
+    assert lib.hs_eval_alpha_workspace_size(1, 8, 8, 151936, 1) > 0
+    assert lib.hs_eval_alpha_workspace_size(0, 8, 8, 151936, 1) == 0
+    assert lib.hs_eval_alpha_workspace_size(1, 65, 8, 151936, 1) == 0
+    assert lib.hs_eval_alpha_workspace_size(1, 8, 8, 151936, 7) == 0
+
+
+def _views(n, ptr=FAKE, sb=8 * 151936, sk=151936):
+    return (hs.hs_view * n)(*[hs.hs_view(ptr + 0x1000000 * (i + 1), sb, sk) for i in range(n)])
+
+
+def _eval(lib, **kw):
+    a = dict(target=hs.hs_view(FAKE, 8 * 151936, 151936), N=8, B=1, K=8, V=151936, dtype=1,
+             T=1.0, mode=0, alpha=FAKE, agree=None, argmax_t=None, argmax_d=None, ws=FAKE * 16,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    d = kw.get("drafters", _views(a["N"]))
+    tv = a["target"]
+    return lib.hs_eval_alpha(ctypes.byref(tv) if tv is not None else None, d, a["N"], a["B"],
+                             a["K"], a["V"], a["dtype"], a["T"], a["mode"], a["alpha"], a["agree"],
+                             a["argmax_t"], a["argmax_d"], a["ws"], a["ws_bytes"], None)
+
+
+def test_eval_alpha_validation_codes():
+    lib = hs.load_library()
+    assert _eval(lib, N=0) == 2
+    assert _eval(lib, B=0) == 2
+    assert _eval(lib, N=65, drafters=_views(65)) == 8
+    assert _eval(lib, K=65) == 8
+    assert _eval(lib, dtype=5) == 3
+    assert _eval(lib, mode=3) == 10
+    assert _eval(lib, target=None) == 1
+    assert _eval(lib, alpha=None) == 1  # sample mode needs alpha
+    assert _eval(lib, mode=1, alpha=None, agree=None) == 1
+    assert _eval(lib, T=0.0) == 5
+    assert _eval(lib, T=float("nan")) == 5
+    assert _eval(lib, T=-1.0) == 5
+    assert _eval(lib, target=hs.hs_view(FAKE + 2, 8 * 151936, 151936)) == 4
+    assert _eval(lib, target=hs.hs_view(FAKE, 8 * 151936, 151937)) == 4
+    assert _eval(lib, drafters=_views(8, sk=3)) == 4
+    assert _eval(lib, ws=None) == 7
+    assert _eval(lib, ws_bytes=16) == 7
+    assert _eval(lib, ws=FAKE * 16 + 8) == 4
+    bad = _views(8)
+    bad[3] = hs.hs_view(None, 0, 0)
+    assert _eval(lib, drafters=bad) == 1
+    assert b"drafter 3" in lib.hs_last_error()
+
+
+def test_accept_len_validation_codes():
+    lib = hs.load_library()
+
+    def call(parent=None, mode=0, loss_kind=0, alpha=FAKE, agree=None, eal=FAKE, K=4, N=4):
+        arr = None if parent is None else (ctypes.c_int32 * len(parent))(*parent)
+        return lib.hs_accept_len(alpha, agree, mode, 2, N, K, arr, None, eal, None, loss_kind,
+                                 None, None)
+
+    assert call(parent=[0, 0, 1, 2]) == 6
+    assert call(parent=[-1, 1, 1, 2]) == 6
+    assert call(parent=[-1, 0, 3, 2]) == 6
+    assert call(parent=[-1, 0, 0, 1], loss_kind=1) == 6
+    assert call(loss_kind=7) == 10
+    assert call(eal=None) == 1
+    assert call(mode=1) == 1  # greedy needs agree
+    assert call(N=0) == 2
+    assert call(K=65) == 8
+
+
+def test_learner_validation_codes():
+    lib = hs.load_library()
+    assert lib.hs_hedge_update(None, FAKE, FAKE, 1, 2, 3, 0.5, None) == 1
+    assert lib.hs_hedge_update(FAKE, FAKE, FAKE, 0, 2, 3, 0.5, None) == 2
+    assert lib.hs_hedge_update(FAKE, FAKE, FAKE, 1, 2, 65, 0.5, None) == 8
+    assert lib.hs_hedge_update(FAKE, FAKE, FAKE, 1, 2, 3, float("inf"), None) == 10
+    assert lib.hs_normalhedge_update(FAKE, FAKE, None, FAKE, 1, 2, 3, None) == 1
+    assert lib.hs_normalhedge_update(FAKE, FAKE, FAKE, FAKE, 1, 0, 3, None) == 2
+
+
+def test_softmax_stats_validation_codes():
+    lib = hs.load_library()
+    assert lib.hs_softmax_stats(None, 0, 4, 100, 100, 1.0, FAKE, None, None, None) == 1
+    assert lib.hs_softmax_stats(FAKE, 4, 4, 100, 100, 1.0, FAKE, None, None, None) == 3
+    assert lib.hs_softmax_stats(FAKE, 0, 4, 100, 99, 1.0, FAKE, None, None, None) == 2
+    assert lib.hs_softmax_stats(FAKE, 0, 4, 100, 101, 1.0, FAKE, None, None, None) == 4
+    assert lib.hs_softmax_stats(FAKE, 0, 4, 100, 100, 0.0, FAKE, None, None, None) == 5
+
+
+def test_round_validation_codes():
+    lib = hs.load_library()
+    d = _views(8)
+    a = hs.hs_round_args()
+    a.target = hs.hs_view(FAKE, 8 * 151936, 151936)
+    a.drafters_host = ctypes.cast(d, ctypes.POINTER(hs.hs_view))
+    a.N, a.B, a.K, a.V, a.dtype, a.temperature, a.mode = 8, 1, 8, 151936, 1, 1.0, 0
+    a.alpha, a.eal, a.workspace, a.workspace_bytes = FAKE, FAKE, FAKE * 16, 1 << 30
+    a.logw = FAKE  # w missing
+    assert lib.hs_round(ctypes.byref(a), None) == 1
+    a.w = FAKE
+    a.R = FAKE  # p, c missing
+    assert lib.hs_round(ctypes.byref(a), None) == 1
+    assert lib.hs_round(None, None) == 1

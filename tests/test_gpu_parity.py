@@ -1,0 +1,347 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on the same bytes.
+
+Tolerances: argmax and greedy indicators bit-exact (ties to the lowest index); alpha within
+2e-5 absolute; expected acceptance length within 1e-4 relative; Hedge and NormalHedge
+weights within 1e-5 absolute.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2510_20064_amd as hs
+import synth
+
+pytestmark = pytest.mark.gpu
+
+ALPHA_TOL = 2e-5
+EAL_RTOL = 1e-4
+W_TOL = 1e-5
+
+WL = synth.workloads()
+
+
+def dev_logits(w, x: np.ndarray) -> torch.Tensor:
+    t = torch.from_numpy(x)
+    if w.dtype == synth.BF16:
+        t = t.view(torch.bfloat16)
+    return t.cuda()
+
+
+def note(msg):
+    print("\n[case] " + msg, flush=True)
+
+
+def check_eval(w, x_host, V=None, T=None, mode=None, want_argmax=True, groups=None):
+    """Run hs_eval_alpha on the whole tensor and compare with the oracle on `groups`
+    (list of (b, k); None = all)."""
+    V = w.V if V is None else V
+    T = w.temperature if T is None else T
+    mode = w.mode if mode is None else mode
+    xd = dev_logits(w, x_host)
+    out = hs.eval_alpha(xd, V=V, temperature=T, mode=mode, want_alpha=(mode == hs.SAMPLE),
+                        want_agree=True, want_argmax=want_argmax)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    if groups is None:
+        ref = oracle.evaluate(x_host, V=V, T=T, want_alpha=(mode == hs.SAMPLE))
+        ref_alpha = ref["alpha"].transpose(0, 2, 1)  # [B][K][N] -> [B][N][K]
+        ref_agree = ref["agree"].transpose(0, 2, 1)
+        ref_am = ref["argmax"]
+        if mode == hs.SAMPLE:
+            err = np.abs(got["alpha"] - ref_alpha).max()
+            assert err <= ALPHA_TOL, err
+        assert np.array_equal(got["agree"], ref_agree)
+        if want_argmax:
+            assert np.array_equal(got["argmax_t"], ref_am[:, :, 0])
+            assert np.array_equal(got["argmax_d"], ref_am[:, :, 1:].transpose(0, 2, 1))
+        return got, ref_alpha if mode == hs.SAMPLE else ref_agree
+    sub = np.stack([x_host[:, b, k] for (b, k) in groups], axis=1)  # [R][G][ld]
+    ref = oracle.evaluate(sub, V=V, T=T, want_alpha=(mode == hs.SAMPLE))
+    for gi, (b, k) in enumerate(groups):
+        if mode == hs.SAMPLE:
+            err = np.abs(got["alpha"][b, :, k] - ref["alpha"][gi]).max()
+            assert err <= ALPHA_TOL, (b, k, err)
+        assert np.array_equal(got["agree"][b, :, k], ref["agree"][gi]), (b, k)
+        if want_argmax:
+            assert got["argmax_t"][b, k] == ref["argmax"][gi, 0]
+            assert np.array_equal(got["argmax_d"][b, :, k], ref["argmax"][gi, 1:])
+    return got, ref
+
+
+def run_round_and_check(w, x_host, T=None, mode=None, parent=None, path_end=None, rounds=1,
+                        gen=None):
+    """hs_round over `rounds` rounds (fresh logits from gen(r)) vs the oracle pipeline."""
+    T = w.temperature if T is None else T
+    mode = w.mode if mode is None else mode
+    pe_dev = None if path_end is None else torch.from_numpy(np.asarray(path_end, np.int32)).cuda()
+    xd = dev_logits(w, x_host)
+    rnd = hs.Round(xd, V=w.V, temperature=T, mode=mode, loss_kind=w.loss, eta=w.eta,
+                   parent=parent, path_end=pe_dev, want_prefix=parent is not None)
+    B, N = w.B, w.N
+    w_or = np.full((B, N), 1.0 / N)
+    R_or = np.zeros((B, N))
+    p_or = np.full((B, N), 1.0 / N)
+    for r in range(rounds):
+        if r > 0:
+            x_host = gen(r)
+            xd = dev_logits(w, x_host)
+            rnd.set_logits(xd)
+        rnd.run()
+        ref = oracle.evaluate(x_host, V=w.V, T=T, want_alpha=(mode == hs.SAMPLE))
+        gam = (ref["alpha"] if mode == hs.SAMPLE else ref["agree"].astype(np.float64))
+        gam = gam.transpose(0, 2, 1)  # [B][N][K]
+        acc = oracle.accept_len(gam, parent=parent, path_end=path_end, loss_kind=w.loss,
+                                want_prefix=parent is not None)
+        w_or = oracle.hedge(w_or, acc["loss"], w.eta)
+        R_or, p_or, c_or = oracle.normalhedge(R_or, p_or, acc["loss"])
+        torch.cuda.synchronize()
+        if mode == hs.SAMPLE:
+            assert np.abs(rnd.alpha.cpu().numpy() - gam).max() <= ALPHA_TOL
+        else:
+            assert np.array_equal(rnd.agree.cpu().numpy().astype(np.float64), gam)
+        eal = rnd.eal.cpu().numpy()
+        assert np.all(np.abs(eal - acc["eal"]) <= EAL_RTOL * np.abs(acc["eal"])), r
+        assert np.abs(rnd.state.w.cpu().numpy() - w_or).max() <= W_TOL, r
+        assert np.abs(rnd.state.p.cpu().numpy() - p_or).max() <= W_TOL, r
+        if parent is not None:
+            assert np.allclose(rnd.prefix.cpu().numpy(), acc["prefix"], rtol=1e-4, atol=1e-6)
+    return rnd
+
+
+# ---------------------------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------------------------
+
+def test_tiny_chain_full():
+    w = WL["tiny_chain"]
+    note("tiny_chain B1 N4 K4 V32000 fp32 (full check, token-level acceptance loss)")
+    x = synth.generate(w)
+    check_eval(w, x)
+    run_round_and_check(w, x)
+
+
+def test_qwen3_8b_single_full():
+    w = WL["qwen3_8b_single"]
+    note("qwen3_8b_single B1 N8 K8 V151936 bf16 (full check)")
+    x = synth.generate(w)
+    check_eval(w, x)
+    run_round_and_check(w, x)
+
+
+def test_qwen3_8b_single_rounds():
+    w = WL["qwen3_8b_single"]
+    note("qwen3_8b_single, 6 rounds of fresh logits through hs_round")
+    run_round_and_check(w, synth.generate(w), rounds=6, gen=lambda r: synth.generate(w, round=r))
+
+
+@pytest.mark.parametrize("run", ["T0.7", "greedy"])
+def test_batched_serving_full_size(run):
+    w = WL["batched_serving"]
+    mode = hs.SAMPLE if run == "T0.7" else hs.GREEDY
+    note("batched_serving B64 N8 K6 V128256 bf16 run %s (full check)" % run)
+    x = synth.generate(w)
+    check_eval(w, x, mode=mode)
+    run_round_and_check(w, x, mode=mode)
+
+
+def test_draft_tree_full_size_sampled_queries():
+    w = WL["draft_tree"]
+    note("draft_tree B16 N16 M64 V151936 bf16 (sampled queries, tree EAL)")
+    x = synth.generate(w)
+    par = w.parent()
+    pe = w.path_end()
+    got, _ = check_eval(w, x, groups=[(b, k) for b in (0, 7, 15) for k in range(0, 64, 9)])
+    # tree acceptance length on the GPU's alpha for sampled queries: oracle alpha for those queries
+    xd = dev_logits(w, x)
+    out = hs.eval_alpha(xd, temperature=1.0)
+    pe_dev = torch.from_numpy(pe).cuda()
+    acc = hs.accept_len(out["alpha"], parent=par, path_end=pe_dev, want_prefix=True)
+    torch.cuda.synchronize()
+    for b in (3, 12):
+        sub = x[:, b]  # [R][M][V]
+        ref = oracle.evaluate(sub, T=1.0)
+        gam = ref["alpha"].T[None]  # [1][N][M]
+        ra = oracle.accept_len(gam, parent=par, path_end=pe[b:b + 1], want_prefix=True)
+        eal = acc["eal"][b].cpu().numpy()
+        assert np.all(np.abs(eal - ra["eal"][0]) <= EAL_RTOL * ra["eal"][0])
+        assert np.allclose(acc["prefix"][b].cpu().numpy(), ra["prefix"][0], rtol=1e-4, atol=1e-6)
+
+
+def test_draft_tree_reduced_vocab_full_round():
+    w = synth.variant(WL["draft_tree"], V=3000)
+    note("draft_tree at V=3000: hs_round with parent pointers, all queries")
+    run_round_and_check(w, synth.generate(w), parent=w.parent(), path_end=w.path_end())
+
+
+def test_large_pool_full_size_sampled_queries():
+    w = WL["large_pool_stream"]
+    note("large_pool_stream B32 N64 K8 V151936 bf16, round 0 and 600 (sampled queries)")
+    for r in (0, 600):
+        x = synth.generate(w, round=r)
+        check_eval(w, x, groups=[(b, k) for b in (0, 31) for k in range(8)] + [(13, 5)])
+        del x
+
+
+def test_large_pool_stream_reduced_vocab_1000_rounds():
+    w = synth.variant(WL["large_pool_stream"], V=256)
+    note("large_pool_stream B32 N64 K8 at V=256: 1000 rounds, regime switch at 500")
+    run_round_and_check(w, synth.generate(w), rounds=1000,
+                        gen=lambda r: synth.generate(w, round=r))
+
+
+def test_learner_stream_full_pool_1000_rounds():
+    B, N, rounds = 32, 64, 1000
+    note("Hedge + NormalHedge, B32 N64, 1000 rounds of seeded losses")
+    losses = synth.synthetic_losses(7, rounds, 1, B, N)
+    eta = WL["large_pool_stream"].eta
+    st = hs.LearnerState(B, N, "cuda")
+    w_or = np.full((B, N), 1.0 / N)
+    R_or = np.zeros((B, N))
+    p_or = np.full((B, N), 1.0 / N)
+    ld = torch.from_numpy(losses).cuda()
+    for r in range(rounds):
+        hs.hedge_update(st.logw, st.w, ld[r], eta)
+        hs.normalhedge_update(st.R, st.p, st.c, ld[r])
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        w_or = oracle.hedge(w_or, losses[r], eta)
+        R_or, p_or, c_or = oracle.normalhedge(R_or, p_or, losses[r])
+    assert np.abs(st.w.cpu().numpy() - w_or).max() <= W_TOL
+    assert np.abs(st.p.cpu().numpy() - p_or).max() <= W_TOL
+    assert np.allclose(st.R.cpu().numpy(), R_or, rtol=1e-9, atol=1e-9)
+    c_gpu = st.c.cpu().numpy()
+    assert np.allclose(c_gpu, c_or, rtol=1e-9)
+
+
+# ---------------------------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------------------------
+
+def _custom(B, N, K, V, dtype=synth.F32, ld=None):
+    return synth.Workload(name="edge", B=B, N=N, K=K, V=V, dtype=dtype, sigma_t=2.0, nboost=0,
+                          boost=0.0, scales=[1.0] * N, permute=False, temperature=1.0,
+                          mode=hs.SAMPLE, loss=synth.LOSS_LENGTH, eta=0.5, seed=11, ld=ld)
+
+
+def _bf16_bits(a: np.ndarray) -> np.ndarray:
+    u = np.asarray(a, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_argmax_ties_across_slices_and_workgroups(dtype):
+    note("argmax ties across slice boundaries, dtype %d" % dtype)
+    V = 40000
+    w = _custom(1, 3, 2, V, dtype)
+    rng = np.random.default_rng(0)
+    x = rng.normal(0, 1, (4, 1, 2, V)).astype(np.float32)
+    x[0, 0, 0, [7999, 8000, 39999]] = 9.0      # tie across the slice boundary at 8000
+    x[1, 0, 0, [39999, 20000]] = 9.0
+    x[2, 0, 0, [5, 6]] = 9.0                    # tie inside one vector
+    x[3, 0, 0, [8192]] = 9.0
+    x[:, 0, 1, :] = 0.0                         # all-equal rows: argmax 0
+    xs = _bf16_bits(x) if dtype == synth.BF16 else x
+    got, _ = check_eval(w, xs)
+    assert got["argmax_t"][0, 0] == 7999 and list(got["argmax_d"][0, :, 0]) == [20000, 5, 8192]
+    assert list(got["argmax_d"][0, :, 1]) == [0, 0, 0]
+
+
+def test_disjoint_supports_and_identical_rows():
+    note("-inf masks: disjoint supports give alpha = 0 exactly; identical rows give 1")
+    V = 20000
+    w = _custom(1, 2, 2, V)
+    rng = np.random.default_rng(1)
+    x = rng.normal(0, 2, (3, 1, 2, V)).astype(np.float32)
+    mask = rng.random(V) < 0.5
+    x[0, 0, :, mask] = -np.inf
+    x[1, 0, :, ~mask] = -np.inf
+    x[2] = x[0]
+    got, _ = check_eval(w, x)
+    assert np.all(got["alpha"][0, 0] == 0.0)
+    assert np.all(np.abs(got["alpha"][0, 1] - 1.0) <= 2e-6)
+
+
+@pytest.mark.parametrize("T", [0.05, 20.0])
+def test_extreme_temperatures_and_large_logits(T):
+    note("T=%g, logits up to 1e4" % T)
+    V = 12000
+    w = _custom(2, 3, 3, V, synth.BF16)
+    rng = np.random.default_rng(2)
+    base = rng.normal(0, 1, (2, 3, V)) * (1.0 if T > 1 else 0.3)
+    x = np.stack([base + rng.normal(0, 0.2, base.shape) * s for s in (0, 0.3, 1, 3)])
+    x[:, 1] += 1.0e4  # query 1: large offsets
+    check_eval(w, _bf16_bits(x.astype(np.float32)), T=T)
+
+
+def test_vocab_one_and_ragged_vocab_with_padded_stride():
+    note("V=1 (alpha = 1) and V=1001 with a padded row stride of 1008")
+    w = _custom(2, 2, 3, 1, ld=8)
+    x = np.zeros((3, 2, 3, 8), np.float32)
+    x[..., 0] = np.random.default_rng(3).normal(0, 1, (3, 2, 3))
+    got, _ = check_eval(w, x, V=1)
+    assert np.all(got["alpha"] == 1.0)
+    w2 = _custom(2, 5, 3, 1001, synth.BF16, ld=1008)
+    x2 = synth.generate(w2)
+    check_eval(w2, x2, V=1001)
+
+
+def test_single_drafter_single_position():
+    note("N=1, K=1")
+    w = _custom(3, 1, 1, 5000)
+    x = synth.generate(w)
+    check_eval(w, x)
+    run_round_and_check(w, x)
+
+
+def test_deterministic_rerun_bitwise():
+    note("determinism: 5 reruns bitwise equal")
+    w = synth.variant(WL["qwen3_8b_single"], K=3)
+    xd = dev_logits(w, synth.generate(w))
+    ws = hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, "cuda")
+    first = hs.eval_alpha(xd, workspace=ws)["alpha"].clone()
+    for _ in range(5):
+        again = hs.eval_alpha(xd, workspace=ws)["alpha"]
+        assert torch.equal(first, again)
+
+
+def test_softmax_stats_entry():
+    note("hs_softmax_stats vs oracle")
+    for w in (WL["tiny_chain"], synth.variant(WL["qwen3_8b_single"], K=2)):
+        x = synth.generate(w).reshape(-1, w.V)
+        xd = dev_logits(w, x)
+        for T in (1.0, 0.5):
+            mx, lse, am = hs.softmax_stats(xd, temperature=T)
+            torch.cuda.synchronize()
+            rm, ra, rl = oracle.softmax_stats(x, T=T)
+            assert np.array_equal(am.cpu().numpy(), ra)
+            assert np.array_equal(mx.cpu().numpy().astype(np.float64), rm)
+            assert np.allclose(lse.cpu().numpy(), rl, rtol=2e-6, atol=1e-5)
+
+
+def test_accept_len_loss_kinds_chain():
+    note("hs_accept_len: all three loss kinds on seeded gamma")
+    rng = np.random.default_rng(4)
+    B, N, K = 5, 7, 6
+    gam = rng.random((B, N, K)).astype(np.float32)
+    gd = torch.from_numpy(gam).cuda()
+    for kind in (hs.LOSS_LENGTH, hs.LOSS_ACCEPT_TOKEN, hs.LOSS_ACCEPT_CHUNK):
+        out = hs.accept_len(gd, loss_kind=kind, want_prefix=True)
+        torch.cuda.synchronize()
+        ref = oracle.accept_len(gam.astype(np.float64), loss_kind=kind, want_prefix=True)
+        assert np.allclose(out["eal"].cpu().numpy(), ref["eal"], rtol=1e-12)
+        assert np.allclose(out["loss"].cpu().numpy(), ref["loss"], rtol=1e-12, atol=1e-14)
+        assert np.allclose(out["prefix"].cpu().numpy(), ref["prefix"], rtol=1e-12)
+    # greedy gamma from uint8 agreement indicators
+    agr = (rng.random((B, N, K)) < 0.7).astype(np.uint8)
+    out = hs.accept_len(torch.from_numpy(agr).cuda(), mode=hs.GREEDY)
+    torch.cuda.synchronize()
+    ref = oracle.accept_len(agr.astype(np.float64))
+    assert np.array_equal(out["eal"].cpu().numpy(), ref["eal"])
+    # out-of-range path end -> NaN
+    out = hs.accept_len(gd, path_end=torch.tensor([0, 5, 6, -1, 2], dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    e = out["eal"].cpu().numpy()
+    assert np.isnan(e[2]).all() and np.isnan(e[3]).all() and np.isfinite(e[[0, 1, 4]]).all()
