@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Throughput of the HedgeSpec drafter-evaluation hot path on one MI355X.
+
+A step is one verification round of the whole path on one batch of synthetic logits:
+temperature softmax statistics, alpha = sum min(p, q_i) for every drafter and position,
+Theorem 3's expected acceptance length, the length loss, and the Hedge and NormalHedge
+updates (hs_round: the evaluation kernel, then the learner kernel).
+
+Workload: the Qwen3-8B-shaped single query (B=1 query, N=8 drafters, K=8 positions,
+V=151936, bf16 logits, T=1). Inputs are resident in HBM before timing starts; successive
+steps rotate through >= 512 MB of distinct rounds so that the 256 MB Infinity Cache cannot
+serve them. Steps are captured in a HIP graph (the path is launch-bound at this size).
+
+Prints one JSON line (rank 0). `value` = drafter-positions evaluated per second (B*N*K per
+step). `roofline` prices the evaluation kernel against HBM bandwidth with algorithmic bytes
+(every logit read once); `cpu_baseline` times the float64 oracle on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+ROTATE_BYTES = 512 * 1024 * 1024
+METRIC = "drafter-positions evaluated/sec + achieved HBM GB/s (% of peak), 1 MI355X"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=4800)
+    ap.add_argument("--warmup", type=int, default=480)
+    ap.add_argument("--workload", default="qwen3_8b_single")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X: this build has no multi-GPU path "
+              "(query sharding needs no exchange; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2510_20064_amd as hs
+    import synth
+
+    hs.load_library()
+    w = synth.workloads()[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # ---- inputs: distinct rounds, resident in HBM -----------------------------------------
+    copies = max(1, math.ceil(ROTATE_BYTES / w.input_bytes))
+    if w.input_bytes * copies > 64e9:
+        copies = max(1, int(64e9 // w.input_bytes))
+    bufs = []
+    for r in range(copies):
+        x = synth.generate(w, round=r)
+        t = torch.from_numpy(x)
+        if w.dtype == synth.BF16:
+            t = t.view(torch.bfloat16)
+        bufs.append(t.to(dev))
+    parent = w.parent()
+    path_end = w.path_end()
+    pe_dev = None if path_end is None else torch.from_numpy(path_end).to(dev)
+
+    rounds = []
+    state = hs.LearnerState(w.B, w.N, dev)
+    for r in range(copies):
+        rounds.append(hs.Round(bufs[r], V=w.V, temperature=w.temperature, mode=w.mode,
+                               loss_kind=w.loss, eta=w.eta, parent=parent, path_end=pe_dev,
+                               state=state, want_loss=False))
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.Stream()
+
+    def step_fn(i):
+        rounds[i % copies].run(stream=torch.cuda.current_stream())
+
+    # ---- graphs of the per-copy steps -----------------------------------------------------
+    use_graph = not args.no_graph
+    graphs = {}
+
+    def graph_for(n):
+        if n not in graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                for i in range(n):  # eager pass before capture
+                    step_fn(i)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=stream):
+                for i in range(n):
+                    step_fn(i)
+            torch.cuda.synchronize()
+            graphs[n] = g
+        return graphs[n]
+
+    def run_steps(n):
+        if not use_graph:
+            with torch.cuda.stream(stream):
+                for i in range(n):
+                    step_fn(i)
+            return
+        full, rem = divmod(n, copies)
+        if full:
+            g = graph_for(copies)
+            with torch.cuda.stream(stream):
+                for _ in range(full):
+                    g.replay()
+        if rem:
+            g = graph_for(rem)
+            with torch.cuda.stream(stream):
+                g.replay()
+
+    # ---- warmup + timed region ------------------------------------------------------------
+    run_steps(args.warmup)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    run_steps(args.steps)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = e0.elapsed_time(e1) / args.steps
+    value = w.positions / (ms_step * 1e-3)
+
+    # ---- evaluation kernel alone, live, on the same stream --------------------------------
+    ev_ws = [hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, dev)]
+    outs = [{"alpha": torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=dev)}]
+
+    def eval_fn(i):
+        hs.eval_alpha(bufs[i % copies], V=w.V, temperature=w.temperature, mode=w.mode,
+                      workspace=ev_ws[0], out=outs[0], stream=torch.cuda.current_stream())
+
+    n_eval = copies * max(1, args.steps // (4 * copies))
+    with torch.cuda.stream(stream):
+        for i in range(copies):
+            eval_fn(i)
+    torch.cuda.synchronize()
+    if use_graph:
+        ge = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(ge, stream=stream):
+            for i in range(copies):
+                eval_fn(i)
+        torch.cuda.synchronize()
+    e2 = torch.cuda.Event(enable_timing=True)
+    e3 = torch.cuda.Event(enable_timing=True)
+    e2.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(n_eval // copies):
+            if use_graph:
+                ge.replay()
+            else:
+                for i in range(copies):
+                    eval_fn(i)
+    e3.record(stream)
+    torch.cuda.synchronize()
+    eval_us = e2.elapsed_time(e3) * 1e3 / n_eval
+    achieved = w.input_bytes / (eval_us * 1e-6) / 1e9
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    # ---- float64 oracle on the host (bounded sample of the same workload) -----------------
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+
+        xs = [synth.generate(w, round=r) for r in range(min(copies, 4))]
+        par = parent
+        wo = np.full((w.B, w.N), 1.0 / w.N)
+        Ro = np.zeros((w.B, w.N))
+        po = np.full((w.B, w.N), 1.0 / w.N)
+        t1 = time.perf_counter()
+        n_done = 0
+        while True:
+            x = xs[n_done % len(xs)]
+            ref = oracle.evaluate(x, V=w.V, T=w.temperature)
+            gam = ref["alpha"].transpose(0, 2, 1)
+            acc = oracle.accept_len(gam, parent=par, path_end=path_end, loss_kind=w.loss)
+            wo = oracle.hedge(wo, acc["loss"], w.eta)
+            Ro, po, _ = oracle.normalhedge(Ro, po, acc["loss"])
+            n_done += 1
+            el = time.perf_counter() - t1
+            if el >= args.cpu_seconds:
+                break
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        threads = min(threads, os.cpu_count() or threads)
+        cpu = {"value": w.positions * n_done / el, "unit": "drafter-positions/s",
+               "cores": threads, "kind": "oracle",
+               "sample": "%d full rounds of the same workload (all %d positions each), "
+                         "float64 C oracle with OpenMP over rows, %.1f s" % (n_done, w.positions, el)}
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "drafter-positions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "N": w.N, "K": w.K, "V": w.V,
+                   "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
+                   "temperature": w.temperature, "loss": "length",
+                   "learners": "hedge+normalhedge", "rotation_copies": copies,
+                   "input_bytes_per_step": w.input_bytes, "hip_graph": use_graph,
+                   "wall_s": round(wall, 4)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "evaluation (hs_eval_alpha)", "kernel_us": eval_us,
+                     "algorithmic_bytes_per_launch": w.input_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

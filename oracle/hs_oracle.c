@@ -283,7 +283,7 @@ static double nh_g(const double* r, int N, double c) {
  * "The workflow of NormalHedge"), one learner per query, for each of the L loss
  * vectors in order:
  *   l_A = sum_i p_i l_i
- *   R_i <- R_i + (l_A - l_i)
+ *   R_i <- R_i + (l_A - l_i)      (evaluated as sum_j p_j (l_j - l_i), see below)
  *   find c > 0 with (1/N) sum_i exp([R_i]_+^2 / (2c)) = e
  *   p_i <- ([R_i]_+ / c) exp([R_i]_+^2 / (2c)), normalised.
  * The left side decreases strictly in c; with M = max_i [R_i]_+^2 it is <= e at
@@ -295,17 +295,22 @@ static double nh_g(const double* r, int N, double c) {
 void or_normalhedge(double* R, double* p, double* c, const double* loss, int L, int B, int N) {
   const double E = exp(1.0);
   double* r = (double*)malloc(sizeof(double) * (size_t)N);
+  double* dR = (double*)malloc(sizeof(double) * (size_t)N);
   for (int b = 0; b < B; ++b) {
     double* Rb = R + (size_t)b * N;
     double* pb = p + (size_t)b * N;
     double cb = 0.0;
     for (int l = 0; l < L; ++l) {
       const double* lb = loss + ((size_t)l * B + b) * N;
-      double la = 0.0;
-      for (int i = 0; i < N; ++i) la += pb[i] * lb[i];
+      /* l_A - l_i evaluated as sum_j p_j (l_j - l_i): the same quantity because the p_j sum
+         to 1, and exactly 0 whenever every drafter in the support of p has drafter i's loss,
+         so ties cannot create spurious regrets out of rounding. */
       double M = 0.0;
+      for (int i = 0; i < N; ++i) dR[i] = 0.0;
+      for (int i = 0; i < N; ++i)
+        for (int j = 0; j < N; ++j) dR[i] += pb[j] * (lb[j] - lb[i]);
       for (int i = 0; i < N; ++i) {
-        Rb[i] = Rb[i] + (la - lb[i]);
+        Rb[i] = Rb[i] + dR[i];
         r[i] = Rb[i] > 0.0 ? Rb[i] : 0.0;
         if (r[i] * r[i] > M) M = r[i] * r[i];
       }
@@ -334,6 +339,7 @@ void or_normalhedge(double* R, double* p, double* c, const double* loss, int L, 
     c[b] = cb;
   }
   free(r);
+  free(dR);
 }
 
 /* Residual (1/N) sum exp(r^2/2c) - e for a given regret row; exposed for the pins. */

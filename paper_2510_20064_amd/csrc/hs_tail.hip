@@ -8,7 +8,8 @@
 //                  sum_{k=1}^{K+1} k (1 - gamma_k) prod_{j<k} gamma_j with gamma_{K+1} = 0
 //   loss         : length, token-level acceptance, or chunk acceptance (HS_LOSS_*)
 //   Hedge        : logw -= eta * loss per vector, w = softmax(logw)
-//   NormalHedge  : regret update, scale c from (1/N) sum exp(r^2 / 2c) = e, p ~ (r/c) exp(r^2/2c)
+//   NormalHedge  : regret update R_i += l_A - l_i, scale c from (1/N) sum exp(r^2 / 2c) = e,
+//                  p ~ (r/c) exp(r^2/2c)
 #include <math.h>
 
 #include "hs_internal.h"
@@ -138,8 +139,11 @@ __global__ __launch_bounds__(64) void hs_tail_kernel(TailArgs a) {
     double cc = 0.0;
     for (int l = 0; l < L; ++l) {
       const double li = loss_at(l);
-      const double la = wsum(act ? pv * li : 0.0);
-      if (act) Rv += la - li;
+      // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
+      // zero when every drafter that carries weight has this drafter's loss
+      double dR = 0.0;
+      for (int j = 0; j < a.N; ++j) dR += __shfl(pv, j, 64) * (__shfl(li, j, 64) - li);
+      if (act) Rv += dR;
       const double r = (act && Rv > 0.0) ? Rv : 0.0;
       const double M2 = wmax(r * r);
       if (!(M2 > 0.0)) {

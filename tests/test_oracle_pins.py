@@ -367,3 +367,19 @@ def test_normalhedge_scale_covariance_and_permutation():
     _, p3, c3 = oracle.normalhedge(R0[:, perm], np.full((1, N), 1 / N), zero)
     assert abs(c3[0] - c1[0]) < 1e-13 * c1[0]
     assert np.allclose(p3, p1[:, perm], atol=1e-13)
+
+
+def test_normalhedge_equal_losses_leave_regrets_exactly_unchanged():
+    # l_A = sum_i p_i l = l when every loss is equal: regrets must not move at all,
+    # whatever p is (no spurious positive regret from rounding)
+    rng = np.random.default_rng(11)
+    N = 8
+    p0 = rng.random((1, N))
+    p0 /= p0.sum()
+    for val in [0.1, 1 / 3, 0.7, 5 / 9]:
+        R, p, c = oracle.normalhedge(np.zeros((1, N)), p0, np.full((1, 1, N), val))
+        assert np.all(R == 0.0) and c[0] == 0.0 and np.allclose(p, 1 / N)
+    # ties among the drafters that carry weight: the tied drafters' regret is exactly 0
+    p1 = np.array([[0.5, 0.5, 0.0, 0.0]])
+    R, _, _ = oracle.normalhedge(np.zeros((1, 4)), p1, np.array([[[1 / 3, 1 / 3, 0.9, 0.1]]]))
+    assert R[0, 0] == 0.0 and R[0, 1] == 0.0 and R[0, 2] < 0 < R[0, 3]
