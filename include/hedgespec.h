@@ -110,7 +110,11 @@ size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
  *                non-NULL output is filled as well.
  * K            : positions per query (chain) or tree nodes M; 1 <= K <= 64.
  * workspace    : at least hs_eval_alpha_workspace_size() bytes of device memory,
- *                256-byte aligned; no initialisation needed.
+ *                256-byte aligned, ZERO-FILLED before its first use (e.g. hipMemset).
+ *                Every call that runs to completion leaves it zero-filled again, so it
+ *                can be reused for any shape without clearing. After a device fault,
+ *                zero it again. A non-zero workspace does not hang the kernel (every
+ *                wait is bounded) but gives NaN / -2 results.
  * Each logit is read from HBM once per call. Results are deterministic (fixed
  * reduction order) for a given shape.
  */
@@ -162,15 +166,18 @@ int hs_hedge_update(double* logw, double* w, const double* loss, int L, int B, i
  *   p_i = (r_i / c) exp(r_i^2 / (2c)) / normaliser.
  * If every r_i is 0 the equation has no root: p = 1/N and c = 0.
  * R : [B][N] fp64 in/out (initialise to 0); p: [B][N] fp64 in/out (initialise to 1/N);
- * c : [B] fp64 out (value of the last update); loss: [L][B][N] fp64.
+ * c : [B] fp64 in/out: on entry only a starting point for the search of c (any value
+ *     works; the previous call's output makes it fastest), on exit the value of the
+ *     last update; loss: [L][B][N] fp64.
  */
 int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, int L, int B,
                           int N, void* stream);
 
 /*
- * hs_round - one verification round of the whole path in two launches:
- * hs_eval_alpha, then one learner kernel that does hs_accept_len's work, the
- * loss, and the Hedge and NormalHedge updates with that loss. Arguments mean
+ * hs_round - one verification round of the whole path in ONE launch: the work of
+ * hs_eval_alpha, then, per query as soon as its K positions are evaluated,
+ * hs_accept_len's work, the loss, and the Hedge and NormalHedge updates with that
+ * loss (same workspace contract as hs_eval_alpha). Arguments mean
  * what they mean in the calls above. Learner state pointers may be NULL to
  * skip that learner (logw and w together; R, p and c together). eal is
  * required; alpha/agree as hs_eval_alpha requires them for `mode`.

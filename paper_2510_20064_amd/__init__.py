@@ -145,7 +145,8 @@ def alloc_workspace(B: int, N: int, K: int, V: int, dtype: int, device) -> torch
     n = eval_workspace_size(B, N, K, V, dtype)
     if n == 0:
         raise ValueError("invalid shape for the evaluation workspace")
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    # zero-filled once; every completed call leaves it zero-filled again
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def _split_logits(target: torch.Tensor, drafters):

@@ -9,11 +9,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhedgespec.so")
-SOURCES = ["hs_api.hip", "hs_eval.hip", "hs_tail.hip"]
+SOURCES = ["hs_api.hip", "hs_stats.hip", "hs_fused.hip", "hs_tail.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden",
+    # no implicit multiply-add contraction: softmax offsets must be the rounded products the
+    # exp2 sums were taken against; every intended fusion is an explicit fmaf
+    "-ffp-contract=off",
     # no packed fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",

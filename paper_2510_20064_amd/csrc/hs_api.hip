@@ -132,12 +132,13 @@ int validate_eval(const EvalReq& q, hs::Geom* g, hs::RowTable* rows) {
   return HS_OK;
 }
 
-int run_eval(const EvalReq& q, const hs::Geom& g, const hs::RowTable& rows, hipStream_t s) {
+int run_eval(const EvalReq& q, const hs::Geom& g, const hs::RowTable& rows,
+             const hs::TailArgs* tail, hipStream_t s) {
   const bool need_sum = q.alpha != nullptr;
   const bool need_arg = q.agree || q.argmax_t || q.argmax_d;
   const float c = need_sum ? (float)(1.4426950408889634 / (double)q.T) : 1.0f;
-  int rc = hs::launch_eval(g, rows, c, need_sum, need_arg, q.alpha, q.agree, q.argmax_t,
-                           q.argmax_d, reinterpret_cast<char*>(q.ws), s);
+  int rc = hs::launch_round(g, rows, c, need_sum, need_arg, q.alpha, q.agree, q.argmax_t,
+                            q.argmax_d, reinterpret_cast<char*>(q.ws), tail, s);
   if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
   return HS_OK;
 }
@@ -243,7 +244,7 @@ HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, in
   hs::RowTable rows;
   int rc = validate_eval(q, &g, &rows);
   if (rc) return rc;
-  rc = run_eval(q, g, rows, (hipStream_t)stream);
+  rc = run_eval(q, g, rows, nullptr, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 
@@ -334,9 +335,6 @@ HS_API int hs_round(const hs_round_args* r, void* stream) {
   a.R = r->R;
   a.p = r->p;
   a.c = r->c;
-  hipStream_t s = (hipStream_t)stream;
-  if ((rc = run_eval(q, g, rows, s))) return rc;
-  rc = hs::launch_tail(a, s);
-  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  if ((rc = run_eval(q, g, rows, &a, (hipStream_t)stream))) return rc;
   return ok();
 }

@@ -24,6 +24,20 @@ struct Vec<HS_F32> {
   static constexpr int kElems = 4;
   static constexpr int kBytes = 4;
   static constexpr int kU = kSliceElems / (kThreads * kElems);  // vectors per thread per slice
+  using Raw = float4;
+  // raw 16-byte vector vi of a row (logits at or beyond V read as -inf)
+  __device__ static inline Raw load_raw(const char* rowp, int64_t vi, int64_t V) {
+    if ((vi + 1) * kElems <= V) return *reinterpret_cast<const float4*>(rowp + vi * 16);
+    const float* p = reinterpret_cast<const float*>(rowp);
+    float z[kElems];
+#pragma unroll
+    for (int e = 0; e < kElems; ++e) z[e] = vi * kElems + e < V ? p[vi * kElems + e] : -INFINITY;
+    return make_float4(z[0], z[1], z[2], z[3]);
+  }
+  __device__ static inline Raw zero_raw() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  __device__ static inline void unpack(const Raw& x, float* z) {
+    z[0] = x.x; z[1] = x.y; z[2] = x.z; z[3] = x.w;
+  }
   __device__ static inline void load(const char* rowp, int64_t vi, int64_t V, float* z) {
     if ((vi + 1) * kElems <= V) {
       float4 x = *reinterpret_cast<const float4*>(rowp + vi * 16);
@@ -45,6 +59,22 @@ struct Vec<HS_BF16> {
   static constexpr int kU = kSliceElems / (kThreads * kElems);
   __device__ static inline float lo(uint32_t w) { return __uint_as_float(w << 16); }
   __device__ static inline float hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+  using Raw = uint4;
+  // raw 16-byte vector vi of a row (logits beyond V read as -inf, bf16 0xFF80)
+  __device__ static inline Raw load_raw(const char* rowp, int64_t vi, int64_t V) {
+    if ((vi + 1) * kElems <= V) return *reinterpret_cast<const uint4*>(rowp + vi * 16);
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(rowp);
+    uint32_t h[kElems];
+#pragma unroll
+    for (int e = 0; e < kElems; ++e) h[e] = vi * kElems + e < V ? p[vi * kElems + e] : 0xFF80u;
+    return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                      h[6] | (h[7] << 16));
+  }
+  __device__ static inline Raw zero_raw() { return make_uint4(0u, 0u, 0u, 0u); }
+  __device__ static inline void unpack(const Raw& x, float* z) {
+    z[0] = lo(x.x); z[1] = hi(x.x); z[2] = lo(x.y); z[3] = hi(x.y);
+    z[4] = lo(x.z); z[5] = hi(x.z); z[6] = lo(x.w); z[7] = hi(x.w);
+  }
   __device__ static inline void load(const char* rowp, int64_t vi, int64_t V, float* z) {
     if ((vi + 1) * kElems <= V) {
       uint4 x = *reinterpret_cast<const uint4*>(rowp + vi * 16);
@@ -86,20 +116,13 @@ struct SliceStat {
   float s;   // sum of exp2(z c - o)
 };
 
-// Whole-row statistics: log2 of the normaliser is O + lS (as a double-float hi + lo).
-struct RowStat {
-  float Xhi;  // fl(O + lS)
-  float Xlo;  // (O + lS) - Xhi
-  int idx;    // argmax of the row
-  float m;    // max of the raw logits
-};
-
-// Workspace of hs_eval_alpha (byte offsets, 256-aligned).
+// Workspace of the evaluation kernel (byte offsets, 256-aligned). Cross-workgroup data is
+// kept as 64-bit tagged words; see hs_fused.hip.
 struct WsLayout {
-  size_t slice_stats;  // [G][R][S] SliceStat
-  size_t row_stats;    // [G][R] RowStat
-  size_t parts;        // [G][N][S] float min-sum partials
-  size_t counters;     // [G] p1 done, [G] ready, [G] p2 done, [16] queues
+  size_t slice_stats;  // [G][R][S][2] words
+  size_t row_stats;    // [G][R][3] words
+  size_t parts;        // [G][N][S] words
+  size_t counters;     // uint32 counters
   size_t total;
 };
 
@@ -109,13 +132,13 @@ inline WsLayout ws_layout(const Geom& g) {
   WsLayout L;
   size_t off = 0;
   L.slice_stats = off;
-  off = align256(off + sizeof(SliceStat) * (size_t)g.G * g.R * g.S);
+  off = align256(off + 16 * (size_t)g.G * g.R * g.S);
   L.row_stats = off;
-  off = align256(off + sizeof(RowStat) * (size_t)g.G * g.R);
+  off = align256(off + 24 * (size_t)g.G * g.R);
   L.parts = off;
-  off = align256(off + sizeof(float) * (size_t)g.G * g.N * g.S);
+  off = align256(off + 8 * (size_t)g.G * g.N * g.S);
   L.counters = off;
-  off = align256(off + sizeof(uint32_t) * ((size_t)g.G * 3 + 64));
+  off = align256(off + 4 * (16 + (size_t)g.G * (2 + 2 * g.N) + g.B));
   L.total = off;
   return L;
 }
@@ -149,9 +172,6 @@ __device__ inline void lse2_combine(float& o, float& s, float o2, float s2) {
 
 // Launchers (host side), defined next to their kernels.
 namespace hs {
-int launch_eval(const Geom& g, const RowTable& rows, float c, bool need_sum, bool need_argmax,
-                float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
-                hipStream_t stream);
 int launch_softmax_stats(const void* x, int dtype, int64_t rows, int64_t V, int64_t ld, float c,
                          float* row_max, float* row_lse, int32_t* row_argmax, hipStream_t stream);
 
@@ -177,4 +197,8 @@ struct TailArgs {
   double* c;
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
+// One persistent launch: evaluation, and the learner step when tail != nullptr.
+int launch_round(const Geom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,
+                 float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
+                 const TailArgs* tail, hipStream_t stream);
 }  // namespace hs

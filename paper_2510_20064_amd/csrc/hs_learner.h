@@ -1,0 +1,189 @@
+// Per-query learner step, run by one wave64 (lane i = drafter i, N <= 64), all in fp64:
+//   gamma       : alpha (speculative sampling, Theorem 1) or argmax agreement (greedy)
+//   prefix[n]   : gamma[n] * prefix[parent[n]]   (chain: parent[n] = n - 1)
+//   EAL         : 1 + sum of prefix over the path root -> path_end. Summing Theorem 3's
+//                 k (1 - gamma_k) prod_{j<k} gamma_j by parts (gamma_{K+1} = 0) gives this form.
+//   loss        : HS_LOSS_LENGTH 1 - EAL/(K_path + 1); HS_LOSS_ACCEPT_CHUNK mean of
+//                 (1 - gamma) over the path; HS_LOSS_ACCEPT_TOKEN the K vectors 1 - gamma_k
+//   Hedge       : logw -= eta * loss for each vector in order; w = softmax(logw)
+//   NormalHedge : per vector, R_i += l_A - l_i; c solves (1/N) sum exp([R]_+^2 / 2c) = e;
+//                 p_i ~ ([R_i]_+ / c) exp([R_i]_+^2 / 2c)
+// The wave is the only user of the query's state (logw, w, R, p, c) within a launch.
+#pragma once
+
+#include <math.h>
+
+#include "hs_internal.h"
+
+namespace hs {
+
+// Wave64 reductions of doubles on the DPP network (no LDS crossbar round trip): pairs and
+// quads by quad_perm, 8- and 16-lane groups by the half-row and row mirrors, then the four
+// row results are read into scalars. Every lane gets the same value; all 64 lanes must be active.
+template <int CTRL>
+__device__ inline double dpp_d(double x) {
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+__device__ inline double lane_d(double x, int lane) {
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)b, lane);
+  const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+__device__ inline double wsum(double v) {
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);  // row_half_mirror
+  v += dpp_d<0x140>(v);  // row_mirror
+  return (lane_d(v, 0) + lane_d(v, 16)) + (lane_d(v, 32) + lane_d(v, 48));
+}
+__device__ inline double wmax(double v) {
+  v = fmax(v, dpp_d<0xB1>(v));
+  v = fmax(v, dpp_d<0x4E>(v));
+  v = fmax(v, dpp_d<0x141>(v));
+  v = fmax(v, dpp_d<0x140>(v));
+  return fmax(fmax(lane_d(v, 0), lane_d(v, 16)), fmax(lane_d(v, 32), lane_d(v, 48)));
+}
+
+// NormalHedge's scale. With a_i = r_i^2 / 2 and s = 1/c, phi(s) = log((1/N) sum exp(a_i s)) - 1
+// is convex and increasing; its root s* lies in [2/M, 2(1 + ln N)/M], M = max r_i^2 (at the
+// upper end every exponent is <= 1 + ln N, so nothing overflows). Newton's method from any
+// start in the bracket converges (from the left it overshoots once, then descends
+// monotonically: the tangent of a convex function lies below it); a step that leaves the
+// bracket is replaced by bisection. The start is the previous round's scale when it lies in
+// the bracket (regrets move little per round), else the upper end. Returns s*.
+__device__ inline double normalhedge_inv_scale(double a, bool act, int N, double M, double s0) {
+  double lo = 2.0 / M, hi = 2.0 * (1.0 + log((double)N)) / M;
+  double s = (s0 > lo && s0 < hi) ? s0 : hi;
+  for (int it = 0; it < 100; ++it) {
+    const double ex = act ? exp(a * s) : 0.0;
+    const double E = wsum(ex);
+    const double F = wsum(act ? a * ex : 0.0);
+    const double phi = log(E / (double)N) - 1.0;
+    if (phi == 0.0 || !(F > 0.0)) break;
+    if (phi > 0.0) hi = s; else lo = s;
+    double sn = s - phi * E / F;
+    if (!(sn > lo && sn < hi)) sn = 0.5 * (lo + hi);
+    const double ds = fabs(sn - s);
+    s = sn;
+    if (ds <= 4e-16 * s || hi - lo <= 4e-16 * hi) break;
+  }
+  return s;
+}
+
+// LDS doubles tail_query needs.
+__host__ __device__ inline int tail_lds_doubles(const TailArgs& a) {
+  if (a.gamma_src == 0) return 1;
+  const int L = a.loss_kind == HS_LOSS_ACCEPT_TOKEN ? a.M : 1;
+  return a.M * a.N + L * a.N;
+}
+
+// Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
+__device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds) {
+  const int i = threadIdx.x & 63;
+  const int N = a.N, M = a.M;
+  const bool act = i < N;
+  double* gam = lds;            // [M][N]: gamma, then prefix products
+  double* lossv = lds + M * N;  // [L][N]
+  int L = a.L;
+
+  if (a.gamma_src != 0) {
+    const int end = a.path_end ? a.path_end[b] : M - 1;
+    const bool ok = end >= 0 && end < M;
+    double sum1mg = 0.0, eal = NAN;
+    int len = 0;
+    if (act) {
+      for (int n = 0; n < M; ++n) {
+        const int64_t o = ((int64_t)b * N + i) * M + n;
+        gam[n * N + i] = (a.gamma_src == 1) ? (double)a.alpha[o] : (double)a.agree[o];
+      }
+      if (ok)
+        for (int n = end; n >= 0; n = a.tree ? a.parent[n] : n - 1) {
+          sum1mg += 1.0 - gam[n * N + i];
+          ++len;
+        }
+      if (a.loss_kind == HS_LOSS_ACCEPT_TOKEN)
+        for (int n = 0; n < M; ++n) lossv[n * N + i] = 1.0 - gam[n * N + i];
+      // prefix products in node order (a parent precedes its children)
+      for (int n = 0; n < M; ++n) {
+        const int pn = a.tree ? a.parent[n] : n - 1;
+        const double pp = pn >= 0 ? gam[pn * N + i] : 1.0;
+        gam[n * N + i] = gam[n * N + i] * pp;
+      }
+      if (ok) {
+        double sp = 0.0;
+        for (int n = end; n >= 0; n = a.tree ? a.parent[n] : n - 1) sp += gam[n * N + i];
+        eal = 1.0 + sp;
+      }
+      a.eal[(int64_t)b * N + i] = eal;
+      if (a.prefix)
+        for (int n = 0; n < M; ++n) a.prefix[((int64_t)b * N + i) * M + n] = gam[n * N + i];
+      if (a.loss_kind == HS_LOSS_LENGTH)
+        lossv[i] = ok ? 1.0 - eal / (double)(len + 1) : NAN;
+      else if (a.loss_kind == HS_LOSS_ACCEPT_CHUNK)
+        lossv[i] = ok ? sum1mg / (double)len : NAN;
+    }
+    L = (a.loss_kind == HS_LOSS_ACCEPT_TOKEN) ? M : 1;
+    if (a.loss_out && act)
+      for (int l = 0; l < L; ++l) a.loss_out[((int64_t)l * a.B + b) * N + i] = lossv[l * N + i];
+  }
+
+  auto loss_at = [&](int l) -> double {
+    if (!act) return 0.0;
+    if (a.gamma_src != 0) return lossv[l * N + i];
+    return a.loss_in[((int64_t)l * a.B + b) * N + i];
+  };
+
+  // ---- Hedge ----
+  if (a.logw) {
+    double lw = act ? a.logw[(int64_t)b * N + i] : -INFINITY;
+    for (int l = 0; l < L; ++l) lw -= a.eta * loss_at(l);
+    const double mx = wmax(act ? lw : -INFINITY);
+    const double e = act ? exp(lw - mx) : 0.0;
+    const double se = wsum(e);
+    if (act) {
+      a.logw[(int64_t)b * N + i] = lw - mx;
+      a.w[(int64_t)b * N + i] = e / se;
+    }
+  }
+
+  // ---- NormalHedge ----
+  if (a.R) {
+    double Rv = act ? a.R[(int64_t)b * N + i] : 0.0;
+    double pv = act ? a.p[(int64_t)b * N + i] : 0.0;
+    double cc = 0.0;
+    const double c_prev = a.c[b];  // warm start of the scale search
+    for (int l = 0; l < L; ++l) {
+      const double li = loss_at(l);
+      // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
+      // zero when every drafter that carries weight has this drafter's loss
+      double dR = 0.0;
+      for (int j = 0; j < N; ++j) dR += lane_d(pv, j) * (lane_d(li, j) - li);
+      if (act) Rv += dR;
+      const double r = (act && Rv > 0.0) ? Rv : 0.0;
+      const double M2 = wmax(r * r);
+      if (!(M2 > 0.0)) {
+        pv = act ? 1.0 / (double)N : 0.0;
+        cc = 0.0;
+        continue;
+      }
+      const double ai = 0.5 * r * r;
+      const double s = normalhedge_inv_scale(ai, act, N, M2,
+                                             cc > 0.0 ? 1.0 / cc : (c_prev > 0.0 ? 1.0 / c_prev : 0.0));
+      const double u = act ? r * exp(ai * s) : 0.0;
+      const double su = wsum(u);
+      pv = u / su;
+      cc = 1.0 / s;
+    }
+    if (act) {
+      a.R[(int64_t)b * N + i] = Rv;
+      a.p[(int64_t)b * N + i] = pv;
+    }
+    if (i == 0) a.c[b] = cc;
+  }
+}
+
+}  // namespace hs

@@ -302,7 +302,7 @@ def test_vocab_one_and_ragged_vocab_with_padded_stride():
     x = np.zeros((3, 2, 3, 8), np.float32)
     x[..., 0] = np.random.default_rng(3).normal(0, 1, (3, 2, 3))
     got, _ = check_eval(w, x, V=1)
-    assert np.all(got["alpha"] == 1.0)
+    assert np.all(np.abs(got["alpha"] - 1.0) <= 2.4e-7)  # a couple of fp32 ulps
     w2 = _custom(2, 5, 3, 1001, synth.BF16, ld=1008)
     x2 = synth.generate(w2)
     check_eval(w2, x2, V=1001)
