@@ -42,7 +42,7 @@ bool make_geom(int B, int N, int K, int64_t V, int dtype, hs::Geom* g) {
   g->V = V;
   g->dtype = dtype;
   g->nvec = (V + E - 1) / E;
-  const int64_t per = (int64_t)hs::kSliceElems / E;
+  const int64_t per = hs::kSliceVecs;
   g->S = (int)((g->nvec + per - 1) / per);
   g->vps = (g->nvec + g->S - 1) / g->S;
   return true;

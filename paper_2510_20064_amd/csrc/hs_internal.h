@@ -12,7 +12,8 @@ namespace hs {
 
 constexpr int kThreads = 256;          // workgroup size of the streaming kernels (4 waves)
 constexpr int kWaves = kThreads / 64;
-constexpr int kSliceElems = 8192;      // max logits of one row handled by one workgroup pass
+constexpr int kSliceElems = 8192;      // logits per workgroup pass in hs_softmax_stats
+constexpr int kSliceVecs = 1024;       // 16-byte vectors per evaluation slice (partials unit)
 constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
 constexpr int kMinsumChunk = 8;        // drafters per min-sum work item
 
@@ -35,6 +36,9 @@ struct Vec<HS_F32> {
     return make_float4(z[0], z[1], z[2], z[3]);
   }
   __device__ static inline Raw zero_raw() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  __device__ static inline Raw neg_raw() {
+    return make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+  }
   __device__ static inline void unpack(const Raw& x, float* z) {
     z[0] = x.x; z[1] = x.y; z[2] = x.z; z[3] = x.w;
   }
@@ -71,6 +75,9 @@ struct Vec<HS_BF16> {
                       h[6] | (h[7] << 16));
   }
   __device__ static inline Raw zero_raw() { return make_uint4(0u, 0u, 0u, 0u); }
+  __device__ static inline Raw neg_raw() {  // four pairs of bf16 -inf
+    return make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+  }
   __device__ static inline void unpack(const Raw& x, float* z) {
     z[0] = lo(x.x); z[1] = hi(x.x); z[2] = lo(x.y); z[3] = hi(x.y);
     z[4] = lo(x.z); z[5] = hi(x.z); z[6] = lo(x.w); z[7] = hi(x.w);
