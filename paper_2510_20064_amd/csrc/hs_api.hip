@@ -28,26 +28,6 @@ int ok() {
 
 int elem_bytes(int dtype) { return dtype == HS_F32 ? 4 : 2; }
 
-bool make_geom(int B, int N, int K, int64_t V, int dtype, hs::Geom* g) {
-  if (B < 1 || N < 1 || K < 1 || V < 1) return false;
-  if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS || K > HS_MAX_POSITIONS || V > INT32_MAX)
-    return false;
-  if (dtype != HS_F32 && dtype != HS_BF16) return false;
-  const int E = 16 / elem_bytes(dtype);
-  g->B = B;
-  g->N = N;
-  g->K = K;
-  g->R = N + 1;
-  g->G = B * K;
-  g->V = V;
-  g->dtype = dtype;
-  g->nvec = (V + E - 1) / E;
-  const int64_t per = hs::kSliceVecs;
-  g->S = (int)((g->nvec + per - 1) / per);
-  g->vps = (g->nvec + g->S - 1) / g->S;
-  return true;
-}
-
 int check_shape(int B, int N, int K, int64_t V) {
   if (B < 1 || N < 1 || K < 1 || V < 1)
     return fail(HS_ERR_SHAPE, "B, N, K and V must be >= 1 (got B=%d N=%d K=%d V=%lld)", B, N, K,
@@ -93,7 +73,7 @@ struct EvalReq {
   size_t ws_bytes;
 };
 
-int validate_eval(const EvalReq& q, hs::Geom* g, hs::RowTable* rows) {
+int validate_eval(const EvalReq& q, hs::TeamGeom* g, hs::RowTable* rows) {
   int rc = check_shape(q.B, q.N, q.K, q.V);
   if (rc) return rc;
   if (q.dtype != HS_F32 && q.dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
@@ -109,10 +89,10 @@ int validate_eval(const EvalReq& q, hs::Geom* g, hs::RowTable* rows) {
   if (q.mode == HS_GREEDY && !q.agree) return fail(HS_ERR_NULL, "greedy mode needs agree");
   if (q.alpha && !(isfinite(q.T) && q.T > 0.0f))
     return fail(HS_ERR_TEMPERATURE, "temperature must be finite and > 0 (got %g)", (double)q.T);
-  make_geom(q.B, q.N, q.K, q.V, q.dtype, g);
-  if ((int64_t)g->G * g->R * g->S >= ((int64_t)1 << 31))
-    return fail(HS_ERR_LIMIT, "too many row slices for one launch");
-  const size_t need = hs::ws_layout(*g).total;
+  if (!hs::team_geom(q.B, q.N, q.K, q.V, q.dtype, g))
+    return fail(HS_ERR_LIMIT, "V = %lld is beyond the evaluation limit of %lld logits per row",
+                (long long)q.V, (long long)hs::kMaxTeamSlices * hs::kThreads * (16 / elem_bytes(q.dtype)));
+  const size_t need = hs::team_ws(*g).total;
   if (!q.ws) return fail(HS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
   if (q.ws_bytes < need)
     return fail(HS_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", q.ws_bytes, need);
@@ -132,7 +112,17 @@ int validate_eval(const EvalReq& q, hs::Geom* g, hs::RowTable* rows) {
   return HS_OK;
 }
 
-int run_eval(const EvalReq& q, const hs::Geom& g, const hs::RowTable& rows,
+// The one check that asks the device, made after every host-side check: a team of S
+// workgroups must fit on the device at once.
+int check_capacity(const EvalReq& q, const hs::TeamGeom& g) {
+  const int cap = hs::team_capacity(g, q.alpha != nullptr, q.agree || q.argmax_t || q.argmax_d);
+  if (cap < g.S)
+    return fail(HS_ERR_LIMIT, "the device holds %d evaluation workgroups at once, %d are needed",
+                cap, g.S);
+  return HS_OK;
+}
+
+int run_eval(const EvalReq& q, const hs::TeamGeom& g, const hs::RowTable& rows,
              const hs::TailArgs* tail, hipStream_t s) {
   const bool need_sum = q.alpha != nullptr;
   const bool need_arg = q.agree || q.argmax_t || q.argmax_d;
@@ -229,9 +219,9 @@ HS_API int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t
 }
 
 HS_API size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype) {
-  hs::Geom g;
-  if (!make_geom(B, N, K, V, dtype, &g)) return 0;
-  return hs::ws_layout(g).total;
+  hs::TeamGeom g;
+  if (!hs::team_geom(B, N, K, V, dtype, &g)) return 0;
+  return hs::team_ws(g).total;
 }
 
 HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
@@ -240,10 +230,11 @@ HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, in
                          size_t workspace_bytes, void* stream) {
   EvalReq q{target, drafters_host, N, B, K, V, dtype, temperature, mode, alpha, agree, argmax_t,
             argmax_d, workspace, workspace_bytes};
-  hs::Geom g;
+  hs::TeamGeom g;
   hs::RowTable rows;
   int rc = validate_eval(q, &g, &rows);
   if (rc) return rc;
+  if ((rc = check_capacity(q, g))) return rc;
   rc = run_eval(q, g, rows, nullptr, (hipStream_t)stream);
   return rc ? rc : ok();
 }
@@ -316,7 +307,7 @@ HS_API int hs_round(const hs_round_args* r, void* stream) {
   EvalReq q{&r->target, r->drafters_host, r->N, r->B, r->K, r->V, r->dtype, r->temperature,
             r->mode, r->alpha, r->agree, r->argmax_t, r->argmax_d, r->workspace,
             r->workspace_bytes};
-  hs::Geom g;
+  hs::TeamGeom g;
   hs::RowTable rows;
   int rc = validate_eval(q, &g, &rows);
   if (rc) return rc;
@@ -335,6 +326,7 @@ HS_API int hs_round(const hs_round_args* r, void* stream) {
   a.R = r->R;
   a.p = r->p;
   a.c = r->c;
+  if ((rc = check_capacity(q, g))) return rc;
   if ((rc = run_eval(q, g, rows, &a, (hipStream_t)stream))) return rc;
   return ok();
 }

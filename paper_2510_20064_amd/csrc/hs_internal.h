@@ -13,9 +13,9 @@ namespace hs {
 constexpr int kThreads = 256;          // workgroup size of the streaming kernels (4 waves)
 constexpr int kWaves = kThreads / 64;
 constexpr int kSliceElems = 8192;      // logits per workgroup pass in hs_softmax_stats
-constexpr int kSliceVecs = 1024;       // 16-byte vectors per evaluation slice (partials unit)
 constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
-constexpr int kMinsumChunk = 8;        // drafters per min-sum work item
+constexpr int kMaxSetDrafters = 8;     // drafters held on chip with the target by one workgroup
+constexpr int kMaxTeamSlices = 512;    // slices per row (one workgroup each) in one team
 
 // Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 logits.
 template <int DT>
@@ -105,13 +105,43 @@ struct RowTable {
   int64_t sk[kMaxRows];
 };
 
-// Split of a row of V logits into S slices of `vps` 16-byte vectors (balanced; last may be shorter).
-struct Geom {
-  int B, N, K, R, G;  // G = B * K groups
-  int64_t V, nvec, vps;
-  int S;
+// Geometry of the evaluation. A group is one (query, position): the target row and the N
+// drafter rows. Its drafters are split into row sets of up to D (1, 2, 4 or 8), and each row
+// is cut into S slices of kThreads 16-byte vectors. One work item = (row set, slice): the
+// target slice and its row set's drafter slices, held by one workgroup.
+struct TeamGeom {
+  int B, N, K, G;     // G = B * K groups
+  int D, nsub;        // drafters per row set, row sets per group
+  int S;              // slices per row
+  int64_t V, nvec;    // logits and 16-byte vectors per row
   int dtype;
+  int64_t items;      // G * nsub * S
 };
+
+inline int team_set_size(int N) { return N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : kMaxSetDrafters; }
+
+// false if the shape is outside the limits of the evaluation kernel
+inline bool team_geom(int B, int N, int K, int64_t V, int dtype, TeamGeom* g) {
+  if (B < 1 || N < 1 || K < 1 || V < 1) return false;
+  if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS || K > HS_MAX_POSITIONS || V > INT32_MAX)
+    return false;
+  if (dtype != HS_F32 && dtype != HS_BF16) return false;
+  const int E = dtype == HS_F32 ? 4 : 8;
+  g->B = B;
+  g->N = N;
+  g->K = K;
+  g->G = B * K;
+  g->D = team_set_size(N);
+  g->nsub = (N + g->D - 1) / g->D;
+  g->V = V;
+  g->nvec = (V + E - 1) / E;
+  g->dtype = dtype;
+  const int64_t S = (g->nvec + kThreads - 1) / kThreads;
+  if (S > kMaxTeamSlices) return false;
+  g->S = (int)S;
+  g->items = (int64_t)g->G * g->nsub * g->S;
+  return g->items < ((int64_t)1 << 31);
+}
 
 // Statistics of one row slice, in log2 units: offset o = fl(m * c) with c = log2(e)/T and
 // s = sum_v exp2(z_v * c - o); every exponent is formed by one fused multiply-add against the
@@ -123,29 +153,32 @@ struct SliceStat {
   float s;   // sum of exp2(z c - o)
 };
 
-// Workspace of the evaluation kernel (byte offsets, 256-aligned). Cross-workgroup data is
-// kept as 64-bit tagged words; see hs_fused.hip.
-struct WsLayout {
-  size_t slice_stats;  // [G][R][S][2] words
-  size_t row_stats;    // [G][R][3] words
-  size_t parts;        // [G][N][S] words
-  size_t counters;     // uint32 counters
+// Workspace of the evaluation (byte offsets, 256-aligned). Words exchanged between
+// workgroups are 64-bit (value, tag) pairs; the tag is the call's epoch, kept in the
+// workspace and advanced once per call, so words of earlier calls are never mistaken for
+// current ones and nothing has to be cleared.
+struct TeamWs {
+  size_t epoch;  // uint32 call counter at +0, the call's fail flag (a word) at +8
+  size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
+  size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
+  size_t part;   // [G][N][S] floats: per-slice sums of min(p, q_i)
   size_t total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-inline WsLayout ws_layout(const Geom& g) {
-  WsLayout L;
+inline TeamWs team_ws(const TeamGeom& g) {
+  TeamWs L;
+  const size_t sets = (size_t)g.G * g.nsub, rows = (size_t)g.D + 1;
   size_t off = 0;
-  L.slice_stats = off;
-  off = align256(off + 16 * (size_t)g.G * g.R * g.S);
-  L.row_stats = off;
-  off = align256(off + 24 * (size_t)g.G * g.R);
-  L.parts = off;
-  off = align256(off + 8 * (size_t)g.G * g.N * g.S);
-  L.counters = off;
-  off = align256(off + 4 * (16 + (size_t)g.G * (2 + 2 * g.N) + g.B));
+  L.epoch = off;
+  off = align256(off + 16);
+  L.stat = off;
+  off = align256(off + 24 * sets * rows * g.S);
+  L.norm = off;
+  off = align256(off + 24 * sets * rows);
+  L.part = off;
+  off = align256(off + 4 * (size_t)g.G * g.N * g.S);
   L.total = off;
   return L;
 }
@@ -204,8 +237,12 @@ struct TailArgs {
   double* c;
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
-// One persistent launch: evaluation, and the learner step when tail != nullptr.
-int launch_round(const Geom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,
+// Evaluation of one round: the team kernel, then the fold of the per-slice sums into alpha
+// (which also advances the workspace epoch), then the learner step when tail != nullptr.
+int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,
                  float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
                  const TailArgs* tail, hipStream_t stream);
+// Workgroups of the team kernel that one device holds at once for this shape and mode (0 if
+// unknown); the launch needs at least S of them.
+int team_capacity(const TeamGeom& g, bool need_sum, bool need_arg);
 }  // namespace hs

@@ -1,0 +1,105 @@
+// Wave64 building blocks of the evaluation kernels: DPP reductions and the 64-bit words
+// through which workgroups exchange results.
+#pragma once
+
+#include <climits>
+
+#include "hs_internal.h"
+
+namespace hs {
+
+// ---- words shared between workgroups ------------------------------------------------------
+// A word is written once per call with one relaxed 64-bit agent-scope store: the value in the
+// high half, a tag naming the call in the low half. A reader that sees the current tag has
+// the whole value (the store is single-copy atomic), so no fence is needed.
+
+__device__ inline void put_word(uint64_t* w, uint64_t v) {
+  __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t get_word(const uint64_t* w) {
+  return __hip_atomic_load(const_cast<uint64_t*>(w), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t word_of(float x, uint32_t tag) {
+  return ((uint64_t)__float_as_uint(x) << 32) | tag;
+}
+__device__ inline uint64_t word_of(int x, uint32_t tag) {
+  return ((uint64_t)(uint32_t)x << 32) | tag;
+}
+__device__ inline float word_f(uint64_t w) { return __uint_as_float((uint32_t)(w >> 32)); }
+__device__ inline int word_i(uint64_t w) { return (int)(uint32_t)(w >> 32); }
+
+// ---- wave reductions on the DPP network ----------------------------------------------------
+// Pairs and quads by quad_perm, 8- and 16-lane groups by the half-row and row mirrors, then
+// the four row results are combined in a fixed order; every lane gets the same value. All
+// 64 lanes must be active.
+
+template <int CTRL>
+__device__ inline float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ inline int dpp_i(int x) {
+  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, false);
+}
+__device__ inline float lane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+__device__ inline float wave_sum_f(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+
+template <int CTRL>
+__device__ inline void argmax_step(float& m, int& idx) {
+  const float m2 = dpp_f<CTRL>(m);
+  const int i2 = dpp_i<CTRL>(idx);
+  argmax_combine(m, idx, m2, i2);
+}
+// Wave max of m; with NEED_ARG also the lowest index attaining it.
+template <bool NEED_ARG>
+__device__ inline void wave_max(float& m, int& idx) {
+  if (NEED_ARG) {
+    argmax_step<0xB1>(m, idx);
+    argmax_step<0x4E>(m, idx);
+    argmax_step<0x141>(m, idx);
+    argmax_step<0x140>(m, idx);
+    float r = lane_f(m, 0);
+    int ri = __builtin_amdgcn_readlane(idx, 0);
+#pragma unroll
+    for (int l = 16; l < 64; l += 16)
+      argmax_combine(r, ri, lane_f(m, l), __builtin_amdgcn_readlane(idx, l));
+    m = r;
+    idx = ri;
+  } else {
+    m = fmaxf(m, dpp_f<0xB1>(m));
+    m = fmaxf(m, dpp_f<0x4E>(m));
+    m = fmaxf(m, dpp_f<0x141>(m));
+    m = fmaxf(m, dpp_f<0x140>(m));
+    m = fmaxf(fmaxf(lane_f(m, 0), lane_f(m, 16)), fmaxf(lane_f(m, 32), lane_f(m, 48)));
+  }
+}
+
+template <int CTRL>
+__device__ inline void lse_step(float& o, float& s) {
+  const float o2 = dpp_f<CTRL>(o);
+  const float s2 = dpp_f<CTRL>(s);
+  lse2_combine(o, s, o2, s2);
+}
+// Wave combine of (offset, exp2 sum) pairs.
+__device__ inline void wave_lse(float& o, float& s) {
+  lse_step<0xB1>(o, s);
+  lse_step<0x4E>(o, s);
+  lse_step<0x141>(o, s);
+  lse_step<0x140>(o, s);
+  float ro = lane_f(o, 0), rs = lane_f(s, 0);
+#pragma unroll
+  for (int l = 16; l < 64; l += 16) lse2_combine(ro, rs, lane_f(o, l), lane_f(s, l));
+  o = ro;
+  s = rs;
+}
+
+}  // namespace hs
