@@ -4,7 +4,7 @@
 A step is one verification round of the whole path on one batch of synthetic logits:
 temperature softmax statistics, alpha = sum min(p, q_i) for every drafter and position,
 Theorem 3's expected acceptance length, the length loss, and the Hedge and NormalHedge
-updates (hs_round: the evaluation kernel, then the learner kernel).
+updates (hs_round: the evaluation kernel, the fold into alpha, then the learner kernel).
 
 Workload: the Qwen3-8B-shaped single query (B=1 query, N=8 drafters, K=8 positions,
 V=151936, bf16 logits, T=1). Inputs are resident in HBM before timing starts; successive
@@ -12,8 +12,11 @@ steps rotate through >= 512 MB of distinct rounds so that the 256 MB Infinity Ca
 serve them. Steps are captured in a HIP graph (the path is launch-bound at this size).
 
 Prints one JSON line (rank 0). `value` = drafter-positions evaluated per second (B*N*K per
-step). `roofline` prices the evaluation kernel against HBM bandwidth with algorithmic bytes
-(every logit read once); `cpu_baseline` times the float64 oracle on the host.
+step). `roofline` prices one hs_eval_alpha call (the team kernel and the fold of its slice
+sums, timed together with HIP events on the stream they run on) against HBM bandwidth with
+algorithmic bytes (every logit read once); `traffic` is the counter-measured HBM bytes of that
+call from the committed FETCH_SIZE / WRITE_SIZE summary, null if the kernel sources changed
+since it was taken. `cpu_baseline` times the float64 oracle on the host.
 """
 from __future__ import annotations
 
@@ -31,6 +34,36 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 512 * 1024 * 1024
 METRIC = "drafter-positions evaluated/sec + achieved HBM GB/s (% of peak), 1 MI355X"
+# Sources of the evaluation kernels; the counter summary below is valid only for these bytes.
+KERNEL_SOURCES = ["paper_2510_20064_amd/csrc/hs_team.hip", "paper_2510_20064_amd/csrc/hs_wave.h",
+                  "paper_2510_20064_amd/csrc/hs_internal.h"]
+PMC_SUMMARY = "profiles/hs_eval_alpha_qwen3_8b_single_pmc.md"
+
+
+def kernel_source_digest() -> str:
+    import hashlib
+
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per hs_eval_alpha call from the committed FETCH_SIZE / WRITE_SIZE summary,
+    or None when there is none for this workload or the kernel sources changed since."""
+    path = os.path.join(ROOT, PMC_SUMMARY)
+    if workload != "qwen3_8b_single" or not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for ln in f:
+            if ln.startswith("traffic-record: "):
+                rec = json.loads(ln[len("traffic-record: "):])
+    if not rec or rec.get("kernel_sources_sha256") != kernel_source_digest():
+        return None
+    return rec["hbm_bytes_per_call"]
 
 
 def parse():
@@ -227,9 +260,9 @@ def main():
                    "input_bytes_per_step": w.input_bytes, "hip_graph": use_graph,
                    "wall_s": round(wall, 4)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "evaluation (hs_eval_alpha)", "kernel_us": eval_us,
-                     "algorithmic_bytes_per_launch": w.input_bytes},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w.name),
+                     "kernel": "hs_eval_alpha = hs_team_kernel + hs_fold_kernel",
+                     "kernel_us": eval_us, "algorithmic_bytes_per_launch": w.input_bytes},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -18,8 +18,10 @@
  *   - The caller owns every buffer and keeps it alive until the stream work has
  *     completed. The library keeps no pointer after a call returns and
  *     allocates no memory; scratch space is a caller-provided workspace.
- *   - Validation is complete and happens before any HIP call: on an error code
- *     nothing has been enqueued and no output has been touched.
+ *   - Validation is complete and happens before anything is enqueued: on an
+ *     error code nothing has been enqueued and no output has been touched. (The
+ *     one check that asks the device, how many evaluation workgroups it holds at
+ *     once, comes last.)
  *   - Device-side faults surface at the caller's next synchronisation.
  *   - Calls that share a workspace must not overlap in time (same stream, or
  *     ordered by events).
@@ -43,7 +45,7 @@ extern "C" {
 #define HS_ERR_TEMPERATURE 5 /* temperature not finite and > 0 where a softmax is needed     */
 #define HS_ERR_TREE 6        /* invalid parent array, or a loss kind a tree does not support */
 #define HS_ERR_WORKSPACE 7   /* workspace NULL or smaller than the queried size              */
-#define HS_ERR_LIMIT 8       /* a size above the library's limits                            */
+#define HS_ERR_LIMIT 8       /* a size above the library's limits (see below)                */
 #define HS_ERR_HIP 9         /* the HIP runtime refused a launch                             */
 #define HS_ERR_ARG 10        /* unknown mode or loss kind                                    */
 
@@ -51,6 +53,9 @@ extern "C" {
 #define HS_MAX_DRAFTERS 64 /* N: one wave64 lane per drafter in the learner kernel  */
 #define HS_MAX_POSITIONS 64 /* K (chain positions) or M (tree nodes)                */
 #define HS_MAX_QUERIES 65535
+/* V: at most 512 * 256 16-byte vectors per row (1048576 bf16 or 524288 fp32 logits), and
+   the device must hold ceil(V / 2048) (bf16) or ceil(V / 1024) (fp32) evaluation
+   workgroups at once: hs_eval_alpha returns HS_ERR_LIMIT otherwise. */
 
 /* ---- enumerations ------------------------------------------------------------------------- */
 #define HS_F32 0  /* fp32 logits                            */
@@ -111,12 +116,16 @@ size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
  * K            : positions per query (chain) or tree nodes M; 1 <= K <= 64.
  * workspace    : at least hs_eval_alpha_workspace_size() bytes of device memory,
  *                256-byte aligned, ZERO-FILLED before its first use (e.g. hipMemset).
- *                Every call that runs to completion leaves it zero-filled again, so it
- *                can be reused for any shape without clearing. After a device fault,
- *                zero it again. A non-zero workspace does not hang the kernel (every
- *                wait is bounded) but gives NaN / -2 results.
- * Each logit is read from HBM once per call. Results are deterministic (fixed
- * reduction order) for a given shape.
+ *                The library keeps a call counter in it and tags every word it
+ *                exchanges between workgroups with it, so the workspace is reused for
+ *                any shape without clearing. After a device fault or an HS_ERR_HIP
+ *                return, zero it again. Waits inside the kernel are bounded: a
+ *                workspace that was not zero-filled, or a device too busy with other
+ *                work to hold a whole team of workgroups at once, gives NaN alpha and
+ *                -2 argmax values instead of a hang.
+ * Each logit is read from HBM once per call (two launches: the evaluation, then the
+ * fold of per-slice sums into alpha). Results are deterministic (fixed reduction
+ * order) for a given shape.
  */
 int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
                   int64_t V, int dtype, float temperature, int mode, float* alpha, uint8_t* agree,
@@ -174,10 +183,10 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
                           int N, void* stream);
 
 /*
- * hs_round - one verification round of the whole path in ONE launch: the work of
- * hs_eval_alpha, then, per query as soon as its K positions are evaluated,
- * hs_accept_len's work, the loss, and the Hedge and NormalHedge updates with that
- * loss (same workspace contract as hs_eval_alpha). Arguments mean
+ * hs_round - one verification round of the whole path, enqueued as three launches
+ * (evaluation, fold into alpha, learner step): the work of hs_eval_alpha, then per
+ * query hs_accept_len's work, the loss, and the Hedge and NormalHedge updates with
+ * that loss (same workspace contract as hs_eval_alpha). Arguments mean
  * what they mean in the calls above. Learner state pointers may be NULL to
  * skip that learner (logw and w together; R, p and c together). eal is
  * required; alpha/agree as hs_eval_alpha requires them for `mode`.
