@@ -155,12 +155,32 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
   }
 }
 
+// Position of work item `it`: row set, slice, group (b, k), drafters n in the set, and the
+// calling thread's vector index within the row.
+struct ItemPos {
+  int set, s, g, sub, b, k, n;
+  int vi;  // a row holds fewer than 2^31 logits
+};
+__device__ inline ItemPos item_pos(const TeamArgs& A, int it, int D) {
+  ItemPos q;
+  q.set = it / A.S;
+  q.s = it - q.set * A.S;
+  q.g = q.set / A.nsub;
+  q.sub = q.set - q.g * A.nsub;
+  q.b = q.g / A.K;
+  q.k = q.g - q.b * A.K;
+  q.n = min(D, A.N - q.sub * D);
+  q.vi = q.s * kThreads + (int)threadIdx.x;
+  return q;
+}
+
 template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
-__global__ __launch_bounds__(kThreads) void hs_team_kernel(TeamArgs A) {
+__global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   using Vt = Vec<DT>;
   using Raw = typename Vt::Raw;
   constexpr int E = Vt::kElems;
   constexpr int RM = D + 1;
+  constexpr int XR = NEED_SUM ? RM : 1;  // rows of kept e_v
   __shared__ float sh_m[kWaves][RM];
   __shared__ float sh_s[kWaves][RM];
   __shared__ int sh_i[kWaves][RM];
@@ -171,62 +191,60 @@ __global__ __launch_bounds__(kThreads) void hs_team_kernel(TeamArgs A) {
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const uint32_t tag = call_tag(A.epoch);
   const int S = A.S;
+  const int P = gridDim.x;
   Raw nxt[RM];
 
   // Issue the loads of item `it` into nxt: one unconditional 16-byte load per row, from an
   // address clamped into the row's complete vectors (lanes past the row end are masked to -inf
-  // when unpacked), so the loads of all rows are in flight together. The one partial vector
-  // at the end of a row (V not a multiple of the vector width) is then re-read element by
+  // before use), so the loads of all rows are in flight together. The one partial vector at
+  // the end of a row (V not a multiple of the vector width) is then re-read element by
   // element, in a branch taken only by the slice that holds it.
   const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
-  auto fetch = [&](int it) {
-    const int set = it / S, s = it - set * S;
-    const int g = set / A.nsub, sub = set - g * A.nsub;
-    const int b = g / A.K, k = g - b * A.K;
-    const int n = min(D, A.N - sub * D);
-    const int64_t vi = (int64_t)s * kThreads + t;
+  auto fetch = [&](int it) __attribute__((always_inline)) {
+    const ItemPos q = item_pos(A, it, D);
     const char* rp[RM];
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
-      const int row = r == 0 ? 0 : sub * D + min(r, n);
+      const int row = r == 0 ? 0 : q.sub * D + min(r, q.n);
       rp[r] = reinterpret_cast<const char*>(A.rows.ptr[row]) +
-              ((int64_t)b * A.rows.sb[row] + (int64_t)k * A.rows.sk[row]) * Vt::kBytes;
+              ((int64_t)q.b * A.rows.sb[row] + (int64_t)q.k * A.rows.sk[row]) * Vt::kBytes;
     }
     if (vfull > 0) {
-      const int64_t vc = vi < vfull ? vi : vfull - 1;
+      // uniform row base + 32-bit lane offset (a row holds < 2^31 logits)
+      const uint32_t off = (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16);
 #pragma unroll
       for (int r = 0; r < RM; ++r)
-        if (r <= n) nxt[r] = *reinterpret_cast<const Raw*>(rp[r] + vc * 16);
+        if (r <= q.n) nxt[r] = *reinterpret_cast<const Raw*>(rp[r] + off);
     }
-    if (vfull < A.nvec && (int64_t)(s + 1) * kThreads > vfull) {  // this slice holds the tail
+    if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
 #pragma unroll
       for (int r = 0; r < RM; ++r)
-        if (r <= n && vi == vfull) nxt[r] = Vt::load_raw(rp[r], vi, A.V);
+        if (r <= q.n && q.vi == vfull) nxt[r] = Vt::load_raw(rp[r], q.vi, A.V);
     }
   };
 
+  float ex[XR][E];  // e_v of the current item, against the wave's offset of its row
+  float ow[RM];     // that offset (wave-uniform), -inf for a wave with no finite logit
+
   int it = blockIdx.x;
   if (it < A.items) fetch(it);
-  for (; it < A.items; it += gridDim.x) {
-    const int set = it / S, s = it - set * S;
-    const int g = set / A.nsub, sub = set - g * A.nsub;
-    const int b = g / A.K, k = g - b * A.K;
-    const int n = min(D, A.N - sub * D);  // drafters in this row set; rows 0..n
-    const int64_t vi = (int64_t)s * kThreads + t;
-
+  for (; it < A.items; it += P) {
+    const ItemPos q = item_pos(A, it, D);
     HS_STAMP(0);
-    Raw cur[RM];
-#pragma unroll
-    for (int r = 0; r < RM; ++r) cur[r] = nxt[r];
 
     // ---- 1. slice statistics of every row; e_v kept for step 3 ----
-    float ex[NEED_SUM ? RM : 1][E];
-    float ol[RM];  // the lane's offset per row
+    // Per row: the wave's max m_w (and lowest argmax), then e_v = exp2(z_v c - o_w) against
+    // o_w = fl(m_w c), and their wave sum; lane 0 leaves (m_w, sum, argmax) in LDS.
+    if ((int64_t)(q.s + 1) * kThreads > A.nvec) {  // the slice that runs past the row end
+#pragma unroll
+      for (int r = 0; r < RM; ++r)
+        if (q.vi >= A.nvec) nxt[r] = Vt::neg_raw();
+    }
 #pragma unroll
     for (int r = 0; r < RM; ++r) {
-      if (r > n) continue;
+      if (r > q.n) continue;
       float z[E];
-      Vt::unpack(vi < A.nvec ? cur[r] : Vt::neg_raw(), z);
+      Vt::unpack(nxt[r], z);
       float m = -INFINITY;
       int idx = INT_MAX;
 #pragma unroll
@@ -234,56 +252,46 @@ __global__ __launch_bounds__(kThreads) void hs_team_kernel(TeamArgs A) {
         if (NEED_ARG) {
           if (z[e] > m) {
             m = z[e];
-            idx = (int)(vi * E + e);
+            idx = q.vi * E + e;
           }
         } else {
           m = fmaxf(m, z[e]);
         }
       }
       // a lane whose logits are all -inf still owns its lowest valid index
-      if (NEED_ARG && idx == INT_MAX && vi < A.nvec) idx = (int)(vi * E);
-      float o = -INFINITY, sl = 0.0f;
-      if constexpr (NEED_SUM) {
-        if (m != -INFINITY) {
-          o = m * A.c;  // rounded product (no contraction); every reader recomputes it alike
-          float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const float x = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -o));
-            ex[r][e] = x;
-            if (e & 1) a1 += x;
-            else a0 += x;
-          }
-          sl = a0 + a1;
-        } else {
-#pragma unroll
-          for (int e = 0; e < E; ++e) ex[r][e] = 0.0f;
-        }
-      }
-      ol[r] = o;
-      float mw = m;
-      int iw = idx;
-      wave_max<NEED_ARG>(mw, iw);
+      if (NEED_ARG && idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
+      wave_max<NEED_ARG>(m, idx);
       float sw = 0.0f;
-      if (NEED_SUM) {
-        const float ow = mw * A.c;
-        sw = wave_sum_f(m != -INFINITY ? sl * __builtin_amdgcn_exp2f(o - ow) : 0.0f);
+      if constexpr (NEED_SUM) {
+        // rounded product (no contraction), recomputed alike by every reader; a wave with
+        // no finite logit takes offset 0 and gets exp2(-inf) = 0 throughout
+        const float oc = m != -INFINITY ? m * A.c : 0.0f;
+        float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float x = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
+          ex[r][e] = x;
+          if (e & 1) a1 += x;
+          else a0 += x;
+        }
+        sw = wave_sum_f(a0 + a1);
+        // wave-uniform: keep it in a scalar register
+        ow[r] = __int_as_float(
+            __builtin_amdgcn_readfirstlane(__float_as_int(m != -INFINITY ? oc : -INFINITY)));
       }
       if (lane == 0) {
-        sh_m[wv][r] = mw;
+        sh_m[wv][r] = m;
         sh_s[wv][r] = sw;
-        if (NEED_ARG) sh_i[wv][r] = iw;
+        if (NEED_ARG) sh_i[wv][r] = idx;
       }
     }
-
     HS_STAMP(1);
-    // the successor's loads fly during the exchange
-    if (it + (int)gridDim.x < A.items) fetch(it + gridDim.x);
+    if (it + P < A.items) fetch(it + P);  // the successor's loads fly during the exchange
     __syncthreads();
     HS_STAMP(2);
 
     // workgroup statistics of each row, published by lane r of wave 0
-    if (wv == 0 && lane <= n) {
+    if (wv == 0 && lane <= q.n) {
       const int r = lane;
       float m = sh_m[0][r];
       int idx = NEED_ARG ? sh_i[0][r] : 0;
@@ -292,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void hs_team_kernel(TeamArgs A) {
         if (NEED_ARG) argmax_combine(m, idx, sh_m[w][r], sh_i[w][r]);
         else m = fmaxf(m, sh_m[w][r]);
       }
-      uint64_t* wp = A.stat + (((int64_t)set * RM + r) * S + s) * 3;
+      uint64_t* wp = A.stat + (((int64_t)q.set * RM + r) * S + q.s) * 3;
       put_word(wp, word_of(m, tag));
       if (NEED_SUM) {
         const float o = m * A.c;
@@ -310,44 +318,49 @@ __global__ __launch_bounds__(kThreads) void hs_team_kernel(TeamArgs A) {
     HS_STAMP(3);
 
     // ---- 2. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
-    for (int rr = s + wv * S; rr <= n; rr += kWaves * S)
-      fold_row<D, NEED_SUM, NEED_ARG>(A, set, rr, b, k, sub, tag, lane);
+    for (int rr = q.s + wv * S; rr <= q.n; rr += kWaves * S)
+      fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
     HS_STAMP(4);
 
     // ---- 3. normalisers, then the min-sum of every drafter ----
     if constexpr (NEED_SUM) {
-    if (wv == 0 && lane < 2 * (n + 1)) {
-      const int r = lane >> 1;
-      const float x = word_f(await_word(A.norm + ((int64_t)set * RM + r) * 3 + (lane & 1), tag, A.fail));
-      if (lane & 1) sh_lo[r] = x;
-      else sh_hi[r] = x;
-    }
-    HS_STAMP(5);
-    __syncthreads();
-    const float at = (ol[0] - sh_hi[0]) - sh_lo[0];
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      if (d >= n) continue;
-      const int r = d + 1;
-      const float ad = (ol[r] - sh_hi[r]) - sh_lo[r];
-      const float G = __builtin_amdgcn_exp2f(at - ad);
-      const float F = __builtin_amdgcn_exp2f(ad);
-      float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float y = fminf(ex[0][e] * G, ex[r][e]);
-        if (e & 1) a1 += y;
-        else a0 += y;
+      if (wv == 0 && lane < 2 * (q.n + 1)) {
+        const int r = lane >> 1;
+        const float x =
+            word_f(await_word(A.norm + ((int64_t)q.set * RM + r) * 3 + (lane & 1), tag, A.fail));
+        if (lane & 1) sh_lo[r] = x;
+        else sh_hi[r] = x;
       }
-      const float v = wave_sum_f((a0 + a1) * F);
-      if (lane == 0) sh_p[wv][d] = v;
-    }
-    __syncthreads();
-    HS_STAMP(6);
-    if (wv == 0 && lane < n)
-      A.part[((int64_t)g * A.N + sub * D + lane) * S + s] =
-          (sh_p[0][lane] + sh_p[1][lane]) + (sh_p[2][lane] + sh_p[3][lane]);
-    HS_STAMP(7);
+      HS_STAMP(5);
+      __syncthreads();
+      // p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d) with a_x = (o_x - hi_x) - lo_x, all
+      // wave-uniform: min(p_v, q_v) = 2^(a_d) min(e_t,v 2^(a_t - a_d), e_d,v)
+      const float at = (ow[0] - sh_hi[0]) - sh_lo[0];
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        if (d >= q.n) continue;
+        const int r = d + 1;
+        const float ad = (ow[r] - sh_hi[r]) - sh_lo[r];
+        const float G = __builtin_amdgcn_exp2f(at - ad);
+        float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          // both >= 0 or +NaN (0 * inf): unsigned order of the bits is their order and a
+          // NaN loses, as with fminf, without fminf's canonicalising of the operands
+          const float y =
+              __uint_as_float(min(__float_as_uint(ex[0][e] * G), __float_as_uint(ex[r][e])));
+          if (e & 1) a1 += y;
+          else a0 += y;
+        }
+        const float v = wave_sum_f(a0 + a1) * __builtin_amdgcn_exp2f(ad);
+        if (lane == 0) sh_p[wv][d] = v;
+      }
+      __syncthreads();
+      HS_STAMP(6);
+      if (wv == 0 && lane < q.n)
+        A.part[((int64_t)q.g * A.N + q.sub * D + lane) * S + q.s] =
+            (sh_p[0][lane] + sh_p[1][lane]) + (sh_p[2][lane] + sh_p[3][lane]);
+      HS_STAMP(7);
     }
   }
 }
@@ -403,14 +416,13 @@ int capacity_t() {
 
 template <int DT, int D, bool NS, bool NA>
 int launch_t(const TeamArgs& A, const TeamGeom& g, hipStream_t stream) {
-  const int cap = capacity_t<DT, D, NS, NA>();
-  const int64_t per_round = (int64_t)(cap / g.S) * g.S;
+  // a round: a multiple of S that the device holds at once
+  const int64_t per_round = (int64_t)(capacity_t<DT, D, NS, NA>() / g.S) * g.S;
   if (per_round == 0) return HS_ERR_LIMIT;
   const int64_t P = std::min<int64_t>(g.items, per_round);
   hs_team_kernel<DT, D, NS, NA><<<(unsigned)P, kThreads, 0, stream>>>(A);
 #ifdef HS_TRACE
-  fprintf(stderr, "team grid %lld capacity %d S %d items %lld\n", (long long)P, cap, g.S,
-          (long long)g.items);
+  fprintf(stderr, "team grid %lld S %d items %lld\n", (long long)P, g.S, (long long)g.items);
 #endif
   return HS_OK;
 }

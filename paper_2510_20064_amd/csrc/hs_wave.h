@@ -33,14 +33,23 @@ __device__ inline int word_i(uint64_t w) { return (int)(uint32_t)(w >> 32); }
 // the four row results are combined in a fixed order; every lane gets the same value. All
 // 64 lanes must be active.
 
+// These patterns read only existing lanes of the row, so bound_ctrl changes no value; with it
+// set the compiler may fold the move into the consuming instruction (v_add_f32_dpp ...).
 template <int CTRL>
 __device__ inline float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 template <int CTRL>
 __device__ inline int dpp_i(int x) {
-  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, false);
+  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, true);
 }
+// Order-preserving map of a non-NaN float to a signed int (and back): negative values have
+// their magnitude bits flipped. Integer max needs no NaN canonicalisation, unlike fmaxf.
+__device__ inline int fkey(float x) {
+  const int b = __float_as_int(x);
+  return b ^ ((b >> 31) & 0x7FFFFFFF);
+}
+__device__ inline float fkey_inv(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF)); }
 __device__ inline float lane_f(float x, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }
@@ -59,7 +68,7 @@ __device__ inline void argmax_step(float& m, int& idx) {
   const int i2 = dpp_i<CTRL>(idx);
   argmax_combine(m, idx, m2, i2);
 }
-// Wave max of m; with NEED_ARG also the lowest index attaining it.
+// Wave max of m (not NaN); with NEED_ARG also the lowest index attaining it.
 template <bool NEED_ARG>
 __device__ inline void wave_max(float& m, int& idx) {
   if (NEED_ARG) {
@@ -74,12 +83,15 @@ __device__ inline void wave_max(float& m, int& idx) {
       argmax_combine(r, ri, lane_f(m, l), __builtin_amdgcn_readlane(idx, l));
     m = r;
     idx = ri;
-  } else {
-    m = fmaxf(m, dpp_f<0xB1>(m));
-    m = fmaxf(m, dpp_f<0x4E>(m));
-    m = fmaxf(m, dpp_f<0x141>(m));
-    m = fmaxf(m, dpp_f<0x140>(m));
-    m = fmaxf(fmaxf(lane_f(m, 0), lane_f(m, 16)), fmaxf(lane_f(m, 32), lane_f(m, 48)));
+  } else {  // m not NaN
+    int k = fkey(m);
+    k = max(k, dpp_i<0xB1>(k));
+    k = max(k, dpp_i<0x4E>(k));
+    k = max(k, dpp_i<0x141>(k));
+    k = max(k, dpp_i<0x140>(k));
+    k = max(max(__builtin_amdgcn_readlane(k, 0), __builtin_amdgcn_readlane(k, 16)),
+            max(__builtin_amdgcn_readlane(k, 32), __builtin_amdgcn_readlane(k, 48)));
+    m = fkey_inv(k);
   }
 }
 
