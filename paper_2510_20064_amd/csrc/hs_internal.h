@@ -16,6 +16,7 @@ constexpr int kSliceElems = 8192;      // logits per workgroup pass in hs_softma
 constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
 constexpr int kMaxSetDrafters = 8;     // drafters held on chip with the target by one workgroup
 constexpr int kMaxTeamSlices = 512;    // slices per row (one workgroup each) in one team
+constexpr int kMaxTeams = 4096;        // teams resident at once (one mailbox ring each)
 
 // Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 logits.
 template <int DT>
@@ -140,7 +141,8 @@ inline bool team_geom(int B, int N, int K, int64_t V, int dtype, TeamGeom* g) {
   if (S > kMaxTeamSlices) return false;
   g->S = (int)S;
   g->items = (int64_t)g->G * g->nsub * g->S;
-  return g->items < ((int64_t)1 << 31);
+  // items index with int; row sets fit the 26 bits a mailbox word gives them
+  return g->items < ((int64_t)1 << 31) && (int64_t)g->G * g->nsub < ((int64_t)1 << 26);
 }
 
 // Statistics of one row slice, in log2 units: offset o = fl(m * c) with c = log2(e)/T and
@@ -158,7 +160,9 @@ struct SliceStat {
 // workspace and advanced once per call, so words of earlier calls are never mistaken for
 // current ones and nothing has to be cleared.
 struct TeamWs {
-  size_t epoch;  // uint32 call counter at +0, the call's fail flag (a word) at +8
+  size_t epoch;  // control block: uint32 call counter at +0, the call's fail flag (word) at
+                 // +8, the tag the evaluation used (uint32) at +16, the row-set counter (uint32)
+                 // at +20, then a ring of 4 mailbox words per team at +64
   size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
   size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
   size_t part;   // [G][N][S] floats: per-slice sums of min(p, q_i)
@@ -172,7 +176,7 @@ inline TeamWs team_ws(const TeamGeom& g) {
   const size_t sets = (size_t)g.G * g.nsub, rows = (size_t)g.D + 1;
   size_t off = 0;
   L.epoch = off;
-  off = align256(off + 16);
+  off = align256(off + 64 + 32 * (size_t)kMaxTeams);
   L.stat = off;
   off = align256(off + 24 * sets * rows * g.S);
   L.norm = off;

@@ -29,11 +29,19 @@
 #include <atomic>
 #include <cstdio>
 
+#include "hs_learner.h"
 #include "hs_wave.h"
 
 namespace hs {
 
 constexpr uint32_t kSpinLimit = 1u << 18;  // polls before a wait gives up (~0.5 s)
+#ifndef HS_POLL_SLEEP
+#define HS_POLL_SLEEP 2
+#endif
+constexpr int kPollSleep = HS_POLL_SLEEP;  // s_sleep units (64 clocks) between polls
+#ifndef HS_CRIT_PRIO
+#define HS_CRIT_PRIO 2
+#endif
 
 struct TeamArgs {
   RowTable rows;
@@ -41,7 +49,10 @@ struct TeamArgs {
   int64_t V, nvec;
   float c;
   const uint32_t* epoch;
-  uint64_t* fail;  // set, with the call's tag, by the first wait that gives up
+  uint64_t* fail;      // set, with the call's tag, by the first wait that gives up
+  uint32_t* used_tag;  // the tag of this call, for the fold launch
+  uint32_t* next_set;  // row sets claimed beyond each team's first
+  uint64_t* mbox;      // [teams][4]: the row set of each team's coming items
   uint64_t* stat;  // [sets][D + 1][S][3]
   uint64_t* norm;  // [sets][D + 1][3]
   float* part;     // [G][N][S]
@@ -80,10 +91,34 @@ __device__ inline uint64_t await_word(const uint64_t* w, uint32_t tag, uint64_t*
       return kLost | tag;
     }
     if ((n & 255) == 0 && (uint32_t)get_word(fail) == tag) return kLost | tag;
-    __builtin_amdgcn_s_sleep(2);
+    __builtin_amdgcn_s_sleep(kPollSleep);
     v = get_word(w);
   }
   return v;
+}
+
+// Mailbox word of a team's item j: the row set in bits 38..63, j mod 64 in bits 32..37, the
+// call's tag below, so neither an earlier item's word in the same ring slot nor an earlier
+// call's word is taken for it.
+__device__ inline uint64_t mbox_word(uint32_t set, int j, uint32_t tag) {
+  return ((uint64_t)((set << 6) | ((uint32_t)j & 63u)) << 32) | tag;
+}
+// The row set posted for item j (bounded: `none` after a time-out, raising the fail flag).
+__device__ inline uint32_t await_mbox(const uint64_t* w, int j, uint32_t tag, uint64_t* fail,
+                                      uint32_t none) {
+  auto ok = [&](uint64_t v) {
+    return (uint32_t)v == tag && ((uint32_t)(v >> 32) & 63u) == ((uint32_t)j & 63u);
+  };
+  uint64_t v = get_word(w);
+  for (uint32_t n = 1; !ok(v); ++n) {
+    if (n == kSpinLimit || ((n & 255) == 0 && (uint32_t)get_word(fail) == tag)) {
+      put_word(fail, word_of(1, tag));
+      return none;
+    }
+    __builtin_amdgcn_s_sleep(kPollSleep);
+    v = get_word(w);
+  }
+  return (uint32_t)(v >> 38);
 }
 
 // Fold of row rr of row set `set`: the S slice statistics, two slices per lane per pass
@@ -174,229 +209,398 @@ __device__ inline ItemPos item_pos(const TeamArgs& A, int it, int D) {
   return q;
 }
 
-template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
-__global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
+// LDS of a team workgroup: per-wave row statistics, the row normalisers, per-wave partials.
+template <int D>
+struct TeamLds {
+  float m[kWaves][D + 1];
+  float s[kWaves][D + 1];
+  int i[kWaves][D + 1];
+  float hi[D + 1];
+  float lo[D + 1];
+  float p[kWaves][D];
+  uint32_t next;  // the row set of the team's next item, read by wave 0 for the workgroup
+};
+
+// Issue the loads of item q into dst: one unconditional 16-byte load per row, from an address
+// clamped into the row's complete vectors (lanes past the row end are masked to -inf before
+// use, mask_tail), so the loads of all rows are in flight together. The one partial vector at
+// the end of a row (V not a multiple of the vector width) is then re-read element by element,
+// in a branch taken only by the slice that holds it.
+template <int DT, int D>
+__device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q,
+                                           typename Vec<DT>::Raw (&dst)[D + 1]) {
   using Vt = Vec<DT>;
   using Raw = typename Vt::Raw;
   constexpr int E = Vt::kElems;
-  constexpr int RM = D + 1;
-  constexpr int XR = NEED_SUM ? RM : 1;  // rows of kept e_v
-  __shared__ float sh_m[kWaves][RM];
-  __shared__ float sh_s[kWaves][RM];
-  __shared__ int sh_i[kWaves][RM];
-  __shared__ float sh_hi[RM];
-  __shared__ float sh_lo[RM];
-  __shared__ float sh_p[kWaves][D];
+  const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
+  const char* rp[D + 1];
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    const int row = r == 0 ? 0 : q.sub * D + min(r, q.n);
+    rp[r] = reinterpret_cast<const char*>(A.rows.ptr[row]) +
+            ((int64_t)q.b * A.rows.sb[row] + (int64_t)q.k * A.rows.sk[row]) * Vt::kBytes;
+  }
+  if (vfull > 0) {
+    // uniform row base + 32-bit lane offset (a row holds < 2^31 logits)
+    const uint32_t off = (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16);
+#pragma unroll
+    for (int r = 0; r <= D; ++r)
+      if (r <= q.n) dst[r] = *reinterpret_cast<const Raw*>(rp[r] + off);
+  }
+  if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
+#pragma unroll
+    for (int r = 0; r <= D; ++r)
+      if (r <= q.n && q.vi == vfull) dst[r] = Vt::load_raw(rp[r], q.vi, A.V);
+  }
+}
 
+// -inf for the lanes of the last slice that lie past the row end.
+template <int DT, int D>
+__device__ __forceinline__ void mask_tail(const TeamArgs& A, const ItemPos& q,
+                                          typename Vec<DT>::Raw (&x)[D + 1]) {
+  if ((int64_t)(q.s + 1) * kThreads > A.nvec) {
+#pragma unroll
+    for (int r = 0; r <= D; ++r)
+      if (q.vi >= A.nvec) x[r] = Vec<DT>::neg_raw();
+  }
+}
+
+// The offset rows are exponentiated against: fl(m_w c) for a wave whose max m_w is finite,
+// 0 for a wave with no finite logit (every e_v is then exp2(-inf) = 0).
+__device__ inline float exp_offset(float ow) { return ow != -INFINITY ? ow : 0.0f; }
+
+// ---- 1. slice statistics of every row of item q (held in x) ----
+// Per row: the wave's max m_w (and lowest argmax), then e_v = exp2(z_v c - o_w) against
+// o_w = fl(m_w c) and their wave sum; lane 0 leaves (m_w, sum, argmax) in LDS. ow[r] gets
+// o_w (-inf for a wave with no finite logit), wave-uniform. With KEEP the e_v stay in ex.
+template <int DT, int D, bool NEED_SUM, bool NEED_ARG, bool KEEP>
+__device__ __forceinline__ void row_stats(const TeamArgs& A, const ItemPos& q,
+                                          const typename Vec<DT>::Raw (&x)[D + 1],
+                                          float (&ex)[KEEP ? D + 1 : 1][Vec<DT>::kElems],
+                                          float (&ow)[D + 1], TeamLds<D>& sh, int lane, int wv) {
+  using Vt = Vec<DT>;
+  constexpr int E = Vt::kElems;
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    if (r > q.n) continue;
+    float z[E];
+    Vt::unpack(x[r], z);
+    float m = -INFINITY;
+    int idx = INT_MAX;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if (NEED_ARG) {
+        if (z[e] > m) {
+          m = z[e];
+          idx = q.vi * E + e;
+        }
+      } else {
+        m = fmaxf(m, z[e]);
+      }
+    }
+    // a lane whose logits are all -inf still owns its lowest valid index
+    if (NEED_ARG && idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
+    wave_max<NEED_ARG>(m, idx);
+    float sw = 0.0f;
+    if constexpr (NEED_SUM) {
+      // rounded product (no contraction), recomputed alike by every reader
+      const float o = __int_as_float(
+          __builtin_amdgcn_readfirstlane(__float_as_int(m != -INFINITY ? m * A.c : -INFINITY)));
+      const float oc = exp_offset(o);
+      float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
+        if constexpr (KEEP) ex[r][e] = v;
+        if (e & 1) a1 += v;
+        else a0 += v;
+      }
+      sw = wave_sum_f(a0 + a1);
+      ow[r] = o;
+    }
+    if (lane == 0) {
+      sh.m[wv][r] = m;
+      sh.s[wv][r] = sw;
+      if (NEED_ARG) sh.i[wv][r] = idx;
+    }
+  }
+}
+
+// Workgroup statistics of each row from the waves' (after a barrier), published by lane r of
+// wave 0 as tagged words.
+template <int D, bool NEED_SUM, bool NEED_ARG>
+__device__ __forceinline__ void publish_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                             const TeamLds<D>& sh, int lane, int wv) {
+  if (wv != 0 || lane > q.n) return;
+  const int r = lane;
+  float m = sh.m[0][r];
+  int idx = NEED_ARG ? sh.i[0][r] : 0;
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) {
+    if (NEED_ARG) argmax_combine(m, idx, sh.m[w][r], sh.i[w][r]);
+    else m = fmaxf(m, sh.m[w][r]);
+  }
+  uint64_t* wp = A.stat + (((int64_t)q.set * (D + 1) + r) * A.S + q.s) * 3;
+  put_word(wp, word_of(m, tag));
+  if (NEED_SUM) {
+    const float o = m * A.c;
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = sh.m[w][r];
+      if (mw != -INFINITY) sum += sh.s[w][r] * __builtin_amdgcn_exp2f(mw * A.c - o);
+    }
+    put_word(wp + 1, word_of(sum, tag));
+  }
+  if (NEED_ARG) put_word(wp + 2, word_of(idx, tag));
+}
+
+// ---- 2. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
+template <int D, bool NEED_SUM, bool NEED_ARG>
+__device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                          int lane, int wv) {
+  for (int rr = q.s + wv * A.S; rr <= q.n; rr += kWaves * A.S)
+    fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
+}
+
+// ---- 3. normalisers (wave 0; a barrier follows), then the min-sum of every drafter ----
+template <int D>
+__device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                            TeamLds<D>& sh, int lane, int wv) {
+  if (wv == 0 && lane < 2 * (q.n + 1)) {
+    const int r = lane >> 1;
+    const float x =
+        word_f(await_word(A.norm + ((int64_t)q.set * (D + 1) + r) * 3 + (lane & 1), tag, A.fail));
+    if (lane & 1) sh.lo[r] = x;
+    else sh.hi[r] = x;
+  }
+}
+
+// min of two values that are >= 0 or +NaN (0 * inf): the unsigned order of the bits is their
+// order and a NaN loses, as with fminf, without fminf's canonicalising of the operands.
+__device__ inline float min_pos(float a, float b) {
+  return __uint_as_float(min(__float_as_uint(a), __float_as_uint(b)));
+}
+
+// p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d) with a_x = (o_x - hi_x) - lo_x, all wave-uniform:
+// min(p_v, q_v) = 2^(a_d) min(e_t,v 2^(a_t - a_d), e_d,v). Per-wave sums go to LDS.
+// ev(r, e_out) yields row r's e_v: the kept ones, or recomputed from the raw logits exactly
+// as row_stats formed them.
+template <int DT, int D, typename EV>
+__device__ __forceinline__ void min_sum(const TeamArgs& A, const ItemPos& q,
+                                        const float (&ow)[D + 1], TeamLds<D>& sh, int lane,
+                                        int wv, EV ev) {
+  constexpr int E = Vec<DT>::kElems;
+  float et[E];
+  ev(0, et);
+  const float at = (ow[0] - sh.hi[0]) - sh.lo[0];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    if (d >= q.n) continue;
+    const int r = d + 1;
+    const float ad = (ow[r] - sh.hi[r]) - sh.lo[r];
+    const float G = __builtin_amdgcn_exp2f(at - ad);
+    float ed[E];
+    ev(r, ed);
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float y = min_pos(et[e] * G, ed[e]);
+      if (e & 1) a1 += y;
+      else a0 += y;
+    }
+    const float v = wave_sum_f(a0 + a1) * __builtin_amdgcn_exp2f(ad);
+    if (lane == 0) sh.p[wv][d] = v;
+  }
+}
+
+// e_v of a raw 16-byte vector, formed exactly as row_stats does
+template <int DT>
+__device__ inline void raw_exps(const typename Vec<DT>::Raw& x, float o, float c,
+                                float (&out)[Vec<DT>::kElems]) {
+  float z[Vec<DT>::kElems];
+  Vec<DT>::unpack(x, z);
+  const float oc = exp_offset(o);
+#pragma unroll
+  for (int e = 0; e < Vec<DT>::kElems; ++e) out[e] = __builtin_amdgcn_exp2f(fmaf(z[e], c, -oc));
+}
+
+// the item's per-drafter partials (wave 0, after a barrier)
+template <int D>
+__device__ __forceinline__ void store_partial(const TeamArgs& A, const ItemPos& q,
+                                              const TeamLds<D>& sh, int lane, int wv) {
+  if (wv == 0 && lane < q.n)
+    A.part[((int64_t)q.g * A.N + q.sub * D + lane) * A.S + q.s] =
+        (sh.p[0][lane] + sh.p[1][lane]) + (sh.p[2][lane] + sh.p[3][lane]);
+}
+
+// A team of S workgroups (slot s takes slice s of every item) works through row sets: its
+// first is set T (T = team), later ones are claimed one item ahead by the team's leader from
+// a device-wide counter and posted in the team's mailbox ring, so teams that run faster (the
+// wave arbiter favours older waves) take more sets and all finish within an item of each
+// other. The loads of the next item fly during the exchange of the current one, whose e_v
+// stay in registers for the min-sum.
+template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
+__global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
+  using Raw = typename Vec<DT>::Raw;
+  constexpr int E = Vec<DT>::kElems;
+  constexpr int RM = D + 1;
+  __shared__ TeamLds<D> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const uint32_t tag = call_tag(A.epoch);
   const int S = A.S;
-  const int P = gridDim.x;
-  Raw nxt[RM];
+  const int teams = gridDim.x / S;
+  const int T = blockIdx.x / S, slot = blockIdx.x - T * S;
+  const uint32_t nsets = (uint32_t)(A.items / S);
+  // slot 0 folds row 0 of every item, so it waits for the whole team each item: it can never
+  // be more than one item ahead of any member, which keeps a ring of 4 mailbox words safe
+  const bool leader = slot == 0;
+  const bool dynamic = teams < (int)nsets;  // else every team has exactly its first set
+  uint64_t* mbox = A.mbox + (size_t)T * 4;
+  if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
 
-  // Issue the loads of item `it` into nxt: one unconditional 16-byte load per row, from an
-  // address clamped into the row's complete vectors (lanes past the row end are masked to -inf
-  // before use), so the loads of all rows are in flight together. The one partial vector at
-  // the end of a row (V not a multiple of the vector width) is then re-read element by
-  // element, in a branch taken only by the slice that holds it.
-  const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
-  auto fetch = [&](int it) __attribute__((always_inline)) {
-    const ItemPos q = item_pos(A, it, D);
-    const char* rp[RM];
-#pragma unroll
-    for (int r = 0; r < RM; ++r) {
-      const int row = r == 0 ? 0 : q.sub * D + min(r, q.n);
-      rp[r] = reinterpret_cast<const char*>(A.rows.ptr[row]) +
-              ((int64_t)q.b * A.rows.sb[row] + (int64_t)q.k * A.rows.sk[row]) * Vt::kBytes;
-    }
-    if (vfull > 0) {
-      // uniform row base + 32-bit lane offset (a row holds < 2^31 logits)
-      const uint32_t off = (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16);
-#pragma unroll
-      for (int r = 0; r < RM; ++r)
-        if (r <= q.n) nxt[r] = *reinterpret_cast<const Raw*>(rp[r] + off);
-    }
-    if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
-#pragma unroll
-      for (int r = 0; r < RM; ++r)
-        if (r <= q.n && q.vi == vfull) nxt[r] = Vt::load_raw(rp[r], q.vi, A.V);
-    }
+  // leader: claim the row set of the team's item j and post it
+  auto claim = [&](int j) __attribute__((always_inline)) {
+    if (!dynamic || !leader || t != 0) return;
+    uint32_t v = (uint32_t)teams +
+                 __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    put_word(mbox + (j & 3), mbox_word(min(v, nsets), j, tag));
+  };
+  // thread 0: the row set of the team's item j >= 1 (nsets: none left) into LDS, so that all
+  // waves of the workgroup take the same one after the next barrier
+  auto post_next = [&](int j) __attribute__((always_inline)) {
+    if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
   };
 
-  float ex[XR][E];  // e_v of the current item, against the wave's offset of its row
-  float ow[RM];     // that offset (wave-uniform), -inf for a wave with no finite logit
-
-  int it = blockIdx.x;
-  if (it < A.items) fetch(it);
-  for (; it < A.items; it += P) {
+  Raw nxt[RM];
+  float ex[NEED_SUM ? RM : 1][E];  // e_v of the current item
+  float ow[RM];
+  uint32_t set = (uint32_t)T;
+  fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), nxt);
+  claim(1);
+  for (int j = 0; set < nsets; ++j) {
+    const int it = (int)set * S + slot;
     const ItemPos q = item_pos(A, it, D);
     HS_STAMP(0);
-
-    // ---- 1. slice statistics of every row; e_v kept for step 3 ----
-    // Per row: the wave's max m_w (and lowest argmax), then e_v = exp2(z_v c - o_w) against
-    // o_w = fl(m_w c), and their wave sum; lane 0 leaves (m_w, sum, argmax) in LDS.
-    if ((int64_t)(q.s + 1) * kThreads > A.nvec) {  // the slice that runs past the row end
-#pragma unroll
-      for (int r = 0; r < RM; ++r)
-        if (q.vi >= A.nvec) nxt[r] = Vt::neg_raw();
-    }
-#pragma unroll
-    for (int r = 0; r < RM; ++r) {
-      if (r > q.n) continue;
-      float z[E];
-      Vt::unpack(nxt[r], z);
-      float m = -INFINITY;
-      int idx = INT_MAX;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        if (NEED_ARG) {
-          if (z[e] > m) {
-            m = z[e];
-            idx = q.vi * E + e;
-          }
-        } else {
-          m = fmaxf(m, z[e]);
-        }
-      }
-      // a lane whose logits are all -inf still owns its lowest valid index
-      if (NEED_ARG && idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
-      wave_max<NEED_ARG>(m, idx);
-      float sw = 0.0f;
-      if constexpr (NEED_SUM) {
-        // rounded product (no contraction), recomputed alike by every reader; a wave with
-        // no finite logit takes offset 0 and gets exp2(-inf) = 0 throughout
-        const float oc = m != -INFINITY ? m * A.c : 0.0f;
-        float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const float x = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
-          ex[r][e] = x;
-          if (e & 1) a1 += x;
-          else a0 += x;
-        }
-        sw = wave_sum_f(a0 + a1);
-        // wave-uniform: keep it in a scalar register
-        ow[r] = __int_as_float(
-            __builtin_amdgcn_readfirstlane(__float_as_int(m != -INFINITY ? oc : -INFINITY)));
-      }
-      if (lane == 0) {
-        sh_m[wv][r] = m;
-        sh_s[wv][r] = sw;
-        if (NEED_ARG) sh_i[wv][r] = idx;
-      }
-    }
+    // the team waits for this workgroup's statistics: ahead of co-resident waves until they
+    // are published
+    __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+    mask_tail<DT, D>(A, q, nxt);
+    row_stats<DT, D, NEED_SUM, NEED_ARG, NEED_SUM>(A, q, nxt, ex, ow, sh, lane, wv);
     HS_STAMP(1);
-    if (it + P < A.items) fetch(it + P);  // the successor's loads fly during the exchange
+    post_next(j + 1);
+    claim(j + 2);
     __syncthreads();
+    const uint32_t next = sh.next;
+    if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), nxt);
     HS_STAMP(2);
-
-    // workgroup statistics of each row, published by lane r of wave 0
-    if (wv == 0 && lane <= q.n) {
-      const int r = lane;
-      float m = sh_m[0][r];
-      int idx = NEED_ARG ? sh_i[0][r] : 0;
-#pragma unroll
-      for (int w = 1; w < kWaves; ++w) {
-        if (NEED_ARG) argmax_combine(m, idx, sh_m[w][r], sh_i[w][r]);
-        else m = fmaxf(m, sh_m[w][r]);
-      }
-      uint64_t* wp = A.stat + (((int64_t)q.set * RM + r) * S + q.s) * 3;
-      put_word(wp, word_of(m, tag));
-      if (NEED_SUM) {
-        const float o = m * A.c;
-        float sum = 0.0f;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-          const float mw = sh_m[w][r];
-          if (mw != -INFINITY) sum += sh_s[w][r] * __builtin_amdgcn_exp2f(mw * A.c - o);
-        }
-        put_word(wp + 1, word_of(sum, tag));
-      }
-      if (NEED_ARG) put_word(wp + 2, word_of(idx, tag));
-    }
+    publish_item<D, NEED_SUM, NEED_ARG>(A, q, tag, sh, lane, wv);
     __syncthreads();
     HS_STAMP(3);
-
-    // ---- 2. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
-    for (int rr = q.s + wv * S; rr <= q.n; rr += kWaves * S)
-      fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
+    fold_item<D, NEED_SUM, NEED_ARG>(A, q, tag, lane, wv);
+    __builtin_amdgcn_s_setprio(0);
     HS_STAMP(4);
-
-    // ---- 3. normalisers, then the min-sum of every drafter ----
     if constexpr (NEED_SUM) {
-      if (wv == 0 && lane < 2 * (q.n + 1)) {
-        const int r = lane >> 1;
-        const float x =
-            word_f(await_word(A.norm + ((int64_t)q.set * RM + r) * 3 + (lane & 1), tag, A.fail));
-        if (lane & 1) sh_lo[r] = x;
-        else sh_hi[r] = x;
-      }
+      await_norms<D>(A, q, tag, sh, lane, wv);
       HS_STAMP(5);
       __syncthreads();
-      // p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d) with a_x = (o_x - hi_x) - lo_x, all
-      // wave-uniform: min(p_v, q_v) = 2^(a_d) min(e_t,v 2^(a_t - a_d), e_d,v)
-      const float at = (ow[0] - sh_hi[0]) - sh_lo[0];
+      min_sum<DT, D>(A, q, ow, sh, lane, wv, [&](int r, float (&o)[E]) {
 #pragma unroll
-      for (int d = 0; d < D; ++d) {
-        if (d >= q.n) continue;
-        const int r = d + 1;
-        const float ad = (ow[r] - sh_hi[r]) - sh_lo[r];
-        const float G = __builtin_amdgcn_exp2f(at - ad);
-        float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          // both >= 0 or +NaN (0 * inf): unsigned order of the bits is their order and a
-          // NaN loses, as with fminf, without fminf's canonicalising of the operands
-          const float y =
-              __uint_as_float(min(__float_as_uint(ex[0][e] * G), __float_as_uint(ex[r][e])));
-          if (e & 1) a1 += y;
-          else a0 += y;
-        }
-        const float v = wave_sum_f(a0 + a1) * __builtin_amdgcn_exp2f(ad);
-        if (lane == 0) sh_p[wv][d] = v;
-      }
+        for (int e = 0; e < E; ++e) o[e] = ex[r][e];
+      });
       __syncthreads();
       HS_STAMP(6);
-      if (wv == 0 && lane < q.n)
-        A.part[((int64_t)q.g * A.N + q.sub * D + lane) * S + q.s] =
-            (sh_p[0][lane] + sh_p[1][lane]) + (sh_p[2][lane] + sh_p[3][lane]);
+      store_partial<D>(A, q, sh, lane, wv);
       HS_STAMP(7);
     }
+    set = next;
   }
 }
 
 // ---- 4. alpha from the slice partials; advances the epoch ----------------------------------
 
 struct FoldArgs {
-  const float* part;  // NULL: epoch only
+  const float* part;  // NULL: no alpha
   float* alpha;
+  uint8_t* agree;
+  int32_t* argmax_t;
+  int32_t* argmax_d;
   int B, N, K, S;
   uint32_t* epoch;
+  const uint64_t* fail;
+  const uint32_t* used_tag;
+  uint32_t* next_set;
 };
 
-// One wave per output alpha[b][i][k]: lane j sums slices j, j + 64, ... in order, then the
-// wave in a fixed order; clamped to [0, 1] (NaN passes through).
-__global__ __launch_bounds__(kThreads) void hs_fold_kernel(FoldArgs A) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) A.epoch[0] = A.epoch[0] + 1u;
-  if (!A.part) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t o = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
-  if (o >= (int64_t)A.B * A.N * A.K) return;
-  const int k = (int)(o % A.K);
+// Fold of outputs [o0, o0 + n) (n <= 64) by one workgroup: 4 threads per output, thread r of
+// the four summing slices r, r + 4, ... in order, then the four combined in a fixed order on
+// the DPP network; alpha is clamped to [0, 1]. If a wait of the evaluation gave up, the
+// outputs are marked instead: alpha NaN, argmax -2, agreement 0 (flag and tag were written by
+// the previous launch; their loads are issued with the partials').
+__device__ __forceinline__ void fold_chunk(const FoldArgs& A, int64_t o0, int n) {
+  const int t = threadIdx.x, lo = t >> 2, r = t & 3;
+  const int64_t o = o0 + lo;
+  const bool mine = lo < n;
+  const int k = mine ? (int)(o % A.K) : 0;
   const int64_t bi = o / A.K;
-  const int i = (int)(bi % A.N);
+  const int i = mine ? (int)(bi % A.N) : 0;
   const int64_t b = bi / A.N;
-  const float* src = A.part + ((b * A.K + k) * A.N + i) * A.S;
+  const uint32_t tag = *A.used_tag;
+  const uint64_t fw = *A.fail;
   float v = 0.0f;
-  for (int j = lane; j < A.S; j += 64) v += src[j];
-  v = wave_sum_f(v);
-  if (lane == 0) A.alpha[o] = v != v ? v : fminf(fmaxf(v, 0.0f), 1.0f);
+  if (A.part && mine) {
+    const float* src = A.part + ((b * A.K + k) * A.N + i) * A.S;
+    for (int j = r; j < A.S; j += 4) v += src[j];
+  }
+  v += dpp_f<0xB1>(v);  // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);  // quad_perm [2,3,0,1]
+  if (!mine || r != 0) return;
+  if ((uint32_t)fw == tag && (fw >> 32) != 0) {
+    if (A.alpha) A.alpha[o] = __int_as_float(0x7FC00000);
+    if (A.agree) A.agree[o] = 0;
+    if (A.argmax_d) A.argmax_d[o] = -2;
+    if (A.argmax_t && i == 0) A.argmax_t[b * A.K + k] = -2;
+  } else if (A.part) {
+    A.alpha[o] = fminf(fmaxf(v, 0.0f), 1.0f);
+  }
+}
+// Block 0 advances the epoch and resets the row-set counter; nothing else in the launch
+// reads either.
+__device__ __forceinline__ void next_call(const FoldArgs& A) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    A.epoch[0] = A.epoch[0] + 1u;
+    *A.next_set = 0u;
+  }
+}
+
+constexpr int kFoldOuts = kThreads / 4;  // outputs per workgroup pass
+
+// hs_eval_alpha's second launch: kFoldOuts outputs per workgroup.
+__global__ __launch_bounds__(kThreads) void hs_fold_kernel(FoldArgs A) {
+  next_call(A);
+  const int64_t total = (int64_t)A.B * A.N * A.K;
+  const int64_t o0 = (int64_t)blockIdx.x * kFoldOuts;
+  fold_chunk(A, o0, (int)std::min<int64_t>(kFoldOuts, total - o0));
+}
+
+// hs_round's second launch, one workgroup per query b: fold the query's N * K outputs, then
+// wave 0 runs the learner step on them.
+__global__ __launch_bounds__(kThreads) void hs_round_tail_kernel(FoldArgs F, TailArgs a) {
+  extern __shared__ double lds[];
+  next_call(F);
+  const int b = blockIdx.x;
+  const int nk = F.N * F.K;
+  for (int o = 0; o < nk; o += kFoldOuts)
+    fold_chunk(F, (int64_t)b * nk + o, std::min(kFoldOuts, nk - o));
+  __syncthreads();
+  if (threadIdx.x < 64) tail_query(a, b, lds);
 }
 
 // ---- host side -------------------------------------------------------------------------------
 
 namespace {
 
+// Workgroups of the team kernel the current device holds at once.
 template <int DT, int D, bool NS, bool NA>
 int capacity_t() {
   static std::atomic<int> cached[64];  // per device; 0 = not yet known
@@ -416,10 +620,12 @@ int capacity_t() {
 
 template <int DT, int D, bool NS, bool NA>
 int launch_t(const TeamArgs& A, const TeamGeom& g, hipStream_t stream) {
-  // a round: a multiple of S that the device holds at once
-  const int64_t per_round = (int64_t)(capacity_t<DT, D, NS, NA>() / g.S) * g.S;
-  if (per_round == 0) return HS_ERR_LIMIT;
-  const int64_t P = std::min<int64_t>(g.items, per_round);
+  // as many teams as the device holds at once, no more than there are row sets or rings
+  const int64_t sets = g.items / g.S;
+  const int64_t teams =
+      std::min<int64_t>({capacity_t<DT, D, NS, NA>() / g.S, sets, (int64_t)kMaxTeams});
+  if (teams <= 0) return HS_ERR_LIMIT;
+  const int64_t P = teams * g.S;
   hs_team_kernel<DT, D, NS, NA><<<(unsigned)P, kThreads, 0, stream>>>(A);
 #ifdef HS_TRACE
   fprintf(stderr, "team grid %lld S %d items %lld\n", (long long)P, g.S, (long long)g.items);
@@ -482,6 +688,9 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.c = c;
   A.epoch = reinterpret_cast<const uint32_t*>(ws + L.epoch);
   A.fail = reinterpret_cast<uint64_t*>(ws + L.epoch + 8);
+  A.used_tag = reinterpret_cast<uint32_t*>(ws + L.epoch + 16);
+  A.next_set = reinterpret_cast<uint32_t*>(ws + L.epoch + 20);
+  A.mbox = reinterpret_cast<uint64_t*>(ws + L.epoch + 64);
   A.stat = reinterpret_cast<uint64_t*>(ws + L.stat);
   A.norm = reinterpret_cast<uint64_t*>(ws + L.norm);
   A.part = need_sum ? reinterpret_cast<float*>(ws + L.part) : nullptr;
@@ -495,13 +704,16 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   if (rc) return rc;
   if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
 
-  FoldArgs F{A.part, alpha, g.B, g.N, g.K, g.S, reinterpret_cast<uint32_t*>(ws + L.epoch)};
-  const int64_t outs = need_sum ? (int64_t)g.B * g.N * g.K : 0;
-  const unsigned blocks = outs ? (unsigned)((outs + kWaves - 1) / kWaves) : 1u;
-  hs_fold_kernel<<<blocks, kThreads, 0, stream>>>(F);
-  if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
-  if (tail) return launch_tail(*tail, stream);
-  return HS_OK;
+  FoldArgs F{A.part,  alpha, agree, argmax_t, argmax_d, g.B, g.N, g.K, g.S,
+             reinterpret_cast<uint32_t*>(ws + L.epoch), A.fail, A.used_tag, A.next_set};
+  if (tail) {  // fold and learner step in one launch
+    const size_t lds = sizeof(double) * (size_t)tail_lds_doubles(*tail);
+    hs_round_tail_kernel<<<g.B, kThreads, lds, stream>>>(F, *tail);
+  } else {
+    const int64_t outs = (int64_t)g.B * g.N * g.K;
+    hs_fold_kernel<<<(unsigned)((outs + kFoldOuts - 1) / kFoldOuts), kThreads, 0, stream>>>(F);
+  }
+  return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
 }
 
 }  // namespace hs
