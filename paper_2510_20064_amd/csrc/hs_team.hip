@@ -71,12 +71,22 @@ extern "C" __attribute__((visibility("default"))) void hs_debug_set_trace(void* 
 }
 #define HS_STAMP(i) \
   if (t == 0 && A.trace) A.trace[(size_t)it * 8 + (i)] = __builtin_amdgcn_s_memrealtime()
+// per workgroup, after the item slots: kernel entry and first loads issued
+#define HS_STAMP_WG(i)                                                                  \
+  if (t == 0 && A.trace)                                                                \
+  A.trace[(size_t)A.items * 8 + (size_t)blockIdx.x * 2 + (i)] = __builtin_amdgcn_s_memrealtime()
 #else
 #define HS_STAMP(i)
+#define HS_STAMP_WG(i)
 #endif
 
 // Tag of this call's words: never 0, the content of a zero-filled workspace.
-__device__ inline uint32_t call_tag(const uint32_t* epoch) { return (*epoch % 0xFFFFFFFFu) + 1u; }
+// (a vector load: a scalar one would hold up the kernel-argument loads waited on with it)
+__device__ inline uint32_t call_tag(const uint32_t* epoch) {
+  const uint32_t e =
+      __hip_atomic_load(const_cast<uint32_t*>(epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)((e % 0xFFFFFFFFu) + 1u));
+}
 
 // The word at w once it carries tag. Bounded: after kSpinLimit polls, or as soon as another
 // wait of this call has given up, the value is 0xFFFFFFFE (a NaN as float, -2 as int); the
@@ -219,6 +229,11 @@ struct TeamLds {
   float lo[D + 1];
   float p[kWaves][D];
   uint32_t next;  // the row set of the team's next item, read by wave 0 for the workgroup
+  // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
+  // chain of dependent scalar loads per item)
+  const char* ptr[kMaxRows];
+  int64_t sb[kMaxRows];
+  int64_t sk[kMaxRows];
 };
 
 // Issue the loads of item q into dst: one unconditional 16-byte load per row, from an address
@@ -228,24 +243,41 @@ struct TeamLds {
 // in a branch taken only by the slice that holds it.
 template <int DT, int D>
 __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q,
+                                           const TeamLds<D>& sh,
                                            typename Vec<DT>::Raw (&dst)[D + 1]) {
   using Vt = Vec<DT>;
   using Raw = typename Vt::Raw;
   constexpr int E = Vt::kElems;
   const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
-  const char* rp[D + 1];
+  // lane r <= n: the base of row r of the item, then broadcast
+  const int l = threadIdx.x & 63;
+  uint64_t base = 0;
+  if (l <= q.n) {
+    const int row = l == 0 ? 0 : q.sub * D + l;
+    base = reinterpret_cast<uint64_t>(sh.ptr[row]) +
+           (uint64_t)(((int64_t)q.b * sh.sb[row] + (int64_t)q.k * sh.sk[row]) * Vt::kBytes);
+  }
+  uint64_t rb[D + 1];
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
-    const int row = r == 0 ? 0 : q.sub * D + min(r, q.n);
-    rp[r] = reinterpret_cast<const char*>(A.rows.ptr[row]) +
-            ((int64_t)q.b * A.rows.sb[row] + (int64_t)q.k * A.rows.sk[row]) * Vt::kBytes;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, r);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), r);
+    rb[r] = ((uint64_t)hi << 32) | lo;
   }
+  const char* rp[D + 1];
+#pragma unroll
+  for (int r = 0; r <= D; ++r) rp[r] = reinterpret_cast<const char*>(rb[r]);
   if (vfull > 0) {
-    // uniform row base + 32-bit lane offset (a row holds < 2^31 logits)
+    // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
+    // 16-byte load
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
     const uint32_t off = (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16);
 #pragma unroll
     for (int r = 0; r <= D; ++r)
-      if (r <= q.n) dst[r] = *reinterpret_cast<const Raw*>(rp[r] + off);
+      if (r <= q.n) {
+        const u4 v = *(const __attribute__((address_space(1))) u4*)(rb[r] + off);
+        __builtin_memcpy(&dst[r], &v, 16);
+      }
   }
   if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
 #pragma unroll
@@ -447,7 +479,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   constexpr int RM = D + 1;
   __shared__ TeamLds<D> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-  const uint32_t tag = call_tag(A.epoch);
+  HS_STAMP_WG(0);
   const int S = A.S;
   const int teams = gridDim.x / S;
   const int T = blockIdx.x / S, slot = blockIdx.x - T * S;
@@ -456,8 +488,14 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   // be more than one item ahead of any member, which keeps a ring of 4 mailbox words safe
   const bool leader = slot == 0;
   const bool dynamic = teams < (int)nsets;  // else every team has exactly its first set
+  uint32_t tag = 0;  // the call's tag: read once the first loads are in flight
   uint64_t* mbox = A.mbox + (size_t)T * 4;
-  if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
+  if (t < kMaxRows) {
+    sh.ptr[t] = reinterpret_cast<const char*>(A.rows.ptr[t]);
+    sh.sb[t] = A.rows.sb[t];
+    sh.sk[t] = A.rows.sk[t];
+  }
+  __syncthreads();
 
   // leader: claim the row set of the team's item j and post it
   auto claim = [&](int j) __attribute__((always_inline)) {
@@ -476,7 +514,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   float ex[NEED_SUM ? RM : 1][E];  // e_v of the current item
   float ow[RM];
   uint32_t set = (uint32_t)T;
-  fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), nxt);
+  fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), sh, nxt);
+  HS_STAMP_WG(1);
+  // the call's tag is first needed after the first loads are in flight
+  tag = call_tag(A.epoch);
+  if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
   claim(1);
   for (int j = 0; set < nsets; ++j) {
     const int it = (int)set * S + slot;
@@ -492,7 +534,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     claim(j + 2);
     __syncthreads();
     const uint32_t next = sh.next;
-    if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), nxt);
+    if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), sh, nxt);
     HS_STAMP(2);
     publish_item<D, NEED_SUM, NEED_ARG>(A, q, tag, sh, lane, wv);
     __syncthreads();
