@@ -243,7 +243,7 @@ HS_API int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int
                          const int32_t* parent_host, const int32_t* path_end, double* eal,
                          double* prefix, int loss_kind, double* loss, void* stream) {
   TailReq q{alpha, agree, mode, B, N, K, parent_host, path_end, eal, prefix, loss_kind, loss};
-  hs::TailArgs a;
+  hs::TailArgs a{};
   int rc = validate_tail(q, &a);
   if (rc) return rc;
   rc = hs::launch_tail(a, (hipStream_t)stream);
@@ -265,7 +265,7 @@ HS_API int hs_hedge_update(double* logw, double* w, const double* loss, int L, i
   int rc = learner_common(loss, L, B, N);
   if (rc) return rc;
   if (!isfinite(eta)) return fail(HS_ERR_ARG, "eta must be finite");
-  hs::TailArgs a;
+  hs::TailArgs a{};
   memset(&a, 0, sizeof(a));
   a.gamma_src = 0;
   a.B = B;
@@ -286,7 +286,7 @@ HS_API int hs_normalhedge_update(double* R, double* p, double* c, const double* 
   if (!R || !p || !c) return fail(HS_ERR_NULL, "R, p and c are required");
   int rc = learner_common(loss, L, B, N);
   if (rc) return rc;
-  hs::TailArgs a;
+  hs::TailArgs a{};
   memset(&a, 0, sizeof(a));
   a.gamma_src = 0;
   a.B = B;
@@ -313,7 +313,7 @@ HS_API int hs_round(const hs_round_args* r, void* stream) {
   if (rc) return rc;
   TailReq t{r->alpha, r->agree, r->mode, r->B, r->N, r->K, r->parent_host, r->path_end, r->eal,
             r->prefix, r->loss_kind, r->loss};
-  hs::TailArgs a;
+  hs::TailArgs a{};
   if ((rc = validate_tail(t, &a))) return rc;
   if ((r->logw == nullptr) != (r->w == nullptr))
     return fail(HS_ERR_NULL, "logw and w must be given together");

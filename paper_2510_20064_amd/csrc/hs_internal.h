@@ -239,10 +239,13 @@ struct TailArgs {
   double* R;
   double* p;
   double* c;
+#ifdef HS_TRACE
+  uint64_t* trace;  // per query: 16 phase timestamps of lane 0
+#endif
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
 // Evaluation of one round: the team kernel, then the fold of the per-slice sums into alpha
-// (which also advances the workspace epoch), then the learner step when tail != nullptr.
+// (which also advances the workspace epoch) and, when tail != nullptr, the learner step.
 int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,
                  float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
                  const TailArgs* tail, hipStream_t stream);

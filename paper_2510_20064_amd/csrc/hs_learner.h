@@ -17,6 +17,13 @@
 
 namespace hs {
 
+#ifdef HS_TRACE
+#define HS_TSTAMP(k) \
+  if ((threadIdx.x & 63) == 0 && a.trace) a.trace[(size_t)b * 16 + (k)] = __builtin_amdgcn_s_memrealtime()
+#else
+#define HS_TSTAMP(k)
+#endif
+
 // Wave64 reductions of doubles on the DPP network (no LDS crossbar round trip): pairs and
 // quads by quad_perm, 8- and 16-lane groups by the half-row and row mirrors, then the four
 // row results are read into scalars. Every lane gets the same value; all 64 lanes must be active.
@@ -82,7 +89,10 @@ __host__ __device__ inline int tail_lds_doubles(const TailArgs& a) {
 }
 
 // Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
-__device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds) {
+// gamma_lds (optional): the query's alpha as [N][M] floats in LDS, instead of a.alpha.
+// Every input is loaded before anything is stored, so the loads are in flight together.
+__device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds,
+                                           const float* gamma_lds = nullptr) {
   const int i = threadIdx.x & 63;
   const int N = a.N, M = a.M;
   const bool act = i < N;
@@ -90,16 +100,45 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
   double* lossv = lds + M * N;  // [L][N]
   int L = a.L;
 
+  // learner state, loaded up front
+  const int64_t si = (int64_t)b * N + i;
+  const double lw0 = (a.logw && act) ? a.logw[si] : 0.0;
+  const double R0 = (a.R && act) ? a.R[si] : 0.0;
+  const double p0 = (a.R && act) ? a.p[si] : 0.0;
+  const double c_prev = a.R ? a.c[b] : 0.0;  // warm start of the scale search
+  const int end = (a.gamma_src != 0 && a.path_end) ? a.path_end[b] : M - 1;
+
   if (a.gamma_src != 0) {
-    const int end = a.path_end ? a.path_end[b] : M - 1;
     const bool ok = end >= 0 && end < M;
     double sum1mg = 0.0, eal = NAN;
     int len = 0;
-    if (act) {
+    auto gamma_at = [&](int n) -> double {
+      const int64_t o = ((int64_t)b * N + i) * M + n;
+      return gamma_lds ? (double)gamma_lds[i * M + n]
+                       : (a.gamma_src == 1) ? (double)a.alpha[o] : (double)a.agree[o];
+    };
+    if (act && !a.tree) {
+      // chain: one pass in position order, the prefix product carried in a register
+      double pp = 1.0, sp = 0.0;
       for (int n = 0; n < M; ++n) {
-        const int64_t o = ((int64_t)b * N + i) * M + n;
-        gam[n * N + i] = (a.gamma_src == 1) ? (double)a.alpha[o] : (double)a.agree[o];
+        const double g = gamma_at(n);
+        if (a.loss_kind == HS_LOSS_ACCEPT_TOKEN) lossv[n * N + i] = 1.0 - g;
+        pp *= g;
+        if (a.prefix) a.prefix[((int64_t)b * N + i) * M + n] = pp;
+        if (n <= end) {
+          sp += pp;
+          sum1mg += 1.0 - g;
+        }
       }
+      len = ok ? end + 1 : 0;
+      if (ok) eal = 1.0 + sp;
+      a.eal[(int64_t)b * N + i] = eal;
+      if (a.loss_kind == HS_LOSS_LENGTH)
+        lossv[i] = ok ? 1.0 - eal / (double)(len + 1) : NAN;
+      else if (a.loss_kind == HS_LOSS_ACCEPT_CHUNK)
+        lossv[i] = ok ? sum1mg / (double)len : NAN;
+    } else if (act) {
+      for (int n = 0; n < M; ++n) gam[n * N + i] = gamma_at(n);
       if (ok)
         for (int n = end; n >= 0; n = a.tree ? a.parent[n] : n - 1) {
           sum1mg += 1.0 - gam[n * N + i];
@@ -131,6 +170,7 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
       for (int l = 0; l < L; ++l) a.loss_out[((int64_t)l * a.B + b) * N + i] = lossv[l * N + i];
   }
 
+  HS_TSTAMP(3);
   auto loss_at = [&](int l) -> double {
     if (!act) return 0.0;
     if (a.gamma_src != 0) return lossv[l * N + i];
@@ -139,7 +179,7 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
 
   // ---- Hedge ----
   if (a.logw) {
-    double lw = act ? a.logw[(int64_t)b * N + i] : -INFINITY;
+    double lw = act ? lw0 : -INFINITY;
     for (int l = 0; l < L; ++l) lw -= a.eta * loss_at(l);
     const double mx = wmax(act ? lw : -INFINITY);
     const double e = act ? exp(lw - mx) : 0.0;
@@ -150,12 +190,12 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
     }
   }
 
+  HS_TSTAMP(4);
   // ---- NormalHedge ----
   if (a.R) {
-    double Rv = act ? a.R[(int64_t)b * N + i] : 0.0;
-    double pv = act ? a.p[(int64_t)b * N + i] : 0.0;
+    double Rv = R0;
+    double pv = p0;
     double cc = 0.0;
-    const double c_prev = a.c[b];  // warm start of the scale search
     for (int l = 0; l < L; ++l) {
       const double li = loss_at(l);
       // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
@@ -184,6 +224,7 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
     }
     if (i == 0) a.c[b] = cc;
   }
+  HS_TSTAMP(5);
 }
 
 }  // namespace hs

@@ -568,18 +568,21 @@ struct FoldArgs {
   int32_t* argmax_t;
   int32_t* argmax_d;
   int B, N, K, S;
+  int alpha_lds;  // hs_round_tail_kernel: keep alpha in LDS for the learner
   uint32_t* epoch;
   const uint64_t* fail;
   const uint32_t* used_tag;
   uint32_t* next_set;
 };
 
-// Fold of outputs [o0, o0 + n) (n <= 64) by one workgroup: 4 threads per output, thread r of
+// Fold of outputs [o0, o0 + n) (n <= 64) by one workgroup (out_lds: also alpha of output
+// o0 + j to out_lds[j]): 4 threads per output, thread r of
 // the four summing slices r, r + 4, ... in order, then the four combined in a fixed order on
 // the DPP network; alpha is clamped to [0, 1]. If a wait of the evaluation gave up, the
 // outputs are marked instead: alpha NaN, argmax -2, agreement 0 (flag and tag were written by
 // the previous launch; their loads are issued with the partials').
-__device__ __forceinline__ void fold_chunk(const FoldArgs& A, int64_t o0, int n) {
+__device__ __forceinline__ void fold_chunk(const FoldArgs& A, int64_t o0, int n,
+                                           float* out_lds = nullptr) {
   const int t = threadIdx.x, lo = t >> 2, r = t & 3;
   const int64_t o = o0 + lo;
   const bool mine = lo < n;
@@ -591,19 +594,29 @@ __device__ __forceinline__ void fold_chunk(const FoldArgs& A, int64_t o0, int n)
   const uint64_t fw = *A.fail;
   float v = 0.0f;
   if (A.part && mine) {
+    // slices r, r + 4, ... in order; 16 loads in flight at a time
     const float* src = A.part + ((b * A.K + k) * A.N + i) * A.S;
-    for (int j = r; j < A.S; j += 4) v += src[j];
+    for (int j0 = r; j0 < A.S; j0 += 64) {
+      float x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = j0 + 4 * u < A.S ? src[j0 + 4 * u] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v += x[u];
+    }
   }
   v += dpp_f<0xB1>(v);  // quad_perm [1,0,3,2]
   v += dpp_f<0x4E>(v);  // quad_perm [2,3,0,1]
   if (!mine || r != 0) return;
   if ((uint32_t)fw == tag && (fw >> 32) != 0) {
     if (A.alpha) A.alpha[o] = __int_as_float(0x7FC00000);
+    if (out_lds) out_lds[lo] = __int_as_float(0x7FC00000);
     if (A.agree) A.agree[o] = 0;
     if (A.argmax_d) A.argmax_d[o] = -2;
     if (A.argmax_t && i == 0) A.argmax_t[b * A.K + k] = -2;
   } else if (A.part) {
-    A.alpha[o] = fminf(fmaxf(v, 0.0f), 1.0f);
+    const float al = fminf(fmaxf(v, 0.0f), 1.0f);
+    A.alpha[o] = al;
+    if (out_lds) out_lds[lo] = al;
   }
 }
 // Block 0 advances the epoch and resets the row-set counter; nothing else in the launch
@@ -625,17 +638,22 @@ __global__ __launch_bounds__(kThreads) void hs_fold_kernel(FoldArgs A) {
   fold_chunk(A, o0, (int)std::min<int64_t>(kFoldOuts, total - o0));
 }
 
-// hs_round's second launch, one workgroup per query b: fold the query's N * K outputs, then
-// wave 0 runs the learner step on them.
+// hs_round's second launch, one workgroup per query b: fold the query's N * K outputs (kept
+// in LDS after the learner's own LDS when they are its gamma), then wave 0 runs the learner
+// step on them.
 __global__ __launch_bounds__(kThreads) void hs_round_tail_kernel(FoldArgs F, TailArgs a) {
   extern __shared__ double lds[];
   next_call(F);
   const int b = blockIdx.x;
   const int nk = F.N * F.K;
+  float* al = F.alpha_lds ? reinterpret_cast<float*>(lds + tail_lds_doubles(a)) : nullptr;
+  HS_TSTAMP(0);
   for (int o = 0; o < nk; o += kFoldOuts)
-    fold_chunk(F, (int64_t)b * nk + o, std::min(kFoldOuts, nk - o));
+    fold_chunk(F, (int64_t)b * nk + o, std::min(kFoldOuts, nk - o), al ? al + o : nullptr);
+  HS_TSTAMP(1);
   __syncthreads();
-  if (threadIdx.x < 64) tail_query(a, b, lds);
+  HS_TSTAMP(2);
+  if (threadIdx.x < 64) tail_query(a, b, lds, al);
 }
 
 // ---- host side -------------------------------------------------------------------------------
@@ -746,10 +764,20 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   if (rc) return rc;
   if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
 
-  FoldArgs F{A.part,  alpha, agree, argmax_t, argmax_d, g.B, g.N, g.K, g.S,
+  FoldArgs F{A.part, alpha, agree, argmax_t, argmax_d, g.B, g.N, g.K, g.S, 0,
              reinterpret_cast<uint32_t*>(ws + L.epoch), A.fail, A.used_tag, A.next_set};
   if (tail) {  // fold and learner step in one launch
-    const size_t lds = sizeof(double) * (size_t)tail_lds_doubles(*tail);
+#ifdef HS_TRACE
+    TailArgs tt = *tail;
+    tt.trace = g_trace ? g_trace + (size_t)g.items * 8 + 2 * kMaxTeams : nullptr;
+    tail = &tt;
+#endif
+    size_t lds = sizeof(double) * (size_t)tail_lds_doubles(*tail);
+    const size_t al = sizeof(float) * (size_t)g.N * g.K;
+    if (tail->gamma_src == 1 && A.part && lds + al <= 65536) {
+      F.alpha_lds = 1;
+      lds += al;
+    }
     hs_round_tail_kernel<<<g.B, kThreads, lds, stream>>>(F, *tail);
   } else {
     const int64_t outs = (int64_t)g.B * g.N * g.K;
