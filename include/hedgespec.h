@@ -183,11 +183,11 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
                           int N, void* stream);
 
 /*
- * hs_round - one verification round of the whole path, enqueued as three launches
- * (evaluation, fold into alpha, learner step): the work of hs_eval_alpha, then per
- * query hs_accept_len's work, the loss, and the Hedge and NormalHedge updates with
- * that loss (same workspace contract as hs_eval_alpha). Arguments mean
- * what they mean in the calls above. Learner state pointers may be NULL to
+ * hs_round - one verification round of the whole path, enqueued as two launches
+ * (the evaluation; then, per query, the fold into alpha and the learner step): the
+ * work of hs_eval_alpha, then per query hs_accept_len's work, the loss, and the
+ * Hedge and NormalHedge updates with that loss (same workspace contract as
+ * hs_eval_alpha). Arguments mean what they mean in the calls above. Learner state pointers may be NULL to
  * skip that learner (logw and w together; R, p and c together). eal is
  * required; alpha/agree as hs_eval_alpha requires them for `mode`.
  */
