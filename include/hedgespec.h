@@ -187,9 +187,9 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
  * (the evaluation; then, per query, the fold into alpha and the learner step): the
  * work of hs_eval_alpha, then per query hs_accept_len's work, the loss, and the
  * Hedge and NormalHedge updates with that loss (same workspace contract as
- * hs_eval_alpha). Arguments mean what they mean in the calls above. Learner state pointers may be NULL to
- * skip that learner (logw and w together; R, p and c together). eal is
- * required; alpha/agree as hs_eval_alpha requires them for `mode`.
+ * hs_eval_alpha). Arguments mean what they mean in the calls above. Learner
+ * state pointers may be NULL to skip that learner (logw and w together; R, p
+ * and c together). eal is required; alpha/agree as hs_eval_alpha requires them for `mode`.
  */
 typedef struct hs_round_args {
   hs_view target;
