@@ -7,9 +7,8 @@
 // one (query, position) group, 256 16-byte vectors each, held in the registers of one
 // 256-thread workgroup (thread t owns vector t of every row). The S items of a row set form
 // a team that is resident at the same time:
-//   1. every item reduces its rows (max, lowest argmax, exp2 sum) and publishes them;
-//      it keeps e_v = exp2(z_v c - o) against its lane's offset o = fl(m_lane c),
-//      c = log2(e) / T;
+//   1. every item reduces its rows (max, lowest argmax, exp2 sum against the slice offset
+//      o = fl(m c), c = log2(e) / T) and publishes them; it keeps e_v = exp2(z_v c - o);
 //   2. item s folds the S slice statistics of row s (rows s, s + S, ... when S is smaller
 //      than the row count) into the row's log2 normaliser L = hi + lo and publishes it;
 //   3. every item reads the normalisers and takes, per drafter,
@@ -17,14 +16,16 @@
 //      F_d = 2^(a_d) and G = 2^(a_t - a_d): one multiply, one min and one add per drafter
 //      logit, no second exponential;
 //   4. a second launch sums each drafter's S slice partials in slice order into alpha.
-// The loads of an item's successor are issued before its exchange (step 2 - 3), so HBM stays
-// busy while the team waits.
+// Within a workgroup every reduction over the slice goes through LDS: each thread stores its
+// per-row value, then one 16-lane group per row reduces the row's 256 values and the result
+// is known to the whole group, so no wave reduces all rows on its own.
+// The loads of an item's successor are issued right after its logits are unpacked, so HBM
+// stays busy while the team reduces and exchanges.
 //
-// Items are dealt to workgroups round-robin, item i to workgroup i mod P, where P is a
-// multiple of S no larger than what the device holds at once: every team lies inside one
-// round and all of its members are resident, so waiting on a team member cannot deadlock.
-// Words crossing workgroups carry the call's epoch as tag; the fold launch advances the
-// epoch. Every wait is bounded: a word that never arrives yields NaN (argmax -2), no hang.
+// The grid holds as many teams as the device keeps resident at once, so all members of a
+// team run together and waiting on one cannot deadlock. Words crossing workgroups carry the
+// call's epoch as tag; the fold launch advances the epoch. Every wait is bounded: a word that
+// never arrives yields NaN (argmax -2), no hang.
 #include <algorithm>
 #include <atomic>
 #include <cstdio>
@@ -219,16 +220,18 @@ __device__ inline ItemPos item_pos(const TeamArgs& A, int it, int D) {
   return q;
 }
 
-// LDS of a team workgroup: per-wave row statistics, the row normalisers, per-wave partials.
-template <int D>
+// LDS of a team workgroup. Per-thread values of every row are stored transposed, [row][thread],
+// so that one 16-lane group reduces one row (group_read) instead of every wave reducing every
+// row on its own.
+template <int D, bool NEED_ARG>
 struct TeamLds {
-  float m[kWaves][D + 1];
-  float s[kWaves][D + 1];
-  int i[kWaves][D + 1];
-  float hi[D + 1];
-  float lo[D + 1];
-  float p[kWaves][D];
-  uint32_t next;  // the row set of the team's next item, read by wave 0 for the workgroup
+  float xt[D + 1][kThreads];              // per-thread max keys / maxima, then exp2 sums
+  int xi[NEED_ARG ? D + 1 : 1][kThreads];  // per-thread argmax
+  float xp[D][kThreads];                  // per-thread min-sums of each drafter
+  float o[D + 1];                         // slice offsets fl(m c)
+  float G[D];                             // 2^(a_t - a_d), a_x = (o_x - hi_x) - lo_x
+  float F[D];                             // 2^(a_d)
+  uint32_t next;  // the row set of the team's next item, posted by thread 0
   // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
   // chain of dependent scalar loads per item)
   const char* ptr[kMaxRows];
@@ -241,12 +244,10 @@ struct TeamLds {
 // use, mask_tail), so the loads of all rows are in flight together. The one partial vector at
 // the end of a row (V not a multiple of the vector width) is then re-read element by element,
 // in a branch taken only by the slice that holds it.
-template <int DT, int D>
-__device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q,
-                                           const TeamLds<D>& sh,
+template <int DT, int D, typename L>
+__device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, const L& sh,
                                            typename Vec<DT>::Raw (&dst)[D + 1]) {
   using Vt = Vec<DT>;
-  using Raw = typename Vt::Raw;
   constexpr int E = Vt::kElems;
   const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
   // lane r <= n: the base of row r of the item, then broadcast
@@ -264,9 +265,6 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q,
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), r);
     rb[r] = ((uint64_t)hi << 32) | lo;
   }
-  const char* rp[D + 1];
-#pragma unroll
-  for (int r = 0; r <= D; ++r) rp[r] = reinterpret_cast<const char*>(rb[r]);
   if (vfull > 0) {
     // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
     // 16-byte load
@@ -282,7 +280,8 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q,
   if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
 #pragma unroll
     for (int r = 0; r <= D; ++r)
-      if (r <= q.n && q.vi == vfull) dst[r] = Vt::load_raw(rp[r], q.vi, A.V);
+      if (r <= q.n && q.vi == vfull)
+        dst[r] = Vt::load_raw(reinterpret_cast<const char*>(rb[r]), q.vi, A.V);
   }
 }
 
@@ -297,116 +296,9 @@ __device__ __forceinline__ void mask_tail(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// The offset rows are exponentiated against: fl(m_w c) for a wave whose max m_w is finite,
-// 0 for a wave with no finite logit (every e_v is then exp2(-inf) = 0).
-__device__ inline float exp_offset(float ow) { return ow != -INFINITY ? ow : 0.0f; }
-
-// ---- 1. slice statistics of every row of item q (held in x) ----
-// Per row: the wave's max m_w (and lowest argmax), then e_v = exp2(z_v c - o_w) against
-// o_w = fl(m_w c) and their wave sum; lane 0 leaves (m_w, sum, argmax) in LDS. ow[r] gets
-// o_w (-inf for a wave with no finite logit), wave-uniform. With KEEP the e_v stay in ex.
-template <int DT, int D, bool NEED_SUM, bool NEED_ARG, bool KEEP>
-__device__ __forceinline__ void row_stats(const TeamArgs& A, const ItemPos& q,
-                                          const typename Vec<DT>::Raw (&x)[D + 1],
-                                          float (&ex)[KEEP ? D + 1 : 1][Vec<DT>::kElems],
-                                          float (&ow)[D + 1], TeamLds<D>& sh, int lane, int wv) {
-  using Vt = Vec<DT>;
-  constexpr int E = Vt::kElems;
-#pragma unroll
-  for (int r = 0; r <= D; ++r) {
-    if (r > q.n) continue;
-    float z[E];
-    Vt::unpack(x[r], z);
-    float m = -INFINITY;
-    int idx = INT_MAX;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      if (NEED_ARG) {
-        if (z[e] > m) {
-          m = z[e];
-          idx = q.vi * E + e;
-        }
-      } else {
-        m = fmaxf(m, z[e]);
-      }
-    }
-    // a lane whose logits are all -inf still owns its lowest valid index
-    if (NEED_ARG && idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
-    wave_max<NEED_ARG>(m, idx);
-    float sw = 0.0f;
-    if constexpr (NEED_SUM) {
-      // rounded product (no contraction), recomputed alike by every reader
-      const float o = __int_as_float(
-          __builtin_amdgcn_readfirstlane(__float_as_int(m != -INFINITY ? m * A.c : -INFINITY)));
-      const float oc = exp_offset(o);
-      float a0 = 0.0f, a1 = 0.0f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
-        if constexpr (KEEP) ex[r][e] = v;
-        if (e & 1) a1 += v;
-        else a0 += v;
-      }
-      sw = wave_sum_f(a0 + a1);
-      ow[r] = o;
-    }
-    if (lane == 0) {
-      sh.m[wv][r] = m;
-      sh.s[wv][r] = sw;
-      if (NEED_ARG) sh.i[wv][r] = idx;
-    }
-  }
-}
-
-// Workgroup statistics of each row from the waves' (after a barrier), published by lane r of
-// wave 0 as tagged words.
-template <int D, bool NEED_SUM, bool NEED_ARG>
-__device__ __forceinline__ void publish_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                             const TeamLds<D>& sh, int lane, int wv) {
-  if (wv != 0 || lane > q.n) return;
-  const int r = lane;
-  float m = sh.m[0][r];
-  int idx = NEED_ARG ? sh.i[0][r] : 0;
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) {
-    if (NEED_ARG) argmax_combine(m, idx, sh.m[w][r], sh.i[w][r]);
-    else m = fmaxf(m, sh.m[w][r]);
-  }
-  uint64_t* wp = A.stat + (((int64_t)q.set * (D + 1) + r) * A.S + q.s) * 3;
-  put_word(wp, word_of(m, tag));
-  if (NEED_SUM) {
-    const float o = m * A.c;
-    float sum = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float mw = sh.m[w][r];
-      if (mw != -INFINITY) sum += sh.s[w][r] * __builtin_amdgcn_exp2f(mw * A.c - o);
-    }
-    put_word(wp + 1, word_of(sum, tag));
-  }
-  if (NEED_ARG) put_word(wp + 2, word_of(idx, tag));
-}
-
-// ---- 2. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
-template <int D, bool NEED_SUM, bool NEED_ARG>
-__device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                          int lane, int wv) {
-  for (int rr = q.s + wv * A.S; rr <= q.n; rr += kWaves * A.S)
-    fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
-}
-
-// ---- 3. normalisers (wave 0; a barrier follows), then the min-sum of every drafter ----
-template <int D>
-__device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                            TeamLds<D>& sh, int lane, int wv) {
-  if (wv == 0 && lane < 2 * (q.n + 1)) {
-    const int r = lane >> 1;
-    const float x =
-        word_f(await_word(A.norm + ((int64_t)q.set * (D + 1) + r) * 3 + (lane & 1), tag, A.fail));
-    if (lane & 1) sh.lo[r] = x;
-    else sh.hi[r] = x;
-  }
-}
+// The offset a slice is exponentiated against: fl(m c) for a slice whose max m is finite,
+// 0 for a slice with no finite logit (every e_v is then exp2(-inf) = 0).
+__device__ inline float exp_offset(float o) { return o != -INFINITY ? o : 0.0f; }
 
 // min of two values that are >= 0 or +NaN (0 * inf): the unsigned order of the bits is their
 // order and a NaN loses, as with fminf, without fminf's canonicalising of the operands.
@@ -414,71 +306,162 @@ __device__ inline float min_pos(float a, float b) {
   return __uint_as_float(min(__float_as_uint(a), __float_as_uint(b)));
 }
 
-// p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d) with a_x = (o_x - hi_x) - lo_x, all wave-uniform:
-// min(p_v, q_v) = 2^(a_d) min(e_t,v 2^(a_t - a_d), e_d,v). Per-wave sums go to LDS.
-// ev(r, e_out) yields row r's e_v: the kept ones, or recomputed from the raw logits exactly
-// as row_stats formed them.
-template <int DT, int D, typename EV>
-__device__ __forceinline__ void min_sum(const TeamArgs& A, const ItemPos& q,
-                                        const float (&ow)[D + 1], TeamLds<D>& sh, int lane,
-                                        int wv, EV ev) {
+// ---- 1. per-thread max (and lowest argmax) of every row of item q; the logits go to x ----
+template <int DT, int D, bool NEED_ARG, typename L>
+__device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
+                                           const typename Vec<DT>::Raw (&raw)[D + 1],
+                                           float (&x)[D + 1][Vec<DT>::kElems], L& sh, int t) {
   constexpr int E = Vec<DT>::kElems;
-  float et[E];
-  ev(0, et);
-  const float at = (ow[0] - sh.hi[0]) - sh.lo[0];
 #pragma unroll
-  for (int d = 0; d < D; ++d) {
-    if (d >= q.n) continue;
-    const int r = d + 1;
-    const float ad = (ow[r] - sh.hi[r]) - sh.lo[r];
-    const float G = __builtin_amdgcn_exp2f(at - ad);
-    float ed[E];
-    ev(r, ed);
-    float a0 = 0.0f, a1 = 0.0f;
+  for (int r = 0; r <= D; ++r) {
+    if (r > q.n) continue;
+    Vec<DT>::unpack(raw[r], x[r]);
+    float m = -INFINITY;
+    int idx = INT_MAX;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const float y = min_pos(et[e] * G, ed[e]);
-      if (e & 1) a1 += y;
-      else a0 += y;
+      if (NEED_ARG) {
+        if (x[r][e] > m) {
+          m = x[r][e];
+          idx = q.vi * E + e;
+        }
+      } else {
+        m = fmaxf(m, x[r][e]);
+      }
     }
-    const float v = wave_sum_f(a0 + a1) * __builtin_amdgcn_exp2f(ad);
-    if (lane == 0) sh.p[wv][d] = v;
+    if (NEED_ARG) {
+      // a lane whose logits are all -inf still owns its lowest valid index
+      if (idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
+      sh.xt[r][t] = m;
+      sh.xi[r][t] = idx;
+    } else {
+      sh.xt[r][t] = __int_as_float(fkey(m));  // integer key: the group max needs no NaN care
+    }
   }
 }
 
-// e_v of a raw 16-byte vector, formed exactly as row_stats does
-template <int DT>
-__device__ inline void raw_exps(const typename Vec<DT>::Raw& x, float o, float c,
-                                float (&out)[Vec<DT>::kElems]) {
-  float z[Vec<DT>::kElems];
-  Vec<DT>::unpack(x, z);
-  const float oc = exp_offset(o);
+// ---- 2. group max: 16-lane group gi reduces row gi of the item (every lane of the group
+// gets the slice max m and argmax). Waves whose groups hold no row skip it. ----
+template <int D, bool NEED_ARG, typename L>
+__device__ __forceinline__ void group_max(const L& sh, int n, int gi, int gl, float& m,
+                                          int& idx) {
+  const int r = min(gi, n);  // groups past the last row reduce a copy of it (all 16 lanes
+                             // of a group must take part in the DPP steps)
+  if (NEED_ARG) {
+    float v[16];
+    int iv[16];
+    group_read(&sh.xt[r][0], gl, v);
+    group_read(&sh.xi[r][0], gl, iv);
+    m = v[0];
+    idx = iv[0];
 #pragma unroll
-  for (int e = 0; e < Vec<DT>::kElems; ++e) out[e] = __builtin_amdgcn_exp2f(fmaf(z[e], c, -oc));
+    for (int u = 1; u < 16; ++u) argmax_combine(m, idx, v[u], iv[u]);
+    row16_argmax(m, idx);
+  } else {
+    int kv[16];
+    group_read(reinterpret_cast<const int*>(&sh.xt[r][0]), gl, kv);
+    int k = kv[0];
+#pragma unroll
+    for (int u = 1; u < 16; ++u) k = max(k, kv[u]);
+    m = fkey_inv(row16_max(k));
+  }
 }
 
-// the item's per-drafter partials (wave 0, after a barrier)
-template <int D>
-__device__ __forceinline__ void store_partial(const TeamArgs& A, const ItemPos& q,
-                                              const TeamLds<D>& sh, int lane, int wv) {
-  if (wv == 0 && lane < q.n)
-    A.part[((int64_t)q.g * A.N + q.sub * D + lane) * A.S + q.s] =
-        (sh.p[0][lane] + sh.p[1][lane]) + (sh.p[2][lane] + sh.p[3][lane]);
+// ---- 3. exponentials: e_v = exp2(z_v c - o) against the slice offset o, kept in x; the
+// per-thread sums go to LDS ----
+template <int DT, int D, typename L>
+__device__ __forceinline__ void thread_exps(const TeamArgs& A, const ItemPos& q,
+                                            float (&x)[D + 1][Vec<DT>::kElems], L& sh, int t) {
+  constexpr int E = Vec<DT>::kElems;
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    if (r > q.n) continue;
+    const float oc = exp_offset(sh.o[r]);
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, -oc));
+      if (e & 1) a1 += x[r][e];
+      else a0 += x[r][e];
+    }
+    sh.xt[r][t] = a0 + a1;
+  }
+}
+
+// Slice statistics of row r as tagged words.
+template <bool NEED_SUM, bool NEED_ARG>
+__device__ __forceinline__ void publish_row(const TeamArgs& A, const ItemPos& q, int r,
+                                            uint32_t tag, float m, float s, int idx, int RM) {
+  uint64_t* wp = A.stat + (((int64_t)q.set * RM + r) * A.S + q.s) * 3;
+  put_word(wp, word_of(m, tag));
+  if (NEED_SUM) put_word(wp + 1, word_of(s, tag));
+  if (NEED_ARG) put_word(wp + 2, word_of(idx, tag));
+}
+
+// ---- 4. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
+template <int D, bool NEED_SUM, bool NEED_ARG>
+__device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                          int lane, int wv) {
+  for (int rr = q.s + wv * A.S; rr <= q.n; rr += kWaves * A.S)
+    fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
+}
+
+// ---- 5. normalisers (wave 0; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
+// lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, G and F to LDS ----
+template <int D, typename L>
+__device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                            L& sh, int lane) {
+  float h = 0.0f;
+  if (lane < 2 * (q.n + 1))
+    h = word_f(await_word(A.norm + ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1),
+                          tag, A.fail));
+  const float lo = dpp_f<0xB1>(h);  // lane 2r: the lo of row r, from lane 2r + 1
+  const float a = (sh.o[min(lane >> 1, D)] - h) - lo;
+  const float at = lane_f(a, 0);
+  if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
+    const int d = (lane >> 1) - 1;
+    sh.G[d] = __builtin_amdgcn_exp2f(at - a);
+    sh.F[d] = __builtin_amdgcn_exp2f(a);
+  }
+}
+
+// ---- 6. per-thread min-sums: p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d), so
+// min(p_v, q_v) = 2^(a_d) min(e_t,v G, e_d,v) with G = 2^(a_t - a_d); the factor 2^(a_d) is
+// applied to the group sum ----
+template <int DT, int D, typename L>
+__device__ __forceinline__ void thread_minsums(const ItemPos& q,
+                                               const float (&x)[D + 1][Vec<DT>::kElems], L& sh,
+                                               int t) {
+  constexpr int E = Vec<DT>::kElems;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    if (d >= q.n) continue;
+    const float G = sh.G[d];
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float y = min_pos(x[0][e] * G, x[d + 1][e]);
+      if (e & 1) a1 += y;
+      else a0 += y;
+    }
+    sh.xp[d][t] = a0 + a1;
+  }
 }
 
 // A team of S workgroups (slot s takes slice s of every item) works through row sets: its
-// first is set T (T = team), later ones are claimed one item ahead by the team's leader from
-// a device-wide counter and posted in the team's mailbox ring, so teams that run faster (the
-// wave arbiter favours older waves) take more sets and all finish within an item of each
-// other. The loads of the next item fly during the exchange of the current one, whose e_v
-// stay in registers for the min-sum.
+// first two are sets T and T + teams (T = team), later ones are claimed two items ahead by
+// the team's leader from a device-wide counter and posted in the team's mailbox ring, so teams
+// that run faster (the wave arbiter favours older waves) take more sets and all finish within
+// an item of each other. The loads of the next item fly while the current one is reduced and
+// exchanged; its e_v stay in registers for the min-sum.
 template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
 __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   using Raw = typename Vec<DT>::Raw;
   constexpr int E = Vec<DT>::kElems;
   constexpr int RM = D + 1;
-  __shared__ TeamLds<D> sh;
+  __shared__ TeamLds<D, NEED_ARG> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int gi = t >> 4, gl = t & 15;  // 16-lane group gi reduces row gi; gl: lane in it
   HS_STAMP_WG(0);
   const int S = A.S;
   const int teams = gridDim.x / S;
@@ -497,29 +480,31 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   }
   __syncthreads();
 
-  // leader: claim the row set of the team's item j and post it
+  // leader: claim the row set of the team's item j >= 2 and post it (the counter starts past
+  // the sets of every team's first two items, so a set is never claimed twice, and once a
+  // team's next item has none every later claim has none either)
   auto claim = [&](int j) __attribute__((always_inline)) {
     if (!dynamic || !leader || t != 0) return;
-    uint32_t v = (uint32_t)teams +
-                 __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t v = 2u * (uint32_t)teams + __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_AGENT);
     put_word(mbox + (j & 3), mbox_word(min(v, nsets), j, tag));
   };
   // thread 0: the row set of the team's item j >= 1 (nsets: none left) into LDS, so that all
   // waves of the workgroup take the same one after the next barrier
   auto post_next = [&](int j) __attribute__((always_inline)) {
-    if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
+    if (t != 0) return;
+    if (j == 1) sh.next = min((uint32_t)(T + teams), nsets);
+    else sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
   };
 
   Raw nxt[RM];
-  float ex[NEED_SUM ? RM : 1][E];  // e_v of the current item
-  float ow[RM];
+  float x[RM][E];  // the current item's logits, then its e_v
   uint32_t set = (uint32_t)T;
   fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), sh, nxt);
   HS_STAMP_WG(1);
   // the call's tag is first needed after the first loads are in flight
   tag = call_tag(A.epoch);
   if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
-  claim(1);
   for (int j = 0; set < nsets; ++j) {
     const int it = (int)set * S + slot;
     const ItemPos q = item_pos(A, it, D);
@@ -528,38 +513,62 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     // are published
     __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
     mask_tail<DT, D>(A, q, nxt);
-    row_stats<DT, D, NEED_SUM, NEED_ARG, NEED_SUM>(A, q, nxt, ex, ow, sh, lane, wv);
-    HS_STAMP(1);
+    thread_max<DT, D, NEED_ARG>(A, q, nxt, x, sh, t);
     post_next(j + 1);
     claim(j + 2);
     __syncthreads();
+    HS_STAMP(1);
     const uint32_t next = sh.next;
     if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), sh, nxt);
-    HS_STAMP(2);
-    publish_item<D, NEED_SUM, NEED_ARG>(A, q, tag, sh, lane, wv);
-    __syncthreads();
+    const bool has_rows = wv * 4 <= q.n;  // this wave holds the group of a row
+    const bool row_lead = gl == 0 && gi <= q.n;
+    float m = 0.0f;
+    int idx = 0;
+    if (has_rows) {
+      group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
+      if (NEED_SUM && row_lead) sh.o[gi] = m != -INFINITY ? m * A.c : -INFINITY;
+      if (!NEED_SUM && row_lead) publish_row<false, NEED_ARG>(A, q, gi, tag, m, 0.0f, idx, RM);
+    }
+    if constexpr (NEED_SUM) {
+      __syncthreads();
+      HS_STAMP(2);
+      thread_exps<DT, D>(A, q, x, sh, t);
+      __syncthreads();
+      if (has_rows) {
+        float v[16];
+        group_read(&sh.xt[min(gi, q.n)][0], gl, v);
+        const float s = row16_sum(sum16(v));
+        if (row_lead) publish_row<true, NEED_ARG>(A, q, gi, tag, m, s, idx, RM);
+      }
+    }
     HS_STAMP(3);
     fold_item<D, NEED_SUM, NEED_ARG>(A, q, tag, lane, wv);
     __builtin_amdgcn_s_setprio(0);
     HS_STAMP(4);
     if constexpr (NEED_SUM) {
-      await_norms<D>(A, q, tag, sh, lane, wv);
-      HS_STAMP(5);
+      if (wv == 0) await_norms<D>(A, q, tag, sh, lane);
       __syncthreads();
-      min_sum<DT, D>(A, q, ow, sh, lane, wv, [&](int r, float (&o)[E]) {
-#pragma unroll
-        for (int e = 0; e < E; ++e) o[e] = ex[r][e];
-      });
+      HS_STAMP(5);
+      thread_minsums<DT, D>(q, x, sh, t);
       __syncthreads();
       HS_STAMP(6);
-      store_partial<D>(A, q, sh, lane, wv);
+      if (wv * 4 < q.n) {
+        float v[16];
+        const int d = min(gi, q.n - 1);
+        group_read(&sh.xp[d][0], gl, v);
+        const float y = row16_sum(sum16(v));
+        if (gl == 0 && gi < q.n)
+          A.part[((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s] = y * sh.F[gi];
+      }
       HS_STAMP(7);
+    } else {
+      __syncthreads();  // the LDS rows are free for the next item
     }
     set = next;
   }
 }
 
-// ---- 4. alpha from the slice partials; advances the epoch ----------------------------------
+// ---- 7. alpha from the slice partials; advances the epoch ----------------------------------
 
 struct FoldArgs {
   const float* part;  // NULL: no alpha

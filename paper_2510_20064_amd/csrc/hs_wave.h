@@ -95,6 +95,52 @@ __device__ inline void wave_max(float& m, int& idx) {
   }
 }
 
+// ---- reductions within a DPP row: 16-lane groups ---------------------------------------------
+// Pairs, quads, half-rows, then the row; afterwards every lane of the group holds the result
+// (each step combines a lane with its mirror, so all lanes form bitwise the same value). All
+// 16 lanes of the group must be active.
+__device__ inline float row16_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return v;
+}
+__device__ inline int row16_max(int k) {
+  k = max(k, dpp_i<0xB1>(k));
+  k = max(k, dpp_i<0x4E>(k));
+  k = max(k, dpp_i<0x141>(k));
+  return max(k, dpp_i<0x140>(k));
+}
+__device__ inline void row16_argmax(float& m, int& idx) {
+  argmax_step<0xB1>(m, idx);
+  argmax_step<0x4E>(m, idx);
+  argmax_step<0x141>(m, idx);
+  argmax_step<0x140>(m, idx);
+}
+
+// Lane j of a 16-lane group reads the values 64 i + 4 j + k (i, k = 0..3) of an LDS row of
+// 256: one 16-byte read per i, consecutive lanes on consecutive 16 bytes (no bank conflict).
+template <typename T>
+__device__ inline void group_read(const T* row, int j, T (&v)[16]) {
+  typedef T T4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const T4 x = *reinterpret_cast<const T4*>(row + 64 * i + 4 * j);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[4 * i + k] = x[k];
+  }
+}
+// Sum of 16 values in a fixed pairwise order.
+__device__ inline float sum16(const float (&v)[16]) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = v[2 * i] + v[2 * i + 1];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = a[2 * i] + a[2 * i + 1];
+  return (a[0] + a[1]) + (a[2] + a[3]);
+}
+
 template <int CTRL>
 __device__ inline void lse_step(float& o, float& s) {
   const float o2 = dpp_f<CTRL>(o);
