@@ -71,7 +71,7 @@ extern "C" __attribute__((visibility("default"))) void hs_debug_set_trace(void* 
   g_trace = reinterpret_cast<uint64_t*>(p);
 }
 #define HS_STAMP(i) \
-  if (t == 0 && A.trace) A.trace[(size_t)it * 8 + (i)] = __builtin_amdgcn_s_memrealtime()
+  if (t == 0 && A.trace) A.trace[(size_t)(set * S + slot) * 8 + (i)] = __builtin_amdgcn_s_memrealtime()
 // per workgroup, after the item slots: kernel entry and first loads issued
 #define HS_STAMP_WG(i)                                                                  \
   if (t == 0 && A.trace)                                                                \
@@ -222,16 +222,17 @@ __device__ inline ItemPos item_pos(const TeamArgs& A, int it, int D) {
 
 // LDS of a team workgroup. Per-thread values of every row are stored transposed, [row][thread],
 // so that one 16-lane group reduces one row (group_read) instead of every wave reducing every
-// row on its own.
+// row on its own. Slice offsets are double-buffered by item parity: an item's min-sum runs
+// after the statistics of its successor.
 template <int D, bool NEED_ARG>
 struct TeamLds {
-  float xt[D + 1][kThreads];              // per-thread max keys / maxima, then exp2 sums
-  int xi[NEED_ARG ? D + 1 : 1][kThreads];  // per-thread argmax
-  float xp[D][kThreads];                  // per-thread min-sums of each drafter
-  float o[D + 1];                         // slice offsets fl(m c)
-  float G[D];                             // 2^(a_t - a_d), a_x = (o_x - hi_x) - lo_x
-  float F[D];                             // 2^(a_d)
-  uint32_t next;  // the row set of the team's next item, posted by thread 0
+  float xt[D + 1][kThreads];                  // per-thread max keys / maxima, then exp2 sums
+  int xi[NEED_ARG ? D + 1 : 1][kThreads];     // per-thread argmax
+  float xp[D][kThreads];                      // per-thread min-sums of each drafter
+  float o[2][D + 1];                          // slice offsets fl(m c)
+  float dl[D];                                // a_t - a_d, a_x = (o_x - hi_x) - lo_x
+  float F[D];                                 // 2^(a_d)
+  uint32_t next;  // a row set of the team's coming items, posted by thread 0
   // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
   // chain of dependent scalar loads per item)
   const char* ptr[kMaxRows];
@@ -239,21 +240,24 @@ struct TeamLds {
   int64_t sk[kMaxRows];
 };
 
-// Issue the loads of item q into dst: one unconditional 16-byte load per row, from an address
-// clamped into the row's complete vectors (lanes past the row end are masked to -inf before
-// use, mask_tail), so the loads of all rows are in flight together. The one partial vector at
-// the end of a row (V not a multiple of the vector width) is then re-read element by element,
-// in a branch taken only by the slice that holds it.
+// Issue the loads of item q into dst: exactly D + 1 unconditional 16-byte loads, so that the
+// number of loads in flight is the same on every path and a later wait for an older item's
+// registers can leave these outstanding. Each comes from an address clamped into the row's
+// complete vectors (lanes past the row end are masked to -inf before use, mask_tail); rows
+// past the set's last drafter, and every row when !valid, read 16 bytes of the workspace's
+// control block instead (a cache-resident dummy, never used). The one partial vector at the
+// end of a row (V not a multiple of the vector width) is then re-read element by element, in
+// a branch taken only by the slice that holds it.
 template <int DT, int D, typename L>
-__device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, const L& sh,
-                                           typename Vec<DT>::Raw (&dst)[D + 1]) {
+__device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, bool valid,
+                                           const L& sh, typename Vec<DT>::Raw (&dst)[D + 1]) {
   using Vt = Vec<DT>;
   constexpr int E = Vt::kElems;
   const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
   // lane r <= n: the base of row r of the item, then broadcast
   const int l = threadIdx.x & 63;
-  uint64_t base = 0;
-  if (l <= q.n) {
+  uint64_t base = reinterpret_cast<uint64_t>(A.epoch);
+  if (valid && l <= q.n) {
     const int row = l == 0 ? 0 : q.sub * D + l;
     base = reinterpret_cast<uint64_t>(sh.ptr[row]) +
            (uint64_t)(((int64_t)q.b * sh.sb[row] + (int64_t)q.k * sh.sk[row]) * Vt::kBytes);
@@ -265,19 +269,18 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, 
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), r);
     rb[r] = ((uint64_t)hi << 32) | lo;
   }
-  if (vfull > 0) {
-    // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
-    // 16-byte load
-    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
-    const uint32_t off = (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16);
+  // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
+  // 16-byte load
+  typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+  const uint32_t off =
+      valid && vfull > 0 ? (uint32_t)((q.vi < vfull ? q.vi : vfull - 1) * 16) : 0u;
 #pragma unroll
-    for (int r = 0; r <= D; ++r)
-      if (r <= q.n) {
-        const u4 v = *(const __attribute__((address_space(1))) u4*)(rb[r] + off);
-        __builtin_memcpy(&dst[r], &v, 16);
-      }
+  for (int r = 0; r <= D; ++r) {
+    const uint32_t o = r <= q.n ? off : 0u;
+    const u4 v = *(const __attribute__((address_space(1))) u4*)(rb[r] + o);
+    __builtin_memcpy(&dst[r], &v, 16);
   }
-  if (vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // this slice holds the tail
+  if (valid && vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // the tail slice
 #pragma unroll
     for (int r = 0; r <= D; ++r)
       if (r <= q.n && q.vi == vfull)
@@ -306,27 +309,42 @@ __device__ inline float min_pos(float a, float b) {
   return __uint_as_float(min(__float_as_uint(a), __float_as_uint(b)));
 }
 
-// ---- 1. per-thread max (and lowest argmax) of every row of item q; the logits go to x ----
+// The raw registers of one row made opaque to the compiler: each stage unpacks the logits
+// afresh (two integer operations per pair) instead of the compiler keeping the unpacked
+// floats of a whole item live from one stage to the next, which would not fit in registers.
+template <typename Raw>
+__device__ __forceinline__ void launder(Raw& x) {
+  static_assert(sizeof(Raw) == 16, "16-byte vectors");
+  uint32_t w[4];
+  __builtin_memcpy(w, &x, 16);
+  asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
+  __builtin_memcpy(&x, w, 16);
+}
+
+// ---- 1. per-thread max (and lowest argmax) of every row of item q, to LDS ----
 template <int DT, int D, bool NEED_ARG, typename L>
 __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
-                                           const typename Vec<DT>::Raw (&raw)[D + 1],
-                                           float (&x)[D + 1][Vec<DT>::kElems], L& sh, int t) {
+                                           const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                           int t) {
   constexpr int E = Vec<DT>::kElems;
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
     if (r > q.n) continue;
-    Vec<DT>::unpack(raw[r], x[r]);
+    typename Vec<DT>::Raw x = raw[r];
+    launder(x);
+    float z[E];
+    Vec<DT>::unpack(x, z);
     float m = -INFINITY;
     int idx = INT_MAX;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       if (NEED_ARG) {
-        if (x[r][e] > m) {
-          m = x[r][e];
+        if (z[e] > m) {
+          m = z[e];
           idx = q.vi * E + e;
         }
       } else {
-        m = fmaxf(m, x[r][e]);
+        m = fmaxf(m, z[e]);
       }
     }
     if (NEED_ARG) {
@@ -340,8 +358,8 @@ __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// ---- 2. group max: 16-lane group gi reduces row gi of the item (every lane of the group
-// gets the slice max m and argmax). Waves whose groups hold no row skip it. ----
+// ---- 2. group max: 16-lane group gi reduces row gi (every lane of the group gets the slice
+// max m and argmax). Waves whose groups hold no row skip it. ----
 template <int D, bool NEED_ARG, typename L>
 __device__ __forceinline__ void group_max(const L& sh, int n, int gi, int gl, float& m,
                                           int& idx) {
@@ -367,22 +385,27 @@ __device__ __forceinline__ void group_max(const L& sh, int n, int gi, int gl, fl
   }
 }
 
-// ---- 3. exponentials: e_v = exp2(z_v c - o) against the slice offset o, kept in x; the
-// per-thread sums go to LDS ----
+// ---- 3. exp2 sums against the slice offsets o (buffer bf): exp2(z_v c - o) summed per
+// thread, to LDS ----
 template <int DT, int D, typename L>
-__device__ __forceinline__ void thread_exps(const TeamArgs& A, const ItemPos& q,
-                                            float (&x)[D + 1][Vec<DT>::kElems], L& sh, int t) {
+__device__ __forceinline__ void thread_sums(const TeamArgs& A, const ItemPos& q,
+                                            const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                            int bf, int t) {
   constexpr int E = Vec<DT>::kElems;
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
     if (r > q.n) continue;
-    const float oc = exp_offset(sh.o[r]);
+    typename Vec<DT>::Raw x = raw[r];
+    launder(x);
+    float z[E];
+    Vec<DT>::unpack(x, z);
+    const float oc = exp_offset(sh.o[bf][r]);
     float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, -oc));
-      if (e & 1) a1 += x[r][e];
-      else a0 += x[r][e];
+      const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
+      if (e & 1) a1 += v;
+      else a0 += v;
     }
     sh.xt[r][t] = a0 + a1;
   }
@@ -407,40 +430,56 @@ __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, u
 }
 
 // ---- 5. normalisers (wave 0; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
-// lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, G and F to LDS ----
+// lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, a_t - a_r and 2^(a_r) to
+// LDS ----
 template <int D, typename L>
 __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                            L& sh, int lane) {
+                                            L& sh, int bf, int lane) {
   float h = 0.0f;
   if (lane < 2 * (q.n + 1))
     h = word_f(await_word(A.norm + ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1),
                           tag, A.fail));
   const float lo = dpp_f<0xB1>(h);  // lane 2r: the lo of row r, from lane 2r + 1
-  const float a = (sh.o[min(lane >> 1, D)] - h) - lo;
+  const float a = (sh.o[bf][min(lane >> 1, D)] - h) - lo;
   const float at = lane_f(a, 0);
   if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
     const int d = (lane >> 1) - 1;
-    sh.G[d] = __builtin_amdgcn_exp2f(at - a);
+    sh.dl[d] = at - a;
     sh.F[d] = __builtin_amdgcn_exp2f(a);
   }
 }
 
-// ---- 6. per-thread min-sums: p_v = e_t,v 2^(a_t), q_v = e_d,v 2^(a_d), so
-// min(p_v, q_v) = 2^(a_d) min(e_t,v G, e_d,v) with G = 2^(a_t - a_d); the factor 2^(a_d) is
-// applied to the group sum ----
+// ---- 6. per-thread min-sums, from the logits again: with u_v = z_t,v c - o_t and
+// w_v = z_d,v c - o_d (formed exactly as for the sums), p_v = 2^(u_v + a_t) and
+// q_v = 2^(w_v + a_d), so min(p_v, q_v) = 2^(a_d) 2^min(u_v + a_t - a_d, w_v); the factor
+// 2^(a_d) is applied to the group sum ----
 template <int DT, int D, typename L>
-__device__ __forceinline__ void thread_minsums(const ItemPos& q,
-                                               const float (&x)[D + 1][Vec<DT>::kElems], L& sh,
-                                               int t) {
+__device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos& q,
+                                               const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                               int bf, int t) {
   constexpr int E = Vec<DT>::kElems;
+  float u[E];
+  typename Vec<DT>::Raw xt = raw[0];
+  launder(xt);
+  Vec<DT>::unpack(xt, u);
+  const float ot = exp_offset(sh.o[bf][0]);
+#pragma unroll
+  for (int e = 0; e < E; ++e) u[e] = fmaf(u[e], A.c, -ot);
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     if (d >= q.n) continue;
-    const float G = sh.G[d];
+    float w[E];
+    typename Vec<DT>::Raw xd = raw[d + 1];
+    launder(xd);
+    Vec<DT>::unpack(xd, w);
+    const float od = exp_offset(sh.o[bf][d + 1]);
+    const float dl = sh.dl[d];
     float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const float y = min_pos(x[0][e] * G, x[d + 1][e]);
+      // both operands are results of arithmetic, so fminf needs no canonicalising; a NaN
+      // (-inf + inf when a whole slice is -inf) loses to the other operand, which is then -inf
+      const float y = __builtin_amdgcn_exp2f(fminf(u[e] + dl, fmaf(w[e], A.c, -od)));
       if (e & 1) a1 += y;
       else a0 += y;
     }
@@ -449,15 +488,17 @@ __device__ __forceinline__ void thread_minsums(const ItemPos& q,
 }
 
 // A team of S workgroups (slot s takes slice s of every item) works through row sets: its
-// first two are sets T and T + teams (T = team), later ones are claimed two items ahead by
-// the team's leader from a device-wide counter and posted in the team's mailbox ring, so teams
-// that run faster (the wave arbiter favours older waves) take more sets and all finish within
-// an item of each other. The loads of the next item fly while the current one is reduced and
-// exchanged; its e_v stay in registers for the min-sum.
+// first three are sets T, T + teams and T + 2 teams (T = team), later ones are claimed three
+// items ahead by the team's leader from a device-wide counter and posted in the team's
+// mailbox ring, so teams that run faster (the wave arbiter favours older waves) take more sets
+// and all finish within an item of each other.
+// With alpha two items are in flight per workgroup: iteration j folds item j (published in the
+// previous iteration), issues the loads of item j + 2, takes the statistics of item j + 1 and
+// publishes them, and only then waits for item j's normalisers and takes its min-sums from the
+// logits again. The exchange of one item thus overlaps the statistics of the next.
 template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
 __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   using Raw = typename Vec<DT>::Raw;
-  constexpr int E = Vec<DT>::kElems;
   constexpr int RM = D + 1;
   __shared__ TeamLds<D, NEED_ARG> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -467,10 +508,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   const int teams = gridDim.x / S;
   const int T = blockIdx.x / S, slot = blockIdx.x - T * S;
   const uint32_t nsets = (uint32_t)(A.items / S);
+  constexpr int kStatic = NEED_SUM ? 3 : 2;  // items per team with a fixed row set
   // slot 0 folds row 0 of every item, so it waits for the whole team each item: it can never
   // be more than one item ahead of any member, which keeps a ring of 4 mailbox words safe
   const bool leader = slot == 0;
-  const bool dynamic = teams < (int)nsets;  // else every team has exactly its first set
+  const bool dynamic = kStatic * teams < (int)nsets;  // else no team has more than its fixed sets
   uint32_t tag = 0;  // the call's tag: read once the first loads are in flight
   uint64_t* mbox = A.mbox + (size_t)T * 4;
   if (t < kMaxRows) {
@@ -480,78 +522,125 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   }
   __syncthreads();
 
-  // leader: claim the row set of the team's item j >= 2 and post it (the counter starts past
-  // the sets of every team's first two items, so a set is never claimed twice, and once a
-  // team's next item has none every later claim has none either)
+  // the row set of the team's item j < kStatic
+  auto fixed_set = [&](int j) { return min((uint32_t)(T + j * teams), nsets); };
+  // leader: claim the row set of the team's item j >= kStatic and post it (the counter starts
+  // past every team's fixed sets, so a set is never claimed twice, and once a team's next item
+  // has none every later claim has none either)
   auto claim = [&](int j) __attribute__((always_inline)) {
     if (!dynamic || !leader || t != 0) return;
-    const uint32_t v = 2u * (uint32_t)teams + __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED,
-                                                                    __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t v = (uint32_t)(kStatic * teams) +
+                       __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
     put_word(mbox + (j & 3), mbox_word(min(v, nsets), j, tag));
   };
-  // thread 0: the row set of the team's item j >= 1 (nsets: none left) into LDS, so that all
-  // waves of the workgroup take the same one after the next barrier
-  auto post_next = [&](int j) __attribute__((always_inline)) {
-    if (t != 0) return;
-    if (j == 1) sh.next = min((uint32_t)(T + teams), nsets);
-    else sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
+  // thread 0: the row set of the team's item j >= kStatic (nsets: none left) into LDS, so that
+  // all waves of the workgroup take the same one after the next barrier
+  auto post_set = [&](int j) __attribute__((always_inline)) {
+    if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
   };
 
-  Raw nxt[RM];
-  float x[RM][E];  // the current item's logits, then its e_v
-  uint32_t set = (uint32_t)T;
-  fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), sh, nxt);
-  HS_STAMP_WG(1);
-  // the call's tag is first needed after the first loads are in flight
-  tag = call_tag(A.epoch);
-  if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
-  for (int j = 0; set < nsets; ++j) {
-    const int it = (int)set * S + slot;
-    const ItemPos q = item_pos(A, it, D);
-    HS_STAMP(0);
-    // the team waits for this workgroup's statistics: ahead of co-resident waves until they
-    // are published
-    __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
-    mask_tail<DT, D>(A, q, nxt);
-    thread_max<DT, D, NEED_ARG>(A, q, nxt, x, sh, t);
-    post_next(j + 1);
-    claim(j + 2);
-    __syncthreads();
-    HS_STAMP(1);
-    const uint32_t next = sh.next;
-    if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), sh, nxt);
-    const bool has_rows = wv * 4 <= q.n;  // this wave holds the group of a row
-    const bool row_lead = gl == 0 && gi <= q.n;
-    float m = 0.0f;
-    int idx = 0;
-    if (has_rows) {
-      group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
-      if (NEED_SUM && row_lead) sh.o[gi] = m != -INFINITY ? m * A.c : -INFINITY;
-      if (!NEED_SUM && row_lead) publish_row<false, NEED_ARG>(A, q, gi, tag, m, 0.0f, idx, RM);
+  if constexpr (!NEED_SUM) {
+    // argmax only: max stage, publish, fold
+    Raw nxt[RM];
+    uint32_t set = (uint32_t)T, next = fixed_set(1);
+    fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), true, sh, nxt);
+    HS_STAMP_WG(1);
+    tag = call_tag(A.epoch);  // first needed once the first loads are in flight
+    if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
+    for (int j = 0; set < nsets; ++j) {
+      const ItemPos q = item_pos(A, (int)set * S + slot, D);
+      HS_STAMP(0);
+      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      mask_tail<DT, D>(A, q, nxt);
+      thread_max<DT, D, NEED_ARG>(A, q, nxt, sh, t);
+      if (j >= 1) post_set(j + 1);
+      claim(j + 2);
+      __syncthreads();
+      HS_STAMP(1);
+      if (j >= 1) next = sh.next;
+      if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), true, sh, nxt);
+      if (wv * 4 <= q.n) {
+        float m;
+        int idx;
+        group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
+        if (gl == 0 && gi <= q.n) publish_row<false, NEED_ARG>(A, q, gi, tag, m, 0.0f, idx, RM);
+      }
+      HS_STAMP(3);
+      fold_item<D, false, NEED_ARG>(A, q, tag, lane, wv);
+      __builtin_amdgcn_s_setprio(0);
+      __syncthreads();  // the LDS rows are free for the next item
+      HS_STAMP(7);
+      set = next;
     }
-    if constexpr (NEED_SUM) {
+  } else {
+    // statistics of item q from raw (bf: its offset buffer), published
+    auto stats = [&](const ItemPos& q, Raw (&raw)[RM], int bf) __attribute__((always_inline)) {
+      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      mask_tail<DT, D>(A, q, raw);
+      thread_max<DT, D, NEED_ARG>(A, q, raw, sh, t);
       __syncthreads();
-      HS_STAMP(2);
-      thread_exps<DT, D>(A, q, x, sh, t);
+      const bool rows = wv * 4 <= q.n;  // this wave holds the group of a row
+      float m = 0.0f;
+      int idx = 0;
+      if (rows) {
+        group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
+        if (gl == 0 && gi <= q.n) sh.o[bf][gi] = m != -INFINITY ? m * A.c : -INFINITY;
+      }
       __syncthreads();
-      if (has_rows) {
+      thread_sums<DT, D>(A, q, raw, sh, bf, t);
+      __syncthreads();
+      if (rows) {
         float v[16];
         group_read(&sh.xt[min(gi, q.n)][0], gl, v);
         const float s = row16_sum(sum16(v));
-        if (row_lead) publish_row<true, NEED_ARG>(A, q, gi, tag, m, s, idx, RM);
+        if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, s, idx, RM);
       }
-    }
-    HS_STAMP(3);
-    fold_item<D, NEED_SUM, NEED_ARG>(A, q, tag, lane, wv);
-    __builtin_amdgcn_s_setprio(0);
-    HS_STAMP(4);
-    if constexpr (NEED_SUM) {
-      if (wv == 0) await_norms<D>(A, q, tag, sh, lane);
+      __builtin_amdgcn_s_setprio(0);
+    };
+
+    Raw R0[RM], R1[RM], R2[RM];
+    uint32_t set = (uint32_t)T, set1 = fixed_set(1), set2 = fixed_set(2);
+    const ItemPos q0 = item_pos(A, (int)set * S + slot, D);
+    fetch_item<DT, D>(A, q0, true, sh, R0);
+    fetch_item<DT, D>(A, item_pos(A, (int)min(set1, nsets - 1) * S + slot, D), set1 < nsets, sh,
+                      R1);
+    HS_STAMP_WG(1);
+    tag = call_tag(A.epoch);  // first needed once the first loads are in flight
+    if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
+    stats(q0, R0, 0);
+
+    // iteration j: rc holds item j (statistics published), rn item j + 1 (loaded), rp receives
+    // item j + 2. Returns false once the team has no item j + 1.
+    auto iter = [&](int j, Raw (&rc)[RM], Raw (&rn)[RM], Raw (&rp)[RM])
+                    __attribute__((always_inline)) -> bool {
+      const int bf = j & 1;
+      const ItemPos q = item_pos(A, (int)set * S + slot, D);
+      HS_STAMP(0);
+      // the leader's claim of item j + 3 goes out before the fold and is posted after it, so
+      // waiting for its result waits for nothing else
+      const bool claiming = dynamic && leader && t == 0 && set2 < nsets;
+      uint32_t cv = 0;
+      if (claiming)
+        cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
+      __builtin_amdgcn_s_setprio(0);
+      if (claiming)
+        put_word(mbox + ((j + 3) & 3),
+                 mbox_word(min((uint32_t)(kStatic * teams) + cv, nsets), j + 3, tag));
+      HS_STAMP(1);
+      fetch_item<DT, D>(A, item_pos(A, (int)min(set2, nsets - 1) * S + slot, D), set2 < nsets, sh,
+                        rp);
+      if (set1 < nsets) stats(item_pos(A, (int)set1 * S + slot, D), rn, bf ^ 1);
+      HS_STAMP(2);
+      if (set2 < nsets) post_set(j + 3);
+      if (wv == 0) await_norms<D>(A, q, tag, sh, bf, lane);
       __syncthreads();
-      HS_STAMP(5);
-      thread_minsums<DT, D>(q, x, sh, t);
+      HS_STAMP(3);
+      thread_minsums<DT, D>(A, q, rc, sh, bf, t);
       __syncthreads();
-      HS_STAMP(6);
+      HS_STAMP(4);
       if (wv * 4 < q.n) {
         float v[16];
         const int d = min(gi, q.n - 1);
@@ -561,10 +650,18 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
           A.part[((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s] = y * sh.F[gi];
       }
       HS_STAMP(7);
-    } else {
-      __syncthreads();  // the LDS rows are free for the next item
+      if (set1 >= nsets) return false;
+      set = set1;
+      set1 = set2;
+      set2 = set2 < nsets ? sh.next : nsets;
+      return true;
+    };
+    // unrolled by three so that the register buffers rotate without copies
+    for (int j = 0;; j += 3) {
+      if (!iter(j, R0, R1, R2)) break;
+      if (!iter(j + 1, R1, R2, R0)) break;
+      if (!iter(j + 2, R2, R0, R1)) break;
     }
-    set = next;
   }
 }
 
