@@ -123,9 +123,8 @@ size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
  *                workspace that was not zero-filled, or a device too busy with other
  *                work to hold a whole team of workgroups at once, gives NaN alpha and
  *                -2 argmax values instead of a hang.
- * Each logit is read from HBM once per call (two launches: the evaluation, then the
- * fold of per-slice sums into alpha). Results are deterministic (fixed reduction
- * order) for a given shape.
+ * Each logit is read from HBM once per call, in one launch. Results are
+ * deterministic (fixed reduction order) for a given shape.
  */
 int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
                   int64_t V, int dtype, float temperature, int mode, float* alpha, uint8_t* agree,
@@ -184,7 +183,7 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
 
 /*
  * hs_round - one verification round of the whole path, enqueued as two launches
- * (the evaluation; then, per query, the fold into alpha and the learner step): the
+ * (the evaluation; then, per query, the learner step on its alpha or agreement): the
  * work of hs_eval_alpha, then per query hs_accept_len's work, the loss, and the
  * Hedge and NormalHedge updates with that loss (same workspace contract as
  * hs_eval_alpha). Arguments mean what they mean in the calls above. Learner

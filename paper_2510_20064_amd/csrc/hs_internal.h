@@ -161,11 +161,11 @@ struct SliceStat {
 // current ones and nothing has to be cleared.
 struct TeamWs {
   size_t epoch;  // control block: uint32 call counter at +0, the call's fail flag (word) at
-                 // +8, the tag the evaluation used (uint32) at +16, the row-set counter (uint32)
-                 // at +20, then a ring of 4 mailbox words per team at +64
+                 // +8, the row-set counter (uint32) at +20, the count of teams that have
+                 // finished (uint32) at +24, then a ring of 4 mailbox words per team at +64
   size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
   size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
-  size_t part;   // [G][N][S] floats: per-slice sums of min(p, q_i)
+  size_t part;   // [G][N][S] words: per-slice sums of min(p, q_i)
   size_t total;
 };
 
@@ -182,7 +182,7 @@ inline TeamWs team_ws(const TeamGeom& g) {
   L.norm = off;
   off = align256(off + 24 * sets * rows);
   L.part = off;
-  off = align256(off + 4 * (size_t)g.G * g.N * g.S);
+  off = align256(off + 8 * (size_t)g.G * g.N * g.S);
   L.total = off;
   return L;
 }
@@ -244,8 +244,8 @@ struct TailArgs {
 #endif
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
-// Evaluation of one round: the team kernel, then the fold of the per-slice sums into alpha
-// (which also advances the workspace epoch) and, when tail != nullptr, the learner step.
+// Evaluation of one round: the team kernel (which also advances the workspace epoch) and, when
+// tail != nullptr, the learner step on its alpha or agreement.
 int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,
                  float* alpha, uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, char* ws,
                  const TailArgs* tail, hipStream_t stream);

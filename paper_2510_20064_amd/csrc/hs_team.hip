@@ -46,17 +46,18 @@ constexpr int kPollSleep = HS_POLL_SLEEP;  // s_sleep units (64 clocks) between 
 
 struct TeamArgs {
   RowTable rows;
-  int N, K, nsub, S, items;
+  int B, N, K, nsub, S, items;
   int64_t V, nvec;
   float c;
-  const uint32_t* epoch;
+  uint32_t* epoch;     // advanced by the last workgroup to finish
   uint64_t* fail;      // set, with the call's tag, by the first wait that gives up
-  uint32_t* used_tag;  // the tag of this call, for the fold launch
-  uint32_t* next_set;  // row sets claimed beyond each team's first
+  uint32_t* next_set;  // row sets claimed beyond each team's fixed ones
+  uint32_t* finished;  // teams of this launch that have finished
   uint64_t* mbox;      // [teams][4]: the row set of each team's coming items
   uint64_t* stat;  // [sets][D + 1][S][3]
   uint64_t* norm;  // [sets][D + 1][3]
-  float* part;     // [G][N][S]
+  uint64_t* part;  // [G][N][S]
+  float* alpha;
   int32_t* argmax_t;
   int32_t* argmax_d;
   uint8_t* agree;
@@ -195,7 +196,7 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
       if (A.argmax_d) A.argmax_d[oi] = idx;
       if (A.agree) {
         const int it = word_i(await_word(A.norm + (int64_t)set * RM * 3 + 2, tag, A.fail));
-        A.agree[oi] = (uint8_t)(idx == it);
+        A.agree[oi] = (uint8_t)(idx == it && it >= 0);
       }
     }
   }
@@ -487,6 +488,73 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
   }
 }
 
+// ---- 7. alpha of the set's drafters from the slice partials: output d is summed by slot
+// d mod S (wave 1 for the first), lane l taking slices l, l + 64, ... in order, then across the
+// wave ----
+template <int D>
+__device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, uint32_t tag,
+                                           int lane, int wv) {
+  const int S = A.S;
+  for (int d = q.s + ((wv + 3) & 3) * S; d < q.n; d += kWaves * S) {
+    const uint64_t* src = A.part + ((int64_t)q.g * A.N + q.sub * D + d) * S;
+    float v = 0.0f;
+    for (int j0 = 0; j0 < S; j0 += 128) {
+      uint64_t w[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)  // issue every load of the pass before waiting on any
+        if (j0 + lane + 64 * h < S) w[h] = get_word(src + j0 + lane + 64 * h);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int j = j0 + lane + 64 * h;
+        if (j < S) {
+          if ((uint32_t)w[h] != tag) w[h] = await_word(src + j, tag, A.fail);
+          v += word_f(w[h]);
+        }
+      }
+    }
+    v = wave_sum_f(v);
+    // clamped to [0, 1]; a NaN (a lost word upstream) stays NaN
+    if (lane == 0)
+      A.alpha[((int64_t)q.b * A.N + q.sub * D + d) * A.K + q.k] =
+          v != v ? v : fminf(fmaxf(v, 0.0f), 1.0f);
+  }
+}
+
+// ---- 8. end of a workgroup ----
+// A team's leader finishes after it has folded row 0 of the team's last item, so every member
+// has by then read the call's tag and no claim of the team is outstanding; the last leader to
+// finish advances the epoch and resets the counters (one atomic per team, not per workgroup).
+// When a wait of this call gave up, every workgroup that sees the fail flag marks every output
+// (alpha NaN, argmax -2, agreement 0): a wave that took a lost word has seen the flag, so each
+// value computed from one is overwritten by the same workgroup, and outputs of row sets that
+// no team reached are marked too; values written without a lost word are correct either way.
+template <typename L>
+__device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool leader, int teams,
+                                       L& sh, int t) {
+  if (t == 0) {
+    const uint64_t fw = get_word(A.fail);
+    uint32_t flags = ((uint32_t)fw == tag && (fw >> 32) != 0) ? 2u : 0u;
+    if (leader &&
+        __hip_atomic_fetch_add(A.finished, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+            (uint32_t)teams - 1u) {
+      *A.finished = 0u;  // every team has finished: nothing reads these any more
+      *A.next_set = 0u;
+      *A.epoch = *A.epoch + 1u;
+    }
+    sh.next = flags;
+  }
+  __syncthreads();
+  if (sh.next == 0u) return;
+  const int64_t outs = (int64_t)A.B * A.N * A.K;
+  for (int64_t o = t; o < outs; o += kThreads) {
+    if (A.alpha) A.alpha[o] = __int_as_float(0x7FC00000);
+    if (A.agree) A.agree[o] = 0;
+    if (A.argmax_d) A.argmax_d[o] = -2;
+  }
+  if (A.argmax_t)
+    for (int64_t o = t; o < (int64_t)A.B * A.K; o += kThreads) A.argmax_t[o] = -2;
+}
+
 // A team of S workgroups (slot s takes slice s of every item) works through row sets: its
 // first three are sets T, T + teams and T + 2 teams (T = team), later ones are claimed three
 // items ahead by the team's leader from a device-wide counter and posted in the team's
@@ -547,7 +615,6 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), true, sh, nxt);
     HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
-    if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
     for (int j = 0; set < nsets; ++j) {
       const ItemPos q = item_pos(A, (int)set * S + slot, D);
       HS_STAMP(0);
@@ -573,6 +640,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       HS_STAMP(7);
       set = next;
     }
+    finish(A, tag, leader, teams, sh, t);
   } else {
     // statistics of item q from raw (bf: its offset buffer), published
     auto stats = [&](const ItemPos& q, Raw (&raw)[RM], int bf) __attribute__((always_inline)) {
@@ -607,9 +675,9 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
                       R1);
     HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
-    if (blockIdx.x == 0 && t == 0) *A.used_tag = tag;
     stats(q0, R0, 0);
 
+    uint32_t pset = nsets;  // the team's previous item, whose alpha is still to be folded
     // iteration j: rc holds item j (statistics published), rn item j + 1 (loaded), rp receives
     // item j + 2. Returns false once the team has no item j + 1.
     auto iter = [&](int j, Raw (&rc)[RM], Raw (&rn)[RM], Raw (&rp)[RM])
@@ -634,6 +702,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
                         rp);
       if (set1 < nsets) stats(item_pos(A, (int)set1 * S + slot, D), rn, bf ^ 1);
       HS_STAMP(2);
+      // alpha of the previous item, whose partials were stored an iteration ago
+      if (pset < nsets) fold_alpha<D>(A, item_pos(A, (int)pset * S + slot, D), tag, lane, wv);
       if (set2 < nsets) post_set(j + 3);
       if (wv == 0) await_norms<D>(A, q, tag, sh, bf, lane);
       __syncthreads();
@@ -647,10 +717,12 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         group_read(&sh.xp[d][0], gl, v);
         const float y = row16_sum(sum16(v));
         if (gl == 0 && gi < q.n)
-          A.part[((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s] = y * sh.F[gi];
+          put_word(A.part + ((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s,
+                   word_of(y * sh.F[gi], tag));
       }
       HS_STAMP(7);
       if (set1 >= nsets) return false;
+      pset = set;
       set = set1;
       set1 = set2;
       set2 = set2 < nsets ? sh.next : nsets;
@@ -662,104 +734,9 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (!iter(j + 1, R1, R2, R0)) break;
       if (!iter(j + 2, R2, R0, R1)) break;
     }
+    fold_alpha<D>(A, item_pos(A, (int)set * S + slot, D), tag, lane, wv);
+    finish(A, tag, leader, teams, sh, t);
   }
-}
-
-// ---- 7. alpha from the slice partials; advances the epoch ----------------------------------
-
-struct FoldArgs {
-  const float* part;  // NULL: no alpha
-  float* alpha;
-  uint8_t* agree;
-  int32_t* argmax_t;
-  int32_t* argmax_d;
-  int B, N, K, S;
-  int alpha_lds;  // hs_round_tail_kernel: keep alpha in LDS for the learner
-  uint32_t* epoch;
-  const uint64_t* fail;
-  const uint32_t* used_tag;
-  uint32_t* next_set;
-};
-
-// Fold of outputs [o0, o0 + n) (n <= 64) by one workgroup (out_lds: also alpha of output
-// o0 + j to out_lds[j]): 4 threads per output, thread r of
-// the four summing slices r, r + 4, ... in order, then the four combined in a fixed order on
-// the DPP network; alpha is clamped to [0, 1]. If a wait of the evaluation gave up, the
-// outputs are marked instead: alpha NaN, argmax -2, agreement 0 (flag and tag were written by
-// the previous launch; their loads are issued with the partials').
-__device__ __forceinline__ void fold_chunk(const FoldArgs& A, int64_t o0, int n,
-                                           float* out_lds = nullptr) {
-  const int t = threadIdx.x, lo = t >> 2, r = t & 3;
-  const int64_t o = o0 + lo;
-  const bool mine = lo < n;
-  const int k = mine ? (int)(o % A.K) : 0;
-  const int64_t bi = o / A.K;
-  const int i = mine ? (int)(bi % A.N) : 0;
-  const int64_t b = bi / A.N;
-  const uint32_t tag = *A.used_tag;
-  const uint64_t fw = *A.fail;
-  float v = 0.0f;
-  if (A.part && mine) {
-    // slices r, r + 4, ... in order; 16 loads in flight at a time
-    const float* src = A.part + ((b * A.K + k) * A.N + i) * A.S;
-    for (int j0 = r; j0 < A.S; j0 += 64) {
-      float x[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) x[u] = j0 + 4 * u < A.S ? src[j0 + 4 * u] : 0.0f;
-#pragma unroll
-      for (int u = 0; u < 16; ++u) v += x[u];
-    }
-  }
-  v += dpp_f<0xB1>(v);  // quad_perm [1,0,3,2]
-  v += dpp_f<0x4E>(v);  // quad_perm [2,3,0,1]
-  if (!mine || r != 0) return;
-  if ((uint32_t)fw == tag && (fw >> 32) != 0) {
-    if (A.alpha) A.alpha[o] = __int_as_float(0x7FC00000);
-    if (out_lds) out_lds[lo] = __int_as_float(0x7FC00000);
-    if (A.agree) A.agree[o] = 0;
-    if (A.argmax_d) A.argmax_d[o] = -2;
-    if (A.argmax_t && i == 0) A.argmax_t[b * A.K + k] = -2;
-  } else if (A.part) {
-    const float al = fminf(fmaxf(v, 0.0f), 1.0f);
-    A.alpha[o] = al;
-    if (out_lds) out_lds[lo] = al;
-  }
-}
-// Block 0 advances the epoch and resets the row-set counter; nothing else in the launch
-// reads either.
-__device__ __forceinline__ void next_call(const FoldArgs& A) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    A.epoch[0] = A.epoch[0] + 1u;
-    *A.next_set = 0u;
-  }
-}
-
-constexpr int kFoldOuts = kThreads / 4;  // outputs per workgroup pass
-
-// hs_eval_alpha's second launch: kFoldOuts outputs per workgroup.
-__global__ __launch_bounds__(kThreads) void hs_fold_kernel(FoldArgs A) {
-  next_call(A);
-  const int64_t total = (int64_t)A.B * A.N * A.K;
-  const int64_t o0 = (int64_t)blockIdx.x * kFoldOuts;
-  fold_chunk(A, o0, (int)std::min<int64_t>(kFoldOuts, total - o0));
-}
-
-// hs_round's second launch, one workgroup per query b: fold the query's N * K outputs (kept
-// in LDS after the learner's own LDS when they are its gamma), then wave 0 runs the learner
-// step on them.
-__global__ __launch_bounds__(kThreads) void hs_round_tail_kernel(FoldArgs F, TailArgs a) {
-  extern __shared__ double lds[];
-  next_call(F);
-  const int b = blockIdx.x;
-  const int nk = F.N * F.K;
-  float* al = F.alpha_lds ? reinterpret_cast<float*>(lds + tail_lds_doubles(a)) : nullptr;
-  HS_TSTAMP(0);
-  for (int o = 0; o < nk; o += kFoldOuts)
-    fold_chunk(F, (int64_t)b * nk + o, std::min(kFoldOuts, nk - o), al ? al + o : nullptr);
-  HS_TSTAMP(1);
-  __syncthreads();
-  HS_TSTAMP(2);
-  if (threadIdx.x < 64) tail_query(a, b, lds, al);
 }
 
 // ---- host side -------------------------------------------------------------------------------
@@ -844,6 +821,7 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   const TeamWs L = team_ws(g);
   TeamArgs A{};
   A.rows = rows;
+  A.B = g.B;
   A.N = g.N;
   A.K = g.K;
   A.nsub = g.nsub;
@@ -852,14 +830,15 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.V = g.V;
   A.nvec = g.nvec;
   A.c = c;
-  A.epoch = reinterpret_cast<const uint32_t*>(ws + L.epoch);
+  A.epoch = reinterpret_cast<uint32_t*>(ws + L.epoch);
   A.fail = reinterpret_cast<uint64_t*>(ws + L.epoch + 8);
-  A.used_tag = reinterpret_cast<uint32_t*>(ws + L.epoch + 16);
   A.next_set = reinterpret_cast<uint32_t*>(ws + L.epoch + 20);
+  A.finished = reinterpret_cast<uint32_t*>(ws + L.epoch + 24);
   A.mbox = reinterpret_cast<uint64_t*>(ws + L.epoch + 64);
   A.stat = reinterpret_cast<uint64_t*>(ws + L.stat);
   A.norm = reinterpret_cast<uint64_t*>(ws + L.norm);
-  A.part = need_sum ? reinterpret_cast<float*>(ws + L.part) : nullptr;
+  A.part = need_sum ? reinterpret_cast<uint64_t*>(ws + L.part) : nullptr;
+  A.alpha = need_sum ? alpha : nullptr;
   A.argmax_t = argmax_t;
   A.argmax_d = argmax_d;
   A.agree = agree;
@@ -869,27 +848,16 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   int rc = dispatch<Launch>(g, need_sum, need_arg, A, g, stream);
   if (rc) return rc;
   if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
-
-  FoldArgs F{A.part, alpha, agree, argmax_t, argmax_d, g.B, g.N, g.K, g.S, 0,
-             reinterpret_cast<uint32_t*>(ws + L.epoch), A.fail, A.used_tag, A.next_set};
-  if (tail) {  // fold and learner step in one launch
+  if (tail) {  // the learner step on this call's alpha or agreement
 #ifdef HS_TRACE
     TailArgs tt = *tail;
     tt.trace = g_trace ? g_trace + (size_t)g.items * 8 + 2 * kMaxTeams : nullptr;
-    tail = &tt;
+    return launch_tail(tt, stream);
+#else
+    return launch_tail(*tail, stream);
 #endif
-    size_t lds = sizeof(double) * (size_t)tail_lds_doubles(*tail);
-    const size_t al = sizeof(float) * (size_t)g.N * g.K;
-    if (tail->gamma_src == 1 && A.part && lds + al <= 65536) {
-      F.alpha_lds = 1;
-      lds += al;
-    }
-    hs_round_tail_kernel<<<g.B, kThreads, lds, stream>>>(F, *tail);
-  } else {
-    const int64_t outs = (int64_t)g.B * g.N * g.K;
-    hs_fold_kernel<<<(unsigned)((outs + kFoldOuts - 1) / kFoldOuts), kThreads, 0, stream>>>(F);
   }
-  return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
+  return HS_OK;
 }
 
 }  // namespace hs
