@@ -166,6 +166,7 @@ struct TeamWs {
   size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
   size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
   size_t part;   // [G][N][S] words: per-slice sums of min(p, q_i)
+  size_t gw;     // [B][N][K] words: gamma (alpha or agreement) for a learner in the same launch
   size_t total;
 };
 
@@ -183,6 +184,8 @@ inline TeamWs team_ws(const TeamGeom& g) {
   off = align256(off + 24 * sets * rows);
   L.part = off;
   off = align256(off + 8 * (size_t)g.G * g.N * g.S);
+  L.gw = off;
+  off = align256(off + 8 * (size_t)g.B * g.N * g.K);
   L.total = off;
   return L;
 }

@@ -89,8 +89,10 @@ __host__ __device__ inline int tail_lds_doubles(const TailArgs& a) {
 }
 
 // Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
+// gamma_lds (optional): the query's gamma as [N][M] floats in LDS, instead of a.alpha / a.agree.
 // Every input is loaded before anything is stored, so the loads are in flight together.
-__device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds) {
+__device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds,
+                                           const float* gamma_lds = nullptr) {
   const int i = threadIdx.x & 63;
   const int N = a.N, M = a.M;
   const bool act = i < N;
@@ -112,7 +114,8 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
     int len = 0;
     auto gamma_at = [&](int n) -> double {
       const int64_t o = ((int64_t)b * N + i) * M + n;
-      return (a.gamma_src == 1) ? (double)a.alpha[o] : (double)a.agree[o];
+      return gamma_lds ? (double)gamma_lds[i * M + n]
+                       : (a.gamma_src == 1) ? (double)a.alpha[o] : (double)a.agree[o];
     };
     if (act && !a.tree) {
       // chain: one pass in position order, the prefix product carried in a register

@@ -61,6 +61,12 @@ struct TeamArgs {
   int32_t* argmax_t;
   int32_t* argmax_d;
   uint8_t* agree;
+  // learner step in the same launch (learn != 0; alpha kernels only): gamma words gw [B][N][K]
+  // are written by the folders (gamma = alpha when learn == 1, agreement when learn == 2), and
+  // workgroup b (mod the grid) runs query b's step once it has finished its own items
+  int learn;
+  uint64_t* gw;
+  TailArgs tail;
 #ifdef HS_TRACE
   uint64_t* trace;  // [items][8] phase timestamps of workgroup thread 0
 #endif
@@ -196,7 +202,9 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
       if (A.argmax_d) A.argmax_d[oi] = idx;
       if (A.agree) {
         const int it = word_i(await_word(A.norm + (int64_t)set * RM * 3 + 2, tag, A.fail));
-        A.agree[oi] = (uint8_t)(idx == it && it >= 0);
+        const bool ag = idx == it && it >= 0;
+        A.agree[oi] = (uint8_t)ag;
+        if (A.learn == 2) put_word(A.gw + oi, word_of(ag ? 1.0f : 0.0f, tag));
       }
     }
   }
@@ -514,10 +522,30 @@ __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, 
     }
     v = wave_sum_f(v);
     // clamped to [0, 1]; a NaN (a lost word upstream) stays NaN
-    if (lane == 0)
-      A.alpha[((int64_t)q.b * A.N + q.sub * D + d) * A.K + q.k] =
-          v != v ? v : fminf(fmaxf(v, 0.0f), 1.0f);
+    if (lane == 0) {
+      const int64_t o = ((int64_t)q.b * A.N + q.sub * D + d) * A.K + q.k;
+      const float al = v != v ? v : fminf(fmaxf(v, 0.0f), 1.0f);
+      A.alpha[o] = al;
+      if (A.learn == 1) put_word(A.gw + o, word_of(al, tag));
+    }
   }
+}
+
+// ---- 9. learner step of query b, once this workgroup has finished its items: the query's
+// N * K gamma words are gathered into LDS (the team buffers are free by now), then wave 0 runs
+// the step. The host only asks for it when the learner's LDS fits in the team's. ----
+template <typename L>
+__device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int b, L& sh,
+                                            int t) {
+  const int nk = A.N * A.K;
+  double* lds = reinterpret_cast<double*>(&sh);
+  float* gam = reinterpret_cast<float*>(lds + tail_lds_doubles(A.tail));
+  const uint64_t* src = A.gw + (int64_t)b * nk;
+  __syncthreads();  // the team buffers are no longer read
+  for (int o = t; o < nk; o += kThreads) gam[o] = word_f(await_word(src + o, tag, A.fail));
+  __syncthreads();
+  if (t < 64) tail_query(A.tail, b, lds, gam);
+  __syncthreads();
 }
 
 // ---- 8. end of a workgroup ----
@@ -735,6 +763,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (!iter(j + 2, R2, R0, R1)) break;
     }
     fold_alpha<D>(A, item_pos(A, (int)set * S + slot, D), tag, lane, wv);
+    if (A.learn)
+      for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
     finish(A, tag, leader, teams, sh, t);
   }
 }
@@ -761,14 +791,22 @@ int capacity_t() {
   return v;
 }
 
+// *learned: whether the launch runs the learner step itself (its LDS fits in the team's).
 template <int DT, int D, bool NS, bool NA>
-int launch_t(const TeamArgs& A, const TeamGeom& g, hipStream_t stream) {
+int launch_t(TeamArgs A, const TeamGeom& g, hipStream_t stream, bool* learned) {
   // as many teams as the device holds at once, no more than there are row sets or rings
   const int64_t sets = g.items / g.S;
   const int64_t teams =
       std::min<int64_t>({capacity_t<DT, D, NS, NA>() / g.S, sets, (int64_t)kMaxTeams});
   if (teams <= 0) return HS_ERR_LIMIT;
   const int64_t P = teams * g.S;
+  if (A.learn) {  // only the alpha kernels carry the learner (it would cost the argmax-only
+                  // kernels a workgroup per CU in registers)
+    const size_t need = sizeof(double) * (size_t)tail_lds_doubles(A.tail) +
+                        sizeof(float) * (size_t)g.N * g.K;
+    if (!NS || need > sizeof(TeamLds<D, NA>)) A.learn = 0;
+  }
+  *learned = A.learn != 0;
   hs_team_kernel<DT, D, NS, NA><<<(unsigned)P, kThreads, 0, stream>>>(A);
 #ifdef HS_TRACE
   fprintf(stderr, "team grid %lld S %d items %lld\n", (long long)P, g.S, (long long)g.items);
@@ -804,8 +842,8 @@ struct Capacity {
 };
 template <int DT, int D, bool NS, bool NA>
 struct Launch {
-  static int run(const TeamArgs& A, const TeamGeom& g, hipStream_t s) {
-    return launch_t<DT, D, NS, NA>(A, g, s);
+  static int run(const TeamArgs& A, const TeamGeom& g, hipStream_t s, bool* learned) {
+    return launch_t<DT, D, NS, NA>(A, g, s, learned);
   }
 };
 
@@ -845,18 +883,19 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
 #ifdef HS_TRACE
   A.trace = g_trace;
 #endif
-  int rc = dispatch<Launch>(g, need_sum, need_arg, A, g, stream);
-  if (rc) return rc;
-  if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
-  if (tail) {  // the learner step on this call's alpha or agreement
+  if (tail) {  // the learner step in the same launch, when its LDS fits
+    A.learn = tail->gamma_src;
+    A.gw = reinterpret_cast<uint64_t*>(ws + L.gw);
+    A.tail = *tail;
 #ifdef HS_TRACE
-    TailArgs tt = *tail;
-    tt.trace = g_trace ? g_trace + (size_t)g.items * 8 + 2 * kMaxTeams : nullptr;
-    return launch_tail(tt, stream);
-#else
-    return launch_tail(*tail, stream);
+    A.tail.trace = g_trace ? g_trace + (size_t)g.items * 8 + 2 * kMaxTeams : nullptr;
 #endif
   }
+  bool learned = false;
+  int rc = dispatch<Launch>(g, need_sum, need_arg, A, g, stream, &learned);
+  if (rc) return rc;
+  if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
+  if (tail && !learned) return launch_tail(A.tail, stream);  // a launch of its own
   return HS_OK;
 }
 
