@@ -46,6 +46,10 @@ constexpr int kPollSleep = HS_POLL_SLEEP;  // s_sleep units (64 clocks) between 
 
 struct TeamArgs {
   RowTable rows;
+  // drafter rows at one constant distance (uni != 0): row bases from these scalars instead of
+  // the row table, so the kernel does not wait for the table at its start
+  int uni;
+  int64_t dd;  // bytes from drafter i's row (b, k) to drafter i + 1's
   int B, N, K, nsub, S, items;
   int64_t V, nvec;
   float c;
@@ -240,6 +244,7 @@ struct TeamLds {
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
   float o[2][D + 1];                          // slice offsets fl(m c)
   float dl[D];                                // a_t - a_d, a_x = (o_x - hi_x) - lo_x
+  float G[D];                                 // 2^(a_t - a_d)
   float F[D];                                 // 2^(a_d)
   uint32_t next;  // a row set of the team's coming items, posted by thread 0
   // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
@@ -257,26 +262,42 @@ struct TeamLds {
 // control block instead (a cache-resident dummy, never used). The one partial vector at the
 // end of a row (V not a multiple of the vector width) is then re-read element by element, in
 // a branch taken only by the slice that holds it.
-template <int DT, int D, typename L>
+template <int DT, int D, bool UNI = false, typename L>
 __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, bool valid,
                                            const L& sh, typename Vec<DT>::Raw (&dst)[D + 1]) {
   using Vt = Vec<DT>;
   constexpr int E = Vt::kElems;
   const int64_t vfull = A.V / E;  // complete 16-byte vectors per row
-  // lane r <= n: the base of row r of the item, then broadcast
-  const int l = threadIdx.x & 63;
-  uint64_t base = reinterpret_cast<uint64_t>(A.epoch);
-  if (valid && l <= q.n) {
-    const int row = l == 0 ? 0 : q.sub * D + l;
-    base = reinterpret_cast<uint64_t>(sh.ptr[row]) +
-           (uint64_t)(((int64_t)q.b * sh.sb[row] + (int64_t)q.k * sh.sk[row]) * Vt::kBytes);
-  }
+  const uint64_t dummy = reinterpret_cast<uint64_t>(A.epoch);
   uint64_t rb[D + 1];
+  if (UNI && A.uni) {
+    // drafters at a constant distance: uniform scalar arithmetic
+    rb[0] = valid ? reinterpret_cast<uint64_t>(A.rows.ptr[0]) +
+                        (uint64_t)(((int64_t)q.b * A.rows.sb[0] + (int64_t)q.k * A.rows.sk[0]) *
+                                   Vt::kBytes)
+                  : dummy;
+    const uint64_t d0 = reinterpret_cast<uint64_t>(A.rows.ptr[1]) +
+                        (uint64_t)(((int64_t)q.b * A.rows.sb[1] + (int64_t)q.k * A.rows.sk[1]) *
+                                   Vt::kBytes) +
+                        (uint64_t)((int64_t)q.sub * D * A.dd);
 #pragma unroll
-  for (int r = 0; r <= D; ++r) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, r);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), r);
-    rb[r] = ((uint64_t)hi << 32) | lo;
+    for (int r = 1; r <= D; ++r)
+      rb[r] = valid && r <= q.n ? d0 + (uint64_t)((int64_t)(r - 1) * A.dd) : dummy;
+  } else {
+    // lane r <= n: the base of row r of the item from the table in LDS, then broadcast
+    const int l = threadIdx.x & 63;
+    uint64_t base = dummy;
+    if (valid && l <= q.n) {
+      const int row = l == 0 ? 0 : q.sub * D + l;
+      base = reinterpret_cast<uint64_t>(sh.ptr[row]) +
+             (uint64_t)(((int64_t)q.b * sh.sb[row] + (int64_t)q.k * sh.sk[row]) * Vt::kBytes);
+    }
+#pragma unroll
+    for (int r = 0; r <= D; ++r) {
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, r);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), r);
+      rb[r] = ((uint64_t)hi << 32) | lo;
+    }
   }
   // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
   // 16-byte load
@@ -454,7 +475,56 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
   if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
     const int d = (lane >> 1) - 1;
     sh.dl[d] = at - a;
+    sh.G[d] = __builtin_amdgcn_exp2f(at - a);
     sh.F[d] = __builtin_amdgcn_exp2f(a);
+  }
+}
+
+// ---- 3'. exponentials kept in registers (workgroups with a single item): e_v = exp2(z_v c - o)
+// against the slice offsets (buffer 0) into x, per-thread sums to LDS ----
+template <int DT, int D, typename L>
+__device__ __forceinline__ void thread_exps_kept(const TeamArgs& A, const ItemPos& q,
+                                                 const typename Vec<DT>::Raw (&raw)[D + 1],
+                                                 float (&x)[D + 1][Vec<DT>::kElems], L& sh,
+                                                 int t) {
+  constexpr int E = Vec<DT>::kElems;
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    if (r > q.n) continue;
+    typename Vec<DT>::Raw xr = raw[r];
+    launder(xr);
+    Vec<DT>::unpack(xr, x[r]);
+    const float oc = exp_offset(sh.o[0][r]);
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, -oc));
+      if (e & 1) a1 += x[r][e];
+      else a0 += x[r][e];
+    }
+    sh.xt[r][t] = a0 + a1;
+  }
+}
+
+// ---- 6'. per-thread min-sums from kept e_v: min(p_v, q_v) = 2^(a_d) min(e_t,v G, e_d,v) with
+// G = 2^(a_t - a_d); one multiply, one min and one add per drafter logit ----
+template <int DT, int D, typename L>
+__device__ __forceinline__ void thread_minsums_kept(const ItemPos& q,
+                                                    const float (&x)[D + 1][Vec<DT>::kElems],
+                                                    L& sh, int t) {
+  constexpr int E = Vec<DT>::kElems;
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    if (d >= q.n) continue;
+    const float G = sh.G[d];
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float y = min_pos(x[0][e] * G, x[d + 1][e]);
+      if (e & 1) a1 += y;
+      else a0 += y;
+    }
+    sh.xp[d][t] = a0 + a1;
   }
 }
 
@@ -592,7 +662,9 @@ __device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool lea
 // previous iteration), issues the loads of item j + 2, takes the statistics of item j + 1 and
 // publishes them, and only then waits for item j's normalisers and takes its min-sums from the
 // logits again. The exchange of one item thus overlaps the statistics of the next.
-template <int DT, int D, bool NEED_SUM, bool NEED_ARG>
+// SINGLE (alpha kernels only): every team has exactly one item, so nothing is pipelined, the
+// e_v stay in registers and drafters at a constant distance are addressed without the table.
+template <int DT, int D, bool NEED_SUM, bool NEED_ARG, bool SINGLE>
 __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   using Raw = typename Vec<DT>::Raw;
   constexpr int RM = D + 1;
@@ -611,7 +683,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   const bool dynamic = kStatic * teams < (int)nsets;  // else no team has more than its fixed sets
   uint32_t tag = 0;  // the call's tag: read once the first loads are in flight
   uint64_t* mbox = A.mbox + (size_t)T * 4;
-  if (t < kMaxRows) {
+  if (!(SINGLE && A.uni) && t < kMaxRows) {
     sh.ptr[t] = reinterpret_cast<const char*>(A.rows.ptr[t]);
     sh.sb[t] = A.rows.sb[t];
     sh.sk[t] = A.rows.sk[t];
@@ -695,10 +767,68 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       __builtin_amdgcn_s_setprio(0);
     };
 
+    // the item's slice partials to the workspace (after a barrier), as tagged words
+    auto store_partials = [&](const ItemPos& q) __attribute__((always_inline)) {
+      if (wv * 4 < q.n) {
+        float v[16];
+        const int d = min(gi, q.n - 1);
+        group_read(&sh.xp[d][0], gl, v);
+        const float y = row16_sum(sum16(v));
+        if (gl == 0 && gi < q.n)
+          put_word(A.part + ((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s,
+                   word_of(y * sh.F[gi], tag));
+      }
+    };
+
     Raw R0[RM], R1[RM], R2[RM];
     uint32_t set = (uint32_t)T, set1 = fixed_set(1), set2 = fixed_set(2);
     const ItemPos q0 = item_pos(A, (int)set * S + slot, D);
-    fetch_item<DT, D>(A, q0, true, sh, R0);
+    fetch_item<DT, D, SINGLE>(A, q0, true, sh, R0);
+    if constexpr (SINGLE) {
+      // one item per workgroup: nothing to overlap, so its e_v stay in registers
+      HS_STAMP_WG(1);
+      tag = call_tag(A.epoch);  // first needed once the first loads are in flight
+      const ItemPos& q = q0;
+      float x[RM][Vec<DT>::kElems];
+      HS_STAMP(0);
+      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      mask_tail<DT, D>(A, q, R0);
+      thread_max<DT, D, NEED_ARG>(A, q, R0, sh, t);
+      __syncthreads();
+      const bool rows = wv * 4 <= q.n;
+      float m = 0.0f;
+      int idx = 0;
+      if (rows) {
+        group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
+        if (gl == 0 && gi <= q.n) sh.o[0][gi] = m != -INFINITY ? m * A.c : -INFINITY;
+      }
+      __syncthreads();
+      thread_exps_kept<DT, D>(A, q, R0, x, sh, t);
+      __syncthreads();
+      if (rows) {
+        float v[16];
+        group_read(&sh.xt[min(gi, q.n)][0], gl, v);
+        const float sm = row16_sum(sum16(v));
+        if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, sm, idx, RM);
+      }
+      HS_STAMP(1);
+      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
+      __builtin_amdgcn_s_setprio(0);
+      HS_STAMP(2);
+      if (wv == 0) await_norms<D>(A, q, tag, sh, 0, lane);
+      __syncthreads();
+      HS_STAMP(3);
+      thread_minsums_kept<DT, D>(q, x, sh, t);
+      __syncthreads();
+      HS_STAMP(4);
+      store_partials(q);
+      HS_STAMP(7);
+      fold_alpha<D>(A, q, tag, lane, wv);
+      if (A.learn)
+        for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
+      finish(A, tag, leader, teams, sh, t);
+      return;
+    }
     fetch_item<DT, D>(A, item_pos(A, (int)min(set1, nsets - 1) * S + slot, D), set1 < nsets, sh,
                       R1);
     HS_STAMP_WG(1);
@@ -739,15 +869,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
       __syncthreads();
       HS_STAMP(4);
-      if (wv * 4 < q.n) {
-        float v[16];
-        const int d = min(gi, q.n - 1);
-        group_read(&sh.xp[d][0], gl, v);
-        const float y = row16_sum(sum16(v));
-        if (gl == 0 && gi < q.n)
-          put_word(A.part + ((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s,
-                   word_of(y * sh.F[gi], tag));
-      }
+      store_partials(q);
       HS_STAMP(7);
       if (set1 >= nsets) return false;
       pset = set;
@@ -774,7 +896,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
 namespace {
 
 // Workgroups of the team kernel the current device holds at once.
-template <int DT, int D, bool NS, bool NA>
+template <int DT, int D, bool NS, bool NA, bool SG>
 int capacity_t() {
   static std::atomic<int> cached[64];  // per device; 0 = not yet known
   int dev = 0;
@@ -782,7 +904,7 @@ int capacity_t() {
   int v = cached[dev].load(std::memory_order_relaxed);
   if (v > 0) return v;
   int per_cu = 0, cus = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, hs_team_kernel<DT, D, NS, NA>,
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, hs_team_kernel<DT, D, NS, NA, SG>,
                                                    kThreads, 0) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
@@ -791,13 +913,17 @@ int capacity_t() {
   return v;
 }
 
+// Runs the team kernel with as many teams as the device holds at once (no more than there are
+// row sets or mailbox rings); the single-item kernel when that covers every row set.
 // *learned: whether the launch runs the learner step itself (its LDS fits in the team's).
 template <int DT, int D, bool NS, bool NA>
 int launch_t(TeamArgs A, const TeamGeom& g, hipStream_t stream, bool* learned) {
-  // as many teams as the device holds at once, no more than there are row sets or rings
   const int64_t sets = g.items / g.S;
+  const bool single = NS && capacity_t<DT, D, NS, NA, NS>() / g.S >= sets;
   const int64_t teams =
-      std::min<int64_t>({capacity_t<DT, D, NS, NA>() / g.S, sets, (int64_t)kMaxTeams});
+      single ? sets
+             : std::min<int64_t>({capacity_t<DT, D, NS, NA, false>() / g.S, sets,
+                                  (int64_t)kMaxTeams});
   if (teams <= 0) return HS_ERR_LIMIT;
   const int64_t P = teams * g.S;
   if (A.learn) {  // only the alpha kernels carry the learner (it would cost the argmax-only
@@ -807,7 +933,8 @@ int launch_t(TeamArgs A, const TeamGeom& g, hipStream_t stream, bool* learned) {
     if (!NS || need > sizeof(TeamLds<D, NA>)) A.learn = 0;
   }
   *learned = A.learn != 0;
-  hs_team_kernel<DT, D, NS, NA><<<(unsigned)P, kThreads, 0, stream>>>(A);
+  if (single) hs_team_kernel<DT, D, NS, NA, NS><<<(unsigned)P, kThreads, 0, stream>>>(A);
+  else hs_team_kernel<DT, D, NS, NA, false><<<(unsigned)P, kThreads, 0, stream>>>(A);
 #ifdef HS_TRACE
   fprintf(stderr, "team grid %lld S %d items %lld\n", (long long)P, g.S, (long long)g.items);
 #endif
@@ -837,8 +964,10 @@ int dispatch(const TeamGeom& g, bool ns, bool na, Args&&... args) {
 }
 
 template <int DT, int D, bool NS, bool NA>
-struct Capacity {
-  static int run() { return capacity_t<DT, D, NS, NA>(); }
+struct Capacity {  // the smaller of the two kernels' (a team must fit in either)
+  static int run() {
+    return std::min(capacity_t<DT, D, NS, NA, false>(), capacity_t<DT, D, NS, NA, NS>());
+  }
 };
 template <int DT, int D, bool NS, bool NA>
 struct Launch {
@@ -859,6 +988,16 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   const TeamWs L = team_ws(g);
   TeamArgs A{};
   A.rows = rows;
+  // drafters at one constant distance with equal strides (e.g. one [N][B][K][V] tensor)
+  A.uni = 1;
+  A.dd = g.N > 1 ? reinterpret_cast<const char*>(rows.ptr[2]) -
+                       reinterpret_cast<const char*>(rows.ptr[1])
+                 : 0;
+  for (int i = 2; i <= g.N && A.uni; ++i)
+    A.uni = reinterpret_cast<const char*>(rows.ptr[i]) -
+                    reinterpret_cast<const char*>(rows.ptr[i - 1]) ==
+                A.dd &&
+            rows.sb[i] == rows.sb[1] && rows.sk[i] == rows.sk[1];
   A.B = g.B;
   A.N = g.N;
   A.K = g.K;

@@ -316,6 +316,25 @@ def test_single_drafter_single_position():
     run_round_and_check(w, x)
 
 
+def test_scattered_drafter_rows_match_contiguous():
+    note("drafter rows in separate allocations (row-table path) vs one tensor (constant-distance "
+         "path): N=9 (a full and a one-drafter row set), V=30001")
+    w = _custom(2, 9, 3, 30001, synth.BF16, ld=30008)
+    x = synth.generate(w)
+    got, _ = check_eval(w, x)  # one tensor: drafters at a constant distance
+    xd = dev_logits(w, x)
+    keep = []  # allocations of uneven size between the copies, in reverse order
+    ds = [None] * w.N
+    for i in reversed(range(w.N)):
+        keep.append(torch.empty(4096 + 37 * i, dtype=torch.uint8, device="cuda"))
+        ds[i] = xd[i + 1].clone()
+    out = hs.eval_alpha(xd[0], ds, V=w.V, temperature=w.temperature, mode=hs.SAMPLE,
+                        want_alpha=True, want_agree=True, want_argmax=True)
+    torch.cuda.synchronize()
+    for k in ("alpha", "agree", "argmax_t", "argmax_d"):
+        assert np.array_equal(out[k].cpu().numpy(), got[k]), k
+
+
 def test_deterministic_rerun_bitwise():
     note("determinism: 5 reruns bitwise equal")
     w = synth.variant(WL["qwen3_8b_single"], K=3)
