@@ -214,18 +214,23 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
   }
 }
 
-// Position of work item `it`: row set, slice, group (b, k), drafters n in the set, and the
-// calling thread's vector index within the row.
+// Position of work item (set, slot): row set, slice, group (b, k), drafters n in the set, and
+// the calling thread's vector index within the row.
 struct ItemPos {
   int set, s, g, sub, b, k, n;
   int vi;  // a row holds fewer than 2^31 logits
 };
-__device__ inline ItemPos item_pos(const TeamArgs& A, int it, int D) {
+__device__ inline ItemPos item_pos(const TeamArgs& A, uint32_t set, int slot, int D) {
   ItemPos q;
-  q.set = it / A.S;
-  q.s = it - q.set * A.S;
-  q.g = q.set / A.nsub;
-  q.sub = q.set - q.g * A.nsub;
+  q.set = (int)set;
+  q.s = slot;
+  if (A.nsub == 1) {
+    q.g = q.set;
+    q.sub = 0;
+  } else {
+    q.g = q.set / A.nsub;
+    q.sub = q.set - q.g * A.nsub;
+  }
   q.b = q.g / A.K;
   q.k = q.g - q.b * A.K;
   q.n = min(D, A.N - q.sub * D);
@@ -243,6 +248,7 @@ struct TeamLds {
   int xi[NEED_ARG ? D + 1 : 1][kThreads];     // per-thread argmax
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
   float o[2][D + 1];                          // slice offsets fl(m c)
+  float no[2][D + 1];                         // -exp_offset(o): the addend of the exponents
   float dl[D];                                // a_t - a_d, a_x = (o_x - hi_x) - lo_x
   float G[D];                                 // 2^(a_t - a_d)
   float F[D];                                 // 2^(a_d)
@@ -354,16 +360,15 @@ __device__ __forceinline__ void launder(Raw& x) {
 // ---- 1. per-thread max (and lowest argmax) of every row of item q, to LDS ----
 template <int DT, int D, bool NEED_ARG, typename L>
 __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
-                                           const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                           typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
                                            int t) {
   constexpr int E = Vec<DT>::kElems;
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
     if (r > q.n) continue;
-    typename Vec<DT>::Raw x = raw[r];
-    launder(x);
+    launder(raw[r]);
     float z[E];
-    Vec<DT>::unpack(x, z);
+    Vec<DT>::unpack(raw[r], z);
     float m = -INFINITY;
     int idx = INT_MAX;
 #pragma unroll
@@ -419,21 +424,20 @@ __device__ __forceinline__ void group_max(const L& sh, int n, int gi, int gl, fl
 // thread, to LDS ----
 template <int DT, int D, typename L>
 __device__ __forceinline__ void thread_sums(const TeamArgs& A, const ItemPos& q,
-                                            const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                            typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
                                             int bf, int t) {
   constexpr int E = Vec<DT>::kElems;
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
     if (r > q.n) continue;
-    typename Vec<DT>::Raw x = raw[r];
-    launder(x);
+    launder(raw[r]);
     float z[E];
-    Vec<DT>::unpack(x, z);
-    const float oc = exp_offset(sh.o[bf][r]);
+    Vec<DT>::unpack(raw[r], z);
+    const float no = sh.no[bf][r];
     float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -oc));
+      const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, no));
       if (e & 1) a1 += v;
       else a0 += v;
     }
@@ -484,21 +488,20 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
 // against the slice offsets (buffer 0) into x, per-thread sums to LDS ----
 template <int DT, int D, typename L>
 __device__ __forceinline__ void thread_exps_kept(const TeamArgs& A, const ItemPos& q,
-                                                 const typename Vec<DT>::Raw (&raw)[D + 1],
+                                                 typename Vec<DT>::Raw (&raw)[D + 1],
                                                  float (&x)[D + 1][Vec<DT>::kElems], L& sh,
                                                  int t) {
   constexpr int E = Vec<DT>::kElems;
 #pragma unroll
   for (int r = 0; r <= D; ++r) {
     if (r > q.n) continue;
-    typename Vec<DT>::Raw xr = raw[r];
-    launder(xr);
-    Vec<DT>::unpack(xr, x[r]);
-    const float oc = exp_offset(sh.o[0][r]);
+    launder(raw[r]);
+    Vec<DT>::unpack(raw[r], x[r]);
+    const float no = sh.no[0][r];
     float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, -oc));
+      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, no));
       if (e & 1) a1 += x[r][e];
       else a0 += x[r][e];
     }
@@ -534,31 +537,29 @@ __device__ __forceinline__ void thread_minsums_kept(const ItemPos& q,
 // 2^(a_d) is applied to the group sum ----
 template <int DT, int D, typename L>
 __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos& q,
-                                               const typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                               typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
                                                int bf, int t) {
   constexpr int E = Vec<DT>::kElems;
   float u[E];
-  typename Vec<DT>::Raw xt = raw[0];
-  launder(xt);
-  Vec<DT>::unpack(xt, u);
-  const float ot = exp_offset(sh.o[bf][0]);
+  launder(raw[0]);
+  Vec<DT>::unpack(raw[0], u);
+  const float nt = sh.no[bf][0];
 #pragma unroll
-  for (int e = 0; e < E; ++e) u[e] = fmaf(u[e], A.c, -ot);
+  for (int e = 0; e < E; ++e) u[e] = fmaf(u[e], A.c, nt);
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     if (d >= q.n) continue;
     float w[E];
-    typename Vec<DT>::Raw xd = raw[d + 1];
-    launder(xd);
-    Vec<DT>::unpack(xd, w);
-    const float od = exp_offset(sh.o[bf][d + 1]);
+    launder(raw[d + 1]);
+    Vec<DT>::unpack(raw[d + 1], w);
+    const float nd = sh.no[bf][d + 1];
     const float dl = sh.dl[d];
     float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       // both operands are results of arithmetic, so fminf needs no canonicalising; a NaN
       // (-inf + inf when a whole slice is -inf) loses to the other operand, which is then -inf
-      const float y = __builtin_amdgcn_exp2f(fminf(u[e] + dl, fmaf(w[e], A.c, -od)));
+      const float y = __builtin_amdgcn_exp2f(fminf(u[e] + dl, fmaf(w[e], A.c, nd)));
       if (e & 1) a1 += y;
       else a0 += y;
     }
@@ -712,11 +713,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     // argmax only: max stage, publish, fold
     Raw nxt[RM];
     uint32_t set = (uint32_t)T, next = fixed_set(1);
-    fetch_item<DT, D>(A, item_pos(A, (int)set * S + slot, D), true, sh, nxt);
+    fetch_item<DT, D>(A, item_pos(A, set, slot, D), true, sh, nxt);
     HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
     for (int j = 0; set < nsets; ++j) {
-      const ItemPos q = item_pos(A, (int)set * S + slot, D);
+      const ItemPos q = item_pos(A, set, slot, D);
       HS_STAMP(0);
       __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
       mask_tail<DT, D>(A, q, nxt);
@@ -726,7 +727,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       __syncthreads();
       HS_STAMP(1);
       if (j >= 1) next = sh.next;
-      if (next < nsets) fetch_item<DT, D>(A, item_pos(A, (int)next * S + slot, D), true, sh, nxt);
+      if (next < nsets) fetch_item<DT, D>(A, item_pos(A, next, slot, D), true, sh, nxt);
       if (wv * 4 <= q.n) {
         float m;
         int idx;
@@ -753,7 +754,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       int idx = 0;
       if (rows) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
-        if (gl == 0 && gi <= q.n) sh.o[bf][gi] = m != -INFINITY ? m * A.c : -INFINITY;
+        if (gl == 0 && gi <= q.n) {
+          const float o = m != -INFINITY ? m * A.c : -INFINITY;
+          sh.o[bf][gi] = o;
+          sh.no[bf][gi] = -exp_offset(o);
+        }
       }
       __syncthreads();
       thread_sums<DT, D>(A, q, raw, sh, bf, t);
@@ -782,7 +787,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
 
     Raw R0[RM], R1[RM], R2[RM];
     uint32_t set = (uint32_t)T, set1 = fixed_set(1), set2 = fixed_set(2);
-    const ItemPos q0 = item_pos(A, (int)set * S + slot, D);
+    const ItemPos q0 = item_pos(A, set, slot, D);
     fetch_item<DT, D, SINGLE>(A, q0, true, sh, R0);
     if constexpr (SINGLE) {
       // one item per workgroup: nothing to overlap, so its e_v stay in registers
@@ -800,7 +805,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       int idx = 0;
       if (rows) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
-        if (gl == 0 && gi <= q.n) sh.o[0][gi] = m != -INFINITY ? m * A.c : -INFINITY;
+        if (gl == 0 && gi <= q.n) {
+          const float o = m != -INFINITY ? m * A.c : -INFINITY;
+          sh.o[0][gi] = o;
+          sh.no[0][gi] = -exp_offset(o);
+        }
       }
       __syncthreads();
       thread_exps_kept<DT, D>(A, q, R0, x, sh, t);
@@ -829,7 +838,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       finish(A, tag, leader, teams, sh, t);
       return;
     }
-    fetch_item<DT, D>(A, item_pos(A, (int)min(set1, nsets - 1) * S + slot, D), set1 < nsets, sh,
+    fetch_item<DT, D>(A, item_pos(A, min(set1, nsets - 1), slot, D), set1 < nsets, sh,
                       R1);
     HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
@@ -841,7 +850,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     auto iter = [&](int j, Raw (&rc)[RM], Raw (&rn)[RM], Raw (&rp)[RM])
                     __attribute__((always_inline)) -> bool {
       const int bf = j & 1;
-      const ItemPos q = item_pos(A, (int)set * S + slot, D);
+      const ItemPos q = item_pos(A, set, slot, D);
       HS_STAMP(0);
       // the leader's claim of item j + 3 goes out before the fold and is posted after it, so
       // waiting for its result waits for nothing else
@@ -856,12 +865,12 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         put_word(mbox + ((j + 3) & 3),
                  mbox_word(min((uint32_t)(kStatic * teams) + cv, nsets), j + 3, tag));
       HS_STAMP(1);
-      fetch_item<DT, D>(A, item_pos(A, (int)min(set2, nsets - 1) * S + slot, D), set2 < nsets, sh,
+      fetch_item<DT, D>(A, item_pos(A, min(set2, nsets - 1), slot, D), set2 < nsets, sh,
                         rp);
-      if (set1 < nsets) stats(item_pos(A, (int)set1 * S + slot, D), rn, bf ^ 1);
+      if (set1 < nsets) stats(item_pos(A, set1, slot, D), rn, bf ^ 1);
       HS_STAMP(2);
       // alpha of the previous item, whose partials were stored an iteration ago
-      if (pset < nsets) fold_alpha<D>(A, item_pos(A, (int)pset * S + slot, D), tag, lane, wv);
+      if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv);
       if (set2 < nsets) post_set(j + 3);
       if (wv == 0) await_norms<D>(A, q, tag, sh, bf, lane);
       __syncthreads();
@@ -884,7 +893,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (!iter(j + 1, R1, R2, R0)) break;
       if (!iter(j + 2, R2, R0, R1)) break;
     }
-    fold_alpha<D>(A, item_pos(A, (int)set * S + slot, D), tag, lane, wv);
+    fold_alpha<D>(A, item_pos(A, set, slot, D), tag, lane, wv);
     if (A.learn)
       for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
     finish(A, tag, leader, teams, sh, t);
