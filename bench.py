@@ -36,7 +36,7 @@ ROTATE_BYTES = 512 * 1024 * 1024
 METRIC = "drafter-positions evaluated/sec + achieved HBM GB/s (% of peak), 1 MI355X"
 # Sources of the evaluation kernels; the counter summary below is valid only for these bytes.
 KERNEL_SOURCES = ["paper_2510_20064_amd/csrc/hs_team.hip", "paper_2510_20064_amd/csrc/hs_wave.h",
-                  "paper_2510_20064_amd/csrc/hs_internal.h"]
+                  "paper_2510_20064_amd/csrc/hs_internal.h", "paper_2510_20064_amd/csrc/hs_learner.h"]
 PMC_SUMMARY = "profiles/hs_eval_alpha_qwen3_8b_single_pmc.md"
 
 
