@@ -88,11 +88,32 @@ __host__ __device__ inline int tail_lds_doubles(const TailArgs& a) {
   return a.M * a.N + L * a.N;
 }
 
+// The state the learner step of query b reads (lane i: drafter i), loaded before the step
+// so that the loads can fly while gamma is gathered.
+struct LearnerIn {
+  double lw0, R0, p0, c_prev;
+  int end;
+};
+__device__ __forceinline__ LearnerIn load_learner_in(const TailArgs& a, int b) {
+  const int i = threadIdx.x & 63;
+  const bool act = i < a.N;
+  const int64_t si = (int64_t)b * a.N + i;
+  LearnerIn s;
+  s.lw0 = (a.logw && act) ? a.logw[si] : 0.0;
+  s.R0 = (a.R && act) ? a.R[si] : 0.0;
+  s.p0 = (a.R && act) ? a.p[si] : 0.0;
+  s.c_prev = a.R ? a.c[b] : 0.0;  // warm start of the scale search
+  s.end = (a.gamma_src != 0 && a.path_end) ? a.path_end[b] : a.M - 1;
+  return s;
+}
+
 // Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
 // gamma_lds (optional): the query's gamma as [N][M] floats in LDS, instead of a.alpha / a.agree.
+// pre (optional): the state, already loaded by load_learner_in.
 // Every input is loaded before anything is stored, so the loads are in flight together.
 __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds,
-                                           const float* gamma_lds = nullptr) {
+                                           const float* gamma_lds = nullptr,
+                                           const LearnerIn* pre = nullptr) {
   const int i = threadIdx.x & 63;
   const int N = a.N, M = a.M;
   const bool act = i < N;
@@ -100,13 +121,9 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
   double* lossv = lds + M * N;  // [L][N]
   int L = a.L;
 
-  // learner state, loaded up front
-  const int64_t si = (int64_t)b * N + i;
-  const double lw0 = (a.logw && act) ? a.logw[si] : 0.0;
-  const double R0 = (a.R && act) ? a.R[si] : 0.0;
-  const double p0 = (a.R && act) ? a.p[si] : 0.0;
-  const double c_prev = a.R ? a.c[b] : 0.0;  // warm start of the scale search
-  const int end = (a.gamma_src != 0 && a.path_end) ? a.path_end[b] : M - 1;
+  const LearnerIn in = pre ? *pre : load_learner_in(a, b);
+  const double lw0 = in.lw0, R0 = in.R0, p0 = in.p0, c_prev = in.c_prev;
+  const int end = in.end;
 
   if (a.gamma_src != 0) {
     const bool ok = end >= 0 && end < M;

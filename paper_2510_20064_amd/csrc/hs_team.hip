@@ -604,7 +604,8 @@ __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, 
 
 // ---- 9. learner step of query b, once this workgroup has finished its items: the query's
 // N * K gamma words are gathered into LDS (the team buffers are free by now), then wave 0 runs
-// the step. The host only asks for it when the learner's LDS fits in the team's. ----
+// the step; the learner's state is loaded before the gather, so those loads fly meanwhile.
+// The host only asks for it when the learner's LDS fits in the team's. ----
 template <typename L>
 __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int b, L& sh,
                                             int t) {
@@ -612,10 +613,12 @@ __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int
   double* lds = reinterpret_cast<double*>(&sh);
   float* gam = reinterpret_cast<float*>(lds + tail_lds_doubles(A.tail));
   const uint64_t* src = A.gw + (int64_t)b * nk;
+  LearnerIn pre{};
+  if (t < 64) pre = load_learner_in(A.tail, b);
   __syncthreads();  // the team buffers are no longer read
   for (int o = t; o < nk; o += kThreads) gam[o] = word_f(await_word(src + o, tag, A.fail));
   __syncthreads();
-  if (t < 64) tail_query(A.tail, b, lds, gam);
+  if (t < 64) tail_query(A.tail, b, lds, gam, &pre);
   __syncthreads();
 }
 
