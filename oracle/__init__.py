@@ -200,3 +200,49 @@ def normalhedge(R: np.ndarray, p: np.ndarray, loss: np.ndarray):
 def normalhedge_residual(R_row: np.ndarray, c: float) -> float:
     r = np.ascontiguousarray(R_row, dtype=np.float64)
     return _load().or_normalhedge_residual(_p(r), len(r), c)
+
+
+def window_losses(gamma: np.ndarray, K: int) -> np.ndarray:
+    """Token-level length losses [T - K + 1][N] of a token stream gamma [T][N] (window K)."""
+    g = np.ascontiguousarray(gamma, dtype=np.float64)
+    T, N = g.shape
+    out = np.zeros((max(T - K + 1, 0), N))
+    n = _load().or_window_losses(_p(g), T, N, K, _p(out))
+    assert n == out.shape[0]
+    return out
+
+
+class QfiD:
+    """Queued Full-Information with Delays (Appendix, algorithm QFI-D) with Hedge and
+    NormalHedge as base learners, one learner pair per query, fed the token-level length loss.
+
+    push(gamma, count): query b's token stream grows by gamma[b, :, :count[b]] (the feedback of
+    its next count[b] tokens, [N] each). Every window of K tokens that is complete and not yet
+    used gives one loss vector; they enter the FIFO in token order and the base learners take
+    them all, in that order, before the next prediction. Returns the loss vectors used per
+    query (a list of [L_b][N] arrays)."""
+
+    def __init__(self, B: int, N: int, K: int, eta: float):
+        self.B, self.N, self.K, self.eta = B, N, K, eta
+        self.stream = [np.zeros((0, N)) for _ in range(B)]
+        self.done = [0] * B  # windows already used
+        self.w = np.full((B, N), 1.0 / N)
+        self.R = np.zeros((B, N))
+        self.p = np.full((B, N), 1.0 / N)
+        self.c = np.zeros(B)
+
+    def push(self, gamma: np.ndarray, count):
+        used = []
+        for b in range(self.B):
+            m = int(count[b])
+            self.stream[b] = np.concatenate([self.stream[b], np.asarray(gamma[b, :, :m]).T])
+            ls = window_losses(self.stream[b], self.K)[self.done[b]:]
+            self.done[b] += ls.shape[0]
+            if ls.shape[0]:
+                lb = ls[:, None, :]  # [L][1][N]
+                self.w[b:b + 1] = hedge(self.w[b:b + 1], lb, self.eta)
+                R, p, c = normalhedge(self.R[b:b + 1], self.p[b:b + 1], lb)
+                self.R[b:b + 1], self.p[b:b + 1], self.c[b] = R, p, c[0]
+            used.append(ls)
+        return used
+

@@ -18,6 +18,8 @@
  *   or_eal_path, or_accept_len : pinned (Theorem 3 against brute force,
  *                             worked example of the censoring appendix, constant-gamma
  *                             closed form, range [1, K+1]).
+ *   or_window_losses        : pinned (all-accept and all-reject windows, K = 1, constant
+ *                             gamma geometric sum, the censoring appendix's worked example).
  *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
  *   or_normalhedge          : pinned (closed-form c for one or m equal positive
  *                             regrets, scale covariance, sum_i p_i dR_i = 0).
@@ -183,6 +185,26 @@ double or_eal_path(const double* gamma, int K) {
     eal += (double)k * (1.0 - gk) * prod;
   }
   return eal;
+}
+
+/*
+ * Token-level length loss (Section 3.3, "HedgeSpec: Loss functions and Delayed Feedback"):
+ * for token s and drafter i, f_s[i] = 1 - EAL(gamma_s .. gamma_{s+K-1})[i] / (K + 1), i.e.
+ * Theorem 3's estimator on the window of K tokens that starts at s (the window's (K+1)-th
+ * term takes gamma := 0, as in the chunk definition above).
+ * gamma: [T][N] token stream; loss: [T - K + 1][N], one vector per complete window in token
+ * order. Returns the number of windows (0 when T < K).
+ */
+int or_window_losses(const double* gamma, int T, int N, int K, double* loss) {
+  int nw = T - K + 1;
+  if (nw < 0) nw = 0;
+  double g[4096];
+  for (int s = 0; s < nw; ++s)
+    for (int i = 0; i < N; ++i) {
+      for (int j = 0; j < K; ++j) g[j] = gamma[(size_t)(s + j) * N + i];
+      loss[(size_t)s * N + i] = 1.0 - or_eal_path(g, K) / (double)(K + 1);
+    }
+  return nw;
 }
 
 /*

@@ -383,3 +383,77 @@ def test_normalhedge_equal_losses_leave_regrets_exactly_unchanged():
     p1 = np.array([[0.5, 0.5, 0.0, 0.0]])
     R, _, _ = oracle.normalhedge(np.zeros((1, 4)), p1, np.array([[[1 / 3, 1 / 3, 0.9, 0.1]]]))
     assert R[0, 0] == 0.0 and R[0, 1] == 0.0 and R[0, 2] < 0 < R[0, 3]
+
+
+# ---- token-level length loss and QFI-D (Section 3.3; Appendix, algorithm QFI-D) ----------------
+
+@pytest.mark.parametrize("K", [1, 2, 5, 8])
+def test_window_losses_closed_forms(K):
+    rng = np.random.default_rng(K)
+    T, N = 3 * K + 4, 3
+    # all accepted: EAL = K + 1, loss 0; all rejected: EAL = 1, loss K / (K + 1)
+    assert np.all(oracle.window_losses(np.ones((T, N)), K) == 0.0)
+    assert np.allclose(oracle.window_losses(np.zeros((T, N)), K), K / (K + 1), rtol=0, atol=1e-15)
+    # constant gamma a: EAL = (1 - a^(K+1)) / (1 - a), the geometric sum
+    for a in (0.25, 0.6, 0.95):
+        want = 1 - (1 - a ** (K + 1)) / (1 - a) / (K + 1)
+        assert np.allclose(oracle.window_losses(np.full((T, N), a), K), want, rtol=0, atol=1e-14)
+    # window count and order: window s uses tokens s .. s + K - 1 only
+    g = rng.random((T, N))
+    ls = oracle.window_losses(g, K)
+    assert ls.shape == (T - K + 1, N)
+    g2 = g.copy()
+    g2[K:] = rng.random((T - K, N))  # change every token after the first window
+    assert np.array_equal(oracle.window_losses(g2, K)[0], ls[0])
+    assert oracle.window_losses(g[:K - 1], K).shape == (0, N)
+
+
+def test_window_loss_k1_is_half_the_rejection_probability():
+    g = np.random.default_rng(3).random((20, 4))
+    assert np.allclose(oracle.window_losses(g, 1), (1 - g) / 2, rtol=0, atol=1e-15)
+
+
+def test_window_loss_of_the_censoring_example():
+    with open(os.path.join(GOLDEN, "censoring_example.json")) as f:
+        gold = json.load(f)
+    for case in gold["cases"]:
+        g = np.asarray(case["gamma"], dtype=np.float64)[:, None]
+        got = oracle.window_losses(g, case["K"])
+        assert got.shape == (1, 1)
+        assert abs(got[0, 0] - (1 - case["eal"] / (case["K"] + 1))) < 1e-12, case["name"]
+
+
+def _stream_counts(rng, rounds, K, B):
+    return rng.integers(0, K + 1, (rounds, B))
+
+
+def test_qfid_is_the_base_learners_on_the_window_stream_whatever_the_chunking():
+    # QFI-D feeds the base learners every window loss in token order, each as soon as its
+    # window is complete: the state after any chunking of the same stream equals the base
+    # learners run on the whole window-loss sequence at once, and no window is used early.
+    rng = np.random.default_rng(11)
+    B, N, K, eta = 3, 5, 4, 0.4
+    T = 40
+    gam = [rng.random((T, N)) for _ in range(B)]
+    results = []
+    for split in range(3):
+        q = oracle.QfiD(B, N, K, eta)
+        pos = [0] * B
+        while min(pos) < T:
+            cnt = [min(int(rng.integers(0, K + 1)), T - pos[b]) for b in range(B)]
+            g = np.zeros((B, N, K))
+            for b in range(B):
+                g[b, :, :cnt[b]] = gam[b][pos[b]:pos[b] + cnt[b]].T
+            used = q.push(g, cnt)
+            for b in range(B):
+                pos[b] += cnt[b]
+                assert q.done[b] == max(0, pos[b] - K + 1)  # every complete window, none early
+                assert used[b].shape[0] <= cnt[b]
+        results.append(q)
+    for b in range(B):
+        ls = oracle.window_losses(gam[b], K)[:, None, :]
+        w = oracle.hedge(np.full((1, N), 1.0 / N), ls, eta)
+        R, p, c = oracle.normalhedge(np.zeros((1, N)), np.full((1, N), 1.0 / N), ls)
+        for q in results:
+            assert np.array_equal(q.w[b], w[0]) and np.array_equal(q.R[b], R[0])
+            assert np.array_equal(q.p[b], p[0]) and q.c[b] == c[0]
