@@ -182,6 +182,40 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
                           int N, void* stream);
 
 /*
+ * hs_delayed_update - the token-level game with delayed feedback (Section 3.3,
+ * "HedgeSpec: Loss functions and Delayed Feedback"; Appendix, algorithm QFI-D,
+ * "Queued Full-Information with Delays", with Hedge and NormalHedge as base learners).
+ * The token-level length loss of token s for drafter i,
+ *   f_s[i] = 1 - EAL(gamma_s .. gamma_{s+K-1})[i] / (K + 1),
+ * is Theorem 3's estimator on the window of K tokens that starts at s (the window's
+ * (K+1)-th term takes gamma = 0, as in hs_accept_len). It is known only once the
+ * feedback of all K tokens of its window has arrived. Per query b, this call appends
+ * the feedback of the query's next count[b] tokens to the history ring, then feeds
+ * every window that is now complete and not yet used to the base learners, in token
+ * order, before returning: the learners see a delay-free loss stream in their own
+ * clock. A query whose call completes no window keeps its learner state unchanged.
+ * alpha / agree : [B][N][K] gamma of this round (HS_SAMPLE: alpha fp32; HS_GREEDY:
+ *                 agree uint8); token j of the call is position j, j < count[b].
+ * count         : [B] int32 device; values outside [0, K] are clamped to it.
+ * hist          : [B][2K][N] fp32 device, the history ring (caller-owned, zero-filled
+ *                 before the first call of a stream, not read by the caller).
+ * clock         : [B][2] int64 device, zero-filled before the first call: tokens
+ *                 received and windows used so far, per query.
+ * logw, w, eta  : Hedge state (both or neither); R, p, c: NormalHedge state (all or
+ *                 none), as in hs_hedge_update / hs_normalhedge_update.
+ * loss          : [K][B][N] fp64 or NULL: the window losses used by this call, in
+ *                 order (rows past nloss[b] are not written).
+ * nloss         : [B] int32 or NULL: how many windows each query used (at most count[b]).
+ * One launch, one wave per query. Errors: HS_ERR_SHAPE / HS_ERR_LIMIT on B, N, K;
+ * HS_ERR_ARG on mode or a non-finite eta; HS_ERR_NULL on missing inputs or unpaired
+ * learner state. Nothing is enqueued on error.
+ */
+int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
+                      const int32_t* count, float* hist, int64_t* clock, double* logw,
+                      double* w, double eta, double* R, double* p, double* c, double* loss,
+                      int32_t* nloss, void* stream);
+
+/*
  * hs_round - one verification round of the whole path, enqueued as two launches
  * (the evaluation; then, per query, the learner step on its alpha or agreement): the
  * work of hs_eval_alpha, then per query hs_accept_len's work, the loss, and the

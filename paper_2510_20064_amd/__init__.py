@@ -74,11 +74,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_hedge_update.argtypes = [P, P, P, I, I, I, D, P]
     lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
     lib.hs_round.argtypes = [ctypes.POINTER(hs_round_args), P]
+    lib.hs_delayed_update.argtypes = [P, P, I, I, I, I, P, P, P, P, P, D, P, P, P, P, P, P]
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
     for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_accept_len", "hs_hedge_update",
-                 "hs_normalhedge_update", "hs_round", "hs_version"]:
+                 "hs_normalhedge_update", "hs_round", "hs_delayed_update", "hs_version"]:
         getattr(lib, name).restype = I
     _lib = lib
     return lib
@@ -244,6 +245,38 @@ class LearnerState:
         self.R = torch.zeros((B, N), dtype=torch.float64, device=device)
         self.p = torch.full((B, N), 1.0 / N, dtype=torch.float64, device=device)
         self.c = torch.zeros((B,), dtype=torch.float64, device=device)
+
+
+class DelayedState:
+    """Device state of hs_delayed_update for B queries, N drafters and window K: the feedback
+    history ring, the per-query clock (tokens received, windows used) and the learners."""
+
+    def __init__(self, B: int, N: int, K: int, device):
+        self.B, self.N, self.K = B, N, K
+        self.hist = torch.zeros((B, 2 * K, N), dtype=torch.float32, device=device)
+        self.clock = torch.zeros((B, 2), dtype=torch.int64, device=device)
+        self.learners = LearnerState(B, N, device)
+        self.loss = torch.zeros((K, B, N), dtype=torch.float64, device=device)
+        self.nloss = torch.zeros((B,), dtype=torch.int32, device=device)
+
+
+def delayed_update(state: DelayedState, gamma: torch.Tensor, count: torch.Tensor, eta: float,
+                   mode: int = SAMPLE, hedge: bool = True, normalhedge: bool = True,
+                   stream=None) -> None:
+    """hs_delayed_update: append query b's next count[b] tokens of feedback (gamma [B][N][K]:
+    alpha fp32 in SAMPLE mode, agree uint8 in GREEDY mode) and feed every newly complete
+    K-token window's length loss to the learners. The losses used are left in state.loss
+    (first state.nloss[b] rows per query)."""
+    B, N, K = gamma.shape
+    st = state.learners
+    alpha = gamma if mode == SAMPLE else None
+    agree = gamma if mode == GREEDY else None
+    _check(load_library().hs_delayed_update(
+        _ptr(alpha), _ptr(agree), mode, B, N, K, _ptr(count), _ptr(state.hist),
+        _ptr(state.clock), _ptr(st.logw if hedge else None), _ptr(st.w if hedge else None),
+        eta, _ptr(st.R if normalhedge else None), _ptr(st.p if normalhedge else None),
+        _ptr(st.c if normalhedge else None), _ptr(state.loss), _ptr(state.nloss),
+        _stream(stream)))
 
 
 class Round:

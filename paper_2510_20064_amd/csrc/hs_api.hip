@@ -302,6 +302,44 @@ HS_API int hs_normalhedge_update(double* R, double* p, double* c, const double* 
   return ok();
 }
 
+HS_API int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode, int B, int N,
+                             int K, const int32_t* count, float* hist, int64_t* clock,
+                             double* logw, double* w, double eta, double* R, double* p,
+                             double* c, double* loss, int32_t* nloss, void* stream) {
+  int rc = check_shape(B, N, K, 1);
+  if (rc) return rc;
+  if (mode != HS_SAMPLE && mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", mode);
+  if (mode == HS_SAMPLE && !alpha) return fail(HS_ERR_NULL, "sample mode needs alpha");
+  if (mode == HS_GREEDY && !agree) return fail(HS_ERR_NULL, "greedy mode needs agree");
+  if (!count || !hist || !clock) return fail(HS_ERR_NULL, "count, hist and clock are required");
+  if ((logw == nullptr) != (w == nullptr))
+    return fail(HS_ERR_NULL, "logw and w must be given together");
+  if (!((R == nullptr) == (p == nullptr) && (R == nullptr) == (c == nullptr)))
+    return fail(HS_ERR_NULL, "R, p and c must be given together");
+  if (logw && !isfinite(eta)) return fail(HS_ERR_ARG, "eta must be finite");
+  hs::DelayArgs a{};
+  a.alpha = alpha;
+  a.agree = agree;
+  a.gamma_src = mode == HS_SAMPLE ? 1 : 2;
+  a.B = B;
+  a.N = N;
+  a.K = K;
+  a.count = count;
+  a.hist = hist;
+  a.clock = clock;
+  a.logw = logw;
+  a.w = w;
+  a.eta = eta;
+  a.R = R;
+  a.p = p;
+  a.c = c;
+  a.loss = loss;
+  a.nloss = nloss;
+  rc = hs::launch_delayed(a, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
 HS_API int hs_round(const hs_round_args* r, void* stream) {
   if (!r) return fail(HS_ERR_NULL, "args is NULL");
   EvalReq q{&r->target, r->drafters_host, r->N, r->B, r->K, r->V, r->dtype, r->temperature,

@@ -1,0 +1,73 @@
+// Delayed feedback (Section 3.3, "HedgeSpec: Loss functions and Delayed Feedback"; Appendix,
+// algorithm "Queued Full-Information with Delays"): the token-level length loss
+//   f_s[i] = 1 - EAL(gamma_s .. gamma_{s+K-1})[i] / (K + 1)
+// (Theorem 3's estimator on the window of K tokens that starts at token s) becomes known only
+// once the feedback of all K tokens of its window has arrived. Each call appends the feedback
+// of a query's newest tokens to its history ring and feeds every window that is now complete,
+// in token order, to Hedge and NormalHedge before anything else happens: the base learners
+// see a delay-free loss stream in their own clock, and a call that completes no window leaves
+// them untouched. One wave64 per query, lane i = drafter i, fp64.
+#include "hs_learner.h"
+
+namespace hs {
+
+__global__ __launch_bounds__(64) void hs_delayed_kernel(DelayArgs a) {
+  extern __shared__ double lossv[];  // [K][N]
+  const int b = blockIdx.x, i = threadIdx.x;
+  const int N = a.N, K = a.K, W = 2 * K;
+  const bool act = i < N;
+  TailArgs st{};  // only the learner-state fields, for load_learner_in
+  st.N = N;
+  st.M = K;
+  st.logw = a.logw;
+  st.R = a.R;
+  st.p = a.p;
+  st.c = a.c;
+  const LearnerIn in = load_learner_in(st, b);
+  const int64_t t_next = a.clock[2 * b], t_used = a.clock[2 * b + 1];
+  const int m = min(max(a.count[b], 0), K);  // counts outside [0, K] are clamped
+  float* hb = a.hist + (int64_t)b * W * N;
+  auto fresh = [&](int j) -> float {  // feedback of the call's j-th token
+    const int64_t o = ((int64_t)b * N + i) * K + j;
+    return a.gamma_src == 1 ? a.alpha[o] : (float)a.agree[o];
+  };
+  if (act)
+    for (int j = 0; j < m; ++j) hb[(int)((t_next + j) % W) * N + i] = fresh(j);
+  const int64_t t_new = t_next + m;
+  // windows s = t_used .. t_new - K are complete; at most m of them are new (the ring holds
+  // tokens t_used .. t_new - 1, at most 2K - 1 of them)
+  const int L = (int)max((int64_t)0, t_new - K + 1 - t_used);
+  for (int l = 0; l < L; ++l) {
+    const int64_t s = t_used + l;
+    double pp = 1.0, sp = 0.0;
+    for (int j = 0; j < K; ++j) {
+      const int64_t tok = s + j;
+      const double g = act ? (double)(tok < t_next ? hb[(int)(tok % W) * N + i]
+                                                   : fresh((int)(tok - t_next)))
+                           : 0.0;
+      pp *= g;
+      sp += pp;
+    }
+    const double f = 1.0 - (1.0 + sp) / (double)(K + 1);
+    if (act) {
+      lossv[l * N + i] = f;
+      if (a.loss) a.loss[((int64_t)l * a.B + b) * N + i] = f;
+    }
+  }
+  if (L > 0)
+    learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in,
+                   [&](int l) -> double { return act ? lossv[l * N + i] : 0.0; });
+  if (i == 0) {
+    a.clock[2 * b] = t_new;
+    a.clock[2 * b + 1] = t_used + L;
+    if (a.nloss) a.nloss[b] = L;
+  }
+}
+
+int launch_delayed(const DelayArgs& a, hipStream_t stream) {
+  const size_t lds = sizeof(double) * (size_t)a.K * a.N;
+  hs_delayed_kernel<<<a.B, 64, lds, stream>>>(a);
+  return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
+}
+
+}  // namespace hs

@@ -247,6 +247,27 @@ struct TailArgs {
 #endif
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
+
+// Delayed feedback: the token-level length loss over a sliding window of K tokens, fed to the
+// base learners as each window completes (hs_delayed.hip).
+struct DelayArgs {
+  const float* alpha;    // [B][N][K] (gamma_src 1)
+  const uint8_t* agree;  // [B][N][K] (gamma_src 2)
+  int gamma_src;
+  int B, N, K;
+  const int32_t* count;  // [B]: tokens whose feedback arrives now (positions 0 .. count - 1)
+  float* hist;           // [B][2K][N]: feedback of the last 2K tokens, by token index mod 2K
+  int64_t* clock;        // [B][2]: tokens received, windows used
+  double* logw;
+  double* w;
+  double eta;
+  double* R;
+  double* p;
+  double* c;
+  double* loss;    // [K][B][N] or NULL: the window losses used, in order
+  int32_t* nloss;  // [B] or NULL: how many
+};
+int launch_delayed(const DelayArgs& a, hipStream_t stream);
 // Evaluation of one round: the team kernel (which also advances the workspace epoch) and, when
 // tail != nullptr, the learner step on its alpha or agreement.
 int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,

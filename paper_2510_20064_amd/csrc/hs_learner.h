@@ -107,6 +107,65 @@ __device__ __forceinline__ LearnerIn load_learner_in(const TailArgs& a, int b) {
   return s;
 }
 
+// The base learners of query b take the L loss vectors loss_at(0 .. L-1) in order (lane i:
+// drafter i, all 64 lanes of the wave; `in` holds the state as loaded by load_learner_in):
+//   Hedge       : logw -= eta * loss for each vector; w = softmax(logw) (logw and w may be NULL)
+//   NormalHedge : per vector, R_i += l_A - l_i, c solves the scale equation, p from R and c
+//                 (R, p and c may be NULL)
+template <typename LossAt>
+__device__ __forceinline__ void learner_update(double* logw, double* w, double eta, double* R,
+                                               double* p, double* c, int b, int N, int L,
+                                               const LearnerIn& in, LossAt loss_at) {
+  const int i = threadIdx.x & 63;
+  const bool act = i < N;
+  // ---- Hedge ----
+  if (logw) {
+    double lw = act ? in.lw0 : -INFINITY;
+    for (int l = 0; l < L; ++l) lw -= eta * loss_at(l);
+    const double mx = wmax(act ? lw : -INFINITY);
+    const double e = act ? exp(lw - mx) : 0.0;
+    const double se = wsum(e);
+    if (act) {
+      logw[(int64_t)b * N + i] = lw - mx;
+      w[(int64_t)b * N + i] = e / se;
+    }
+  }
+
+  // ---- NormalHedge ----
+  if (R) {
+    double Rv = in.R0;
+    double pv = in.p0;
+    double cc = 0.0;
+    for (int l = 0; l < L; ++l) {
+      const double li = loss_at(l);
+      // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
+      // zero when every drafter that carries weight has this drafter's loss
+      double dR = 0.0;
+      for (int j = 0; j < N; ++j) dR += lane_d(pv, j) * (lane_d(li, j) - li);
+      if (act) Rv += dR;
+      const double r = (act && Rv > 0.0) ? Rv : 0.0;
+      const double M2 = wmax(r * r);
+      if (!(M2 > 0.0)) {
+        pv = act ? 1.0 / (double)N : 0.0;
+        cc = 0.0;
+        continue;
+      }
+      const double ai = 0.5 * r * r;
+      const double s = normalhedge_inv_scale(
+          ai, act, N, M2, cc > 0.0 ? 1.0 / cc : (in.c_prev > 0.0 ? 1.0 / in.c_prev : 0.0));
+      const double u = act ? r * exp(ai * s) : 0.0;
+      const double su = wsum(u);
+      pv = u / su;
+      cc = 1.0 / s;
+    }
+    if (act) {
+      R[(int64_t)b * N + i] = Rv;
+      p[(int64_t)b * N + i] = pv;
+    }
+    if (i == 0) c[b] = cc;
+  }
+}
+
 // Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
 // gamma_lds (optional): the query's gamma as [N][M] floats in LDS, instead of a.alpha / a.agree.
 // pre (optional): the state, already loaded by load_learner_in.
@@ -122,7 +181,6 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
   int L = a.L;
 
   const LearnerIn in = pre ? *pre : load_learner_in(a, b);
-  const double lw0 = in.lw0, R0 = in.R0, p0 = in.p0, c_prev = in.c_prev;
   const int end = in.end;
 
   if (a.gamma_src != 0) {
@@ -193,54 +251,7 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
     if (a.gamma_src != 0) return lossv[l * N + i];
     return a.loss_in[((int64_t)l * a.B + b) * N + i];
   };
-
-  // ---- Hedge ----
-  if (a.logw) {
-    double lw = act ? lw0 : -INFINITY;
-    for (int l = 0; l < L; ++l) lw -= a.eta * loss_at(l);
-    const double mx = wmax(act ? lw : -INFINITY);
-    const double e = act ? exp(lw - mx) : 0.0;
-    const double se = wsum(e);
-    if (act) {
-      a.logw[(int64_t)b * N + i] = lw - mx;
-      a.w[(int64_t)b * N + i] = e / se;
-    }
-  }
-
-  HS_TSTAMP(4);
-  // ---- NormalHedge ----
-  if (a.R) {
-    double Rv = R0;
-    double pv = p0;
-    double cc = 0.0;
-    for (int l = 0; l < L; ++l) {
-      const double li = loss_at(l);
-      // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
-      // zero when every drafter that carries weight has this drafter's loss
-      double dR = 0.0;
-      for (int j = 0; j < N; ++j) dR += lane_d(pv, j) * (lane_d(li, j) - li);
-      if (act) Rv += dR;
-      const double r = (act && Rv > 0.0) ? Rv : 0.0;
-      const double M2 = wmax(r * r);
-      if (!(M2 > 0.0)) {
-        pv = act ? 1.0 / (double)N : 0.0;
-        cc = 0.0;
-        continue;
-      }
-      const double ai = 0.5 * r * r;
-      const double s = normalhedge_inv_scale(ai, act, N, M2,
-                                             cc > 0.0 ? 1.0 / cc : (c_prev > 0.0 ? 1.0 / c_prev : 0.0));
-      const double u = act ? r * exp(ai * s) : 0.0;
-      const double su = wsum(u);
-      pv = u / su;
-      cc = 1.0 / s;
-    }
-    if (act) {
-      a.R[(int64_t)b * N + i] = Rv;
-      a.p[(int64_t)b * N + i] = pv;
-    }
-    if (i == 0) a.c[b] = cc;
-  }
+  learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in, loss_at);
   HS_TSTAMP(5);
 }
 

@@ -138,3 +138,29 @@ def test_round_validation_codes():
     a.R = FAKE  # p, c missing
     assert lib.hs_round(ctypes.byref(a), None) == 1
     assert lib.hs_round(None, None) == 1
+
+
+def _delayed(lib, **kw):
+    a = dict(alpha=FAKE, agree=None, mode=0, B=4, N=8, K=8, count=FAKE, hist=FAKE, clock=FAKE,
+             logw=FAKE, w=FAKE, eta=0.5, R=FAKE, p=FAKE, c=FAKE, loss=None, nloss=None)
+    a.update(kw)
+    return lib.hs_delayed_update(a["alpha"], a["agree"], a["mode"], a["B"], a["N"], a["K"],
+                                 a["count"], a["hist"], a["clock"], a["logw"], a["w"], a["eta"],
+                                 a["R"], a["p"], a["c"], a["loss"], a["nloss"], None)
+
+
+def test_delayed_update_validation_codes():
+    lib = hs.load_library()
+    assert _delayed(lib, B=0) == 2
+    assert _delayed(lib, K=0) == 2
+    assert _delayed(lib, N=65) == 8
+    assert _delayed(lib, K=65) == 8
+    assert _delayed(lib, mode=2) == 10
+    assert _delayed(lib, alpha=None) == 1
+    assert _delayed(lib, mode=1, agree=None) == 1
+    assert _delayed(lib, count=None) == 1
+    assert _delayed(lib, hist=None) == 1
+    assert _delayed(lib, clock=None) == 1
+    assert _delayed(lib, w=None) == 1
+    assert _delayed(lib, c=None) == 1
+    assert _delayed(lib, eta=float("inf")) == 10
