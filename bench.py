@@ -77,7 +77,65 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--delayed", action="store_true",
+                    help="time hs_delayed_update (token-level delayed feedback) on the workload's "
+                         "B, N, K instead, K new tokens per query per round")
     return ap.parse_args()
+
+
+def bench_delayed(args, w, hs, torch, dev):
+    """hs_delayed_update in steady state: every call brings K new tokens per query, so each
+    query's learners take K window losses in order (K NormalHedge solves per query)."""
+    B, N, K = w.B, w.N, w.K
+    copies = 16
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed)
+    gam = [torch.rand((B, N, K), generator=gen, device=dev) for _ in range(copies)]
+    cnt = torch.full((B,), K, dtype=torch.int32, device=dev)
+    st = hs.DelayedState(B, N, K, dev)
+    stream = torch.cuda.Stream()
+
+    def call(i):
+        hs.delayed_update(st, gam[i % copies], cnt, w.eta, stream=torch.cuda.current_stream())
+
+    with torch.cuda.stream(stream):
+        for i in range(copies):  # past the first K tokens: every later call completes K windows
+            call(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // copies)
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup // copies)):
+            g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+    nl = st.nloss.cpu()
+    assert bool(torch.all(nl == K)), "steady state expected K windows per query per call"
+    # bytes a call moves: gamma in, history ring in and out, learner state in and out, losses out
+    nbytes = B * N * K * 4 + 2 * B * 2 * K * N * 4 + 2 * 5 * B * N * 8 + B * K * N * 8
+    line = {"metric": "delayed-feedback learner: drafter-window losses used per second",
+            "value": B * N * K / (us * 1e-6), "unit": "drafter-windows/s", "n_gpus": 1,
+            "steps": reps * copies, "warmup": max(1, args.warmup // copies) * copies,
+            "us_per_call": us, "higher_is_better": True, "dtype": "f64", "data": "synthetic",
+            "config": {"workload": w.name, "B": B, "N": N, "K": K, "eta": w.eta,
+                       "tokens_per_call": K, "hip_graph": True},
+            "roofline": {"bound": "latency", "achieved": nbytes / (us * 1e-6) / 1e9,
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                         "kernel": "hs_delayed_kernel (one wave per query, K sequential window "
+                                   "updates each)", "bytes_per_call": nbytes}}
+    print(json.dumps(line), flush=True)
 
 
 def main():
@@ -98,6 +156,9 @@ def main():
     w = synth.workloads()[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.delayed:
+        bench_delayed(args, w, hs, torch, dev)
+        return
 
     # ---- inputs: distinct rounds, resident in HBM -----------------------------------------
     copies = max(1, math.ceil(ROTATE_BYTES / w.input_bytes))

@@ -12,10 +12,14 @@
 namespace hs {
 
 __global__ __launch_bounds__(64) void hs_delayed_kernel(DelayArgs a) {
-  extern __shared__ double lossv[];  // [K][N]
+  // LDS: the window losses [K][N] doubles, the learners' scratch, then the feedback of tokens
+  // t_used .. t_new - 1 (at most 2K - 1 of them) as [2K][N] floats
+  extern __shared__ double lossv[];
   const int b = blockIdx.x, i = threadIdx.x;
   const int N = a.N, K = a.K, W = 2 * K;
   const bool act = i < N;
+  double* scratch = lossv + K * N;
+  float* gw = reinterpret_cast<float*>(scratch + kLearnScratch);
   TailArgs st{};  // only the learner-state fields, for load_learner_in
   st.N = N;
   st.M = K;
@@ -27,25 +31,25 @@ __global__ __launch_bounds__(64) void hs_delayed_kernel(DelayArgs a) {
   const int64_t t_next = a.clock[2 * b], t_used = a.clock[2 * b + 1];
   const int m = min(max(a.count[b], 0), K);  // counts outside [0, K] are clamped
   float* hb = a.hist + (int64_t)b * W * N;
-  auto fresh = [&](int j) -> float {  // feedback of the call's j-th token
-    const int64_t o = ((int64_t)b * N + i) * K + j;
-    return a.gamma_src == 1 ? a.alpha[o] : (float)a.agree[o];
-  };
-  if (act)
-    for (int j = 0; j < m; ++j) hb[(int)((t_next + j) % W) * N + i] = fresh(j);
   const int64_t t_new = t_next + m;
-  // windows s = t_used .. t_new - K are complete; at most m of them are new (the ring holds
-  // tokens t_used .. t_new - 1, at most 2K - 1 of them)
+  // the ring holds tokens t_used .. t_next - 1 (t_used >= t_next - K + 1), the call brings
+  // t_next .. t_new - 1: at most 2K - 1 tokens in all, so no two share a ring slot
+  const int nold = (int)(t_next - t_used);
+  if (act) {
+    for (int j = 0; j < nold; ++j) gw[j * N + i] = hb[(int)((t_used + j) % W) * N + i];
+    for (int j = 0; j < m; ++j) {
+      const int64_t o = ((int64_t)b * N + i) * K + j;
+      const float g = a.gamma_src == 1 ? a.alpha[o] : (float)a.agree[o];
+      gw[(nold + j) * N + i] = g;
+      hb[(int)((t_next + j) % W) * N + i] = g;
+    }
+  }
+  // windows s = t_used .. t_new - K are complete; at most m of them
   const int L = (int)max((int64_t)0, t_new - K + 1 - t_used);
   for (int l = 0; l < L; ++l) {
-    const int64_t s = t_used + l;
     double pp = 1.0, sp = 0.0;
     for (int j = 0; j < K; ++j) {
-      const int64_t tok = s + j;
-      const double g = act ? (double)(tok < t_next ? hb[(int)(tok % W) * N + i]
-                                                   : fresh((int)(tok - t_next)))
-                           : 0.0;
-      pp *= g;
+      pp *= act ? (double)gw[(l + j) * N + i] : 0.0;
       sp += pp;
     }
     const double f = 1.0 - (1.0 + sp) / (double)(K + 1);
@@ -55,7 +59,7 @@ __global__ __launch_bounds__(64) void hs_delayed_kernel(DelayArgs a) {
     }
   }
   if (L > 0)
-    learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in,
+    learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in, scratch,
                    [&](int l) -> double { return act ? lossv[l * N + i] : 0.0; });
   if (i == 0) {
     a.clock[2 * b] = t_new;
@@ -65,7 +69,8 @@ __global__ __launch_bounds__(64) void hs_delayed_kernel(DelayArgs a) {
 }
 
 int launch_delayed(const DelayArgs& a, hipStream_t stream) {
-  const size_t lds = sizeof(double) * (size_t)a.K * a.N;
+  const size_t lds = sizeof(double) * ((size_t)a.K * a.N + kLearnScratch) +
+                     sizeof(float) * 2 * (size_t)a.K * a.N;
   hs_delayed_kernel<<<a.B, 64, lds, stream>>>(a);
   return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
 }

@@ -56,14 +56,17 @@ __device__ inline double wmax(double v) {
 }
 
 // NormalHedge's scale. With a_i = r_i^2 / 2 and s = 1/c, phi(s) = log((1/N) sum exp(a_i s)) - 1
-// is convex and increasing; its root s* lies in [2/M, 2(1 + ln N)/M], M = max r_i^2 (at the
-// upper end every exponent is <= 1 + ln N, so nothing overflows). Newton's method from any
-// start in the bracket converges (from the left it overshoots once, then descends
-// monotonically: the tangent of a convex function lies below it); a step that leaves the
-// bracket is replaced by bisection. The start is the previous round's scale when it lies in
-// the bracket (regrets move little per round), else the upper end. Returns s*.
+// is convex and increasing; its root s* lies in [2/M, 2(1+ln N)/M], M = max r_i^2 (at the
+// upper end every exponent is <= 1 + ln N, so nothing overflows, and phi >= 0 there). Newton's
+// method decreases monotonically to s* from any point right of it (the tangent of a convex
+// function lies below it). From a point left of s* the step overshoots to the right; an
+// overshoot past the bracket restarts from the bracket's right end instead, so every later
+// iterate lies right of s* (bisection would land left again and again: up to 55 iterations
+// instead of 6 on random loss streams of 64 drafters). The start is the previous round's scale
+// when it lies in the bracket (regrets move little per round), else the right end. Returns s*.
 __device__ inline double normalhedge_inv_scale(double a, bool act, int N, double M, double s0) {
-  double lo = 2.0 / M, hi = 2.0 * (1.0 + log((double)N)) / M;
+  double lo = 2.0 / M;
+  const double hi = 2.0 * (1.0 + log((double)N)) / M;
   double s = (s0 > lo && s0 < hi) ? s0 : hi;
   for (int it = 0; it < 100; ++it) {
     const double ex = act ? exp(a * s) : 0.0;
@@ -71,21 +74,29 @@ __device__ inline double normalhedge_inv_scale(double a, bool act, int N, double
     const double F = wsum(act ? a * ex : 0.0);
     const double phi = log(E / (double)N) - 1.0;
     if (phi == 0.0 || !(F > 0.0)) break;
-    if (phi > 0.0) hi = s; else lo = s;
     double sn = s - phi * E / F;
-    if (!(sn > lo && sn < hi)) sn = 0.5 * (lo + hi);
+    if (phi < 0.0) {
+      lo = s;
+      if (!(sn < hi)) sn = hi;
+    } else if (!(sn > lo)) {  // rounding only: a right-side step stays right of s* > lo
+      sn = 0.5 * (lo + s);
+    }
     const double ds = fabs(sn - s);
     s = sn;
-    if (ds <= 4e-16 * s || hi - lo <= 4e-16 * hi) break;
+    if (ds <= 4e-16 * s) break;
   }
   return s;
 }
 
-// LDS doubles tail_query needs.
+// LDS doubles learner_update uses as scratch: p and the loss vector of every drafter.
+constexpr int kLearnScratch = 2 * 64;
+
+// LDS doubles tail_query needs: gamma / prefix products [M][N], losses [L][N], then the
+// learner's scratch.
 __host__ __device__ inline int tail_lds_doubles(const TailArgs& a) {
-  if (a.gamma_src == 0) return 1;
+  if (a.gamma_src == 0) return kLearnScratch;
   const int L = a.loss_kind == HS_LOSS_ACCEPT_TOKEN ? a.M : 1;
-  return a.M * a.N + L * a.N;
+  return a.M * a.N + L * a.N + kLearnScratch;
 }
 
 // The state the learner step of query b reads (lane i: drafter i), loaded before the step
@@ -108,14 +119,16 @@ __device__ __forceinline__ LearnerIn load_learner_in(const TailArgs& a, int b) {
 }
 
 // The base learners of query b take the L loss vectors loss_at(0 .. L-1) in order (lane i:
-// drafter i, all 64 lanes of the wave; `in` holds the state as loaded by load_learner_in):
+// drafter i, all 64 lanes of the wave; `in` holds the state as loaded by load_learner_in;
+// scratch: kLearnScratch doubles of LDS used by this wave only):
 //   Hedge       : logw -= eta * loss for each vector; w = softmax(logw) (logw and w may be NULL)
 //   NormalHedge : per vector, R_i += l_A - l_i, c solves the scale equation, p from R and c
 //                 (R, p and c may be NULL)
 template <typename LossAt>
 __device__ __forceinline__ void learner_update(double* logw, double* w, double eta, double* R,
                                                double* p, double* c, int b, int N, int L,
-                                               const LearnerIn& in, LossAt loss_at) {
+                                               const LearnerIn& in, double* scratch,
+                                               LossAt loss_at) {
   const int i = threadIdx.x & 63;
   const bool act = i < N;
   // ---- Hedge ----
@@ -139,9 +152,25 @@ __device__ __forceinline__ void learner_update(double* logw, double* w, double e
     for (int l = 0; l < L; ++l) {
       const double li = loss_at(l);
       // l_A - l_i as sum_j p_j (l_j - l_i): equal to it because sum_j p_j = 1, and exactly
-      // zero when every drafter that carries weight has this drafter's loss
-      double dR = 0.0;
-      for (int j = 0; j < N; ++j) dR += lane_d(pv, j) * (lane_d(li, j) - li);
+      // zero when every drafter that carries weight has this drafter's loss. Every lane reads
+      // all (p_j, l_j) from LDS (the wave's own writes: LDS operations of a wave execute in
+      // order), in four interleaved partial sums combined in a fixed order.
+      scratch[i] = pv;
+      scratch[64 + i] = li;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;
+      int j = 0;
+      for (; j + 4 <= N; j += 4) {
+        d0 += scratch[j] * (scratch[64 + j] - li);
+        d1 += scratch[j + 1] * (scratch[64 + j + 1] - li);
+        d2 += scratch[j + 2] * (scratch[64 + j + 2] - li);
+        d3 += scratch[j + 3] * (scratch[64 + j + 3] - li);
+      }
+      for (; j < N; ++j) d0 += scratch[j] * (scratch[64 + j] - li);
+      const double dR = (d0 + d1) + (d2 + d3);
+      __builtin_amdgcn_wave_barrier();  // every lane has read before the next vector's writes
       if (act) Rv += dR;
       const double r = (act && Rv > 0.0) ? Rv : 0.0;
       const double M2 = wmax(r * r);
@@ -251,7 +280,8 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
     if (a.gamma_src != 0) return lossv[l * N + i];
     return a.loss_in[((int64_t)l * a.B + b) * N + i];
   };
-  learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in, loss_at);
+  learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in,
+                 lds + tail_lds_doubles(a) - kLearnScratch, loss_at);
   HS_TSTAMP(5);
 }
 
