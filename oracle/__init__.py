@@ -47,6 +47,8 @@ def _load():
         lib.or_alpha.restype = D
         lib.or_eval.argtypes = [P, I, I64, I, I64, I64, D, I, P, P, P, P, P]
         lib.or_eval.restype = I
+        lib.or_topl.argtypes = [P, I, I64, I, I64, I64, I, D, I, P, P, P]
+        lib.or_topl.restype = I
         lib.or_softmax_stats.argtypes = [P, I, I64, I64, I64, D, P, P, P]
         lib.or_softmax_stats.restype = I
         lib.or_path.argtypes = [P, I, I, P]
@@ -130,6 +132,32 @@ def evaluate(logits: np.ndarray, V: Optional[int] = None, T: float = 1.0, want_a
     return {"alpha": alpha.reshape(gshape + (N,)), "agree": agree.reshape(gshape + (N,)),
             "argmax": argmax.reshape(gshape + (R,)), "rmax": rmax.reshape(gshape + (R,)),
             "rlse": rlse.reshape(gshape + (R,))}
+
+
+def topl(logits: np.ndarray, L: int, V: Optional[int] = None, T: float = 1.0,
+         want_mass: bool = True):
+    """Theorem 2 (EAGLE): the target's probability mass on each drafter's Top_L tokens.
+
+    logits as in ``evaluate``. Returns dict with gamma [G..][N] (NaN when not want_mass),
+    hit [G..][N] (uint8: target argmax in Top_L) and idx [G..][N][L] (Top_L in rank order:
+    larger logit first, lower index first among equal logits).
+    """
+    R = logits.shape[0]
+    gshape = logits.shape[1:-1]
+    ld = logits.shape[-1]
+    V = ld if V is None else V
+    G = int(np.prod(gshape)) if gshape else 1
+    x = np.ascontiguousarray(logits).reshape(R, G, ld)
+    N = R - 1
+    gamma = np.full((G, N), np.nan)
+    hit = np.zeros((G, N), dtype=np.uint8)
+    idx = np.zeros((G, N, L), dtype=np.int32)
+    rc = _load().or_topl(_p(x), _dtype_of(x), ld, R, G, V, L, T, 1 if want_mass else 0,
+                         _p(gamma), _p(hit), _p(idx))
+    if rc != 0:
+        raise ValueError("or_topl failed: %d" % rc)
+    return {"gamma": gamma.reshape(gshape + (N,)), "hit": hit.reshape(gshape + (N,)),
+            "idx": idx.reshape(gshape + (N, L))}
 
 
 def softmax_stats(x: np.ndarray, V: Optional[int] = None, T: float = 1.0):

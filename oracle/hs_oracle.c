@@ -18,6 +18,11 @@
  *   or_eal_path, or_accept_len : pinned (Theorem 3 against brute force,
  *                             worked example of the censoring appendix, constant-gamma
  *                             closed form, range [1, K+1]).
+ *   or_topl                 : pinned (closed-form top-L masses of a target built from a
+ *                             known distribution, full vocabulary gives 1, brute-force
+ *                             enumeration of the dominating L-subset, ties and signed
+ *                             zeros by index, invariance under exact rescaling of the
+ *                             drafter, L = 1 greedy hit equals argmax agreement).
  *   or_window_losses        : pinned (all-accept and all-reject windows, K = 1, constant
  *                             gamma geometric sum, the censoring appendix's worked example).
  *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
@@ -140,6 +145,71 @@ int or_eval(const void* logits, int dtype, int64_t ld, int R, int64_t G, int64_t
   free(mx);
   free(am);
   return 0;
+}
+
+/*
+ * EAGLE acceptance probability (Theorem 2, proof in the appendix "Theorem 2 proof"):
+ * the greedy draft tree gives the node reached after the verified prefix the L children
+ * Top_L(q), the L tokens that the drafter ranks highest, and the next token is accepted
+ * when the target's sample is one of them:
+ *   gamma = sum_{v in Top_L(q)} p(v),   p = softmax(z_t / T).
+ * The drafter's ranking is that of its raw logits (a softmax at any temperature keeps it).
+ * Equal logits rank by lower token index first, as for the greedy argmax; -0 equals +0.
+ * Top_L is taken by L passes over the row, each picking the best unpicked token.
+ * Greedy decoding (one-hot p at the target's argmax): hit = 1 if that argmax is in Top_L.
+ *   logits     : [R][G][ld] as in or_eval (row 0 target, row 1 + i drafter i).
+ *   gamma      : [G][N] (when want_mass; needs T > 0), hit: [G][N], idx: [G][N][L] (Top_L in
+ *                rank order). Any output may be NULL.
+ */
+int or_topl(const void* logits, int dtype, int64_t ld, int R, int64_t G, int64_t V, int L,
+            double T, int want_mass, double* gamma, uint8_t* hit, int32_t* idx) {
+  if (R < 2 || G < 1 || V < 1 || ld < V || L < 1 || L > V) return -1;
+  if (want_mass && !(T > 0.0)) return -2;
+  int N = R - 1;
+  size_t es = (dtype == OR_F32) ? 4 : 2;
+  int rc = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t x = 0; x < (int64_t)N * G; ++x) {
+    int64_t g = x / N;
+    int i = (int)(x % N);
+    const char* zt = (const char*)logits + (size_t)((0 * G + g) * ld) * es;
+    const char* zq = (const char*)logits + (size_t)(((1 + i) * G + g) * ld) * es;
+    uint8_t* picked = (uint8_t*)calloc((size_t)V, 1);
+    int64_t* top = (int64_t*)malloc(sizeof(int64_t) * (size_t)L);
+    if (!picked || !top) {
+      rc = -3;
+    } else {
+      for (int r = 0; r < L; ++r) {
+        int64_t best = -1;
+        double qb = 0.0;
+        for (int64_t v = 0; v < V; ++v) {
+          if (picked[v]) continue;
+          double q = or_decode(zq, dtype, v);
+          if (best < 0 || q > qb) {
+            best = v;
+            qb = q;
+          }
+        }
+        picked[best] = 1;
+        top[r] = best;
+      }
+      double m, lse;
+      int64_t am;
+      or_row_stats(zt, dtype, V, want_mass ? T : 1.0, &m, &am, &lse);
+      if (want_mass && gamma) {
+        double s = 0.0, in = 0.0;
+        for (int64_t v = 0; v < V; ++v) s += exp((or_decode(zt, dtype, v) - m) / T);
+        for (int r = 0; r < L; ++r) in += exp((or_decode(zt, dtype, top[r]) - m) / T);
+        gamma[g * N + i] = in / s;
+      }
+      if (hit) hit[g * N + i] = picked[am];
+      if (idx)
+        for (int r = 0; r < L; ++r) idx[(g * N + i) * L + r] = (int32_t)top[r];
+    }
+    free(picked);
+    free(top);
+  }
+  return rc;
 }
 
 /* Row statistics of `rows` rows of a [rows][ld] tensor (one temperature softmax each). */

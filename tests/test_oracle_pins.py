@@ -457,3 +457,133 @@ def test_qfid_is_the_base_learners_on_the_window_stream_whatever_the_chunking():
         for q in results:
             assert np.array_equal(q.w[b], w[0]) and np.array_equal(q.R[b], R[0])
             assert np.array_equal(q.p[b], p[0]) and q.c[b] == c[0]
+
+
+# ------------------------------------------------------------------------------------------
+# Theorem 2 (EAGLE): gamma = sum of the target's p over the drafter's Top_L tokens
+# ------------------------------------------------------------------------------------------
+
+def _known_target(w: np.ndarray, T: float) -> np.ndarray:
+    """fp32 target logits whose softmax at temperature T is w (up to fp32 rounding)."""
+    return (T * np.log(w)).astype(np.float32)
+
+
+@pytest.mark.parametrize("T", [1.0, 0.5])
+@pytest.mark.parametrize("L", [1, 3, 10])
+def test_topl_closed_form_on_a_linear_target(T, L):
+    V = 200
+    w = np.arange(1, V + 1, dtype=np.float64)
+    w /= w.sum()
+    rising = np.arange(V, dtype=np.float32)  # ranks the last tokens first
+    x = np.stack([_known_target(w, T), rising, -rising])[:, None, :]
+    out = oracle.topl(x, L, T=T)
+    tri = V * (V + 1) / 2
+    assert abs(out["gamma"][0, 0] - sum(range(V - L + 1, V + 1)) / tri) < 1e-6
+    assert abs(out["gamma"][0, 1] - L * (L + 1) / 2 / tri) < 1e-6
+    assert list(out["idx"][0, 0]) == list(range(V - 1, V - 1 - L, -1))
+    assert list(out["idx"][0, 1]) == list(range(L))
+    # the target's argmax V-1 is the rising drafter's first choice, the falling one's last
+    assert out["hit"][0, 0] == 1 and out["hit"][0, 1] == 0
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_topl_full_vocabulary_has_mass_one_and_a_valid_order(bf16):
+    rng = np.random.default_rng(11)
+    V = 300
+    x = rng.normal(0, 3, (4, 2, V)).astype(np.float32)
+    x[2] = np.round(x[2])  # a drafter with many equal logits
+    if bf16:
+        x = _bf16(x)
+    out = oracle.topl(x, V, T=0.7)
+    assert np.all(np.abs(out["gamma"] - 1.0) < 1e-12)
+    assert np.all(out["hit"] == 1)
+    q = x.view(np.uint16).astype(np.uint32) << 16 if bf16 else x
+    q = q.view(np.float32) if bf16 else q
+    for g in range(2):
+        for i in range(3):
+            idx = out["idx"][g, i]
+            assert sorted(idx) == list(range(V))
+            v = q[1 + i, g, idx].astype(np.float64)
+            assert np.all(v[:-1] >= v[1:])
+            eq = v[:-1] == v[1:]
+            assert np.all(idx[:-1][eq] < idx[1:][eq])
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_topl_bruteforce_dominating_subset(seed):
+    """Top_L is the one L-subset whose every member ranks above every non-member."""
+    rng = np.random.default_rng(100 + seed)
+    V, T = 7, 0.8
+    zt = rng.normal(0, 2, V).astype(np.float32)
+    q = rng.integers(-2, 3, V).astype(np.float32)  # few levels: many ties
+    p = _softmax(zt, T)
+    x = np.stack([zt, q])[:, None, :]
+    for L in range(1, V + 1):
+        found = []
+        for S in itertools.combinations(range(V), L):
+            out_ = [u for u in range(V) if u not in S]
+            if all(q[v] > q[u] or (q[v] == q[u] and v < u) for v in S for u in out_):
+                found.append(set(S))
+        assert len(found) == 1
+        o = oracle.topl(x, L, T=T)
+        assert set(o["idx"][0, 0]) == found[0]
+        assert abs(o["gamma"][0, 0] - sum(p[v] for v in found[0])) < 1e-12
+        assert o["hit"][0, 0] == (int(np.argmax(zt)) in found[0])
+
+
+def test_topl_signed_zeros_rank_as_equal_by_index():
+    zt = np.zeros(4, dtype=np.float32)
+    for q, want in ((np.array([-0.0, 0.0, -1.0, 0.0], np.float32), [0, 1, 3]),
+                    (np.array([0.0, -0.0, -1.0, -0.0], np.float32), [0, 1, 3])):
+        for x in (np.stack([zt, q])[:, None, :], _bf16(np.stack([zt, q]))[:, None, :]):
+            assert list(oracle.topl(x, 3, T=1.0)["idx"][0, 0]) == want
+
+
+def test_topl_depends_on_the_drafter_only_through_its_ranking():
+    rng = np.random.default_rng(12)
+    V, L = 1000, 10
+    zt = rng.normal(0, 3, V).astype(np.float32)
+    q = rng.integers(-50, 50, V).astype(np.float32)
+    base = oracle.topl(np.stack([zt, q])[:, None, :], L, T=0.5)
+    for q2 in (q * 4, q * 0.25, q + 64, q - 1024):  # exact in fp32: same order, same ties
+        o = oracle.topl(np.stack([zt, q2.astype(np.float32)])[:, None, :], L, T=0.5)
+        assert np.array_equal(o["idx"], base["idx"]) and o["gamma"][0, 0] == base["gamma"][0, 0]
+    for T in (0.1, 3.0):  # the children do not depend on the temperature, only the mass does
+        assert np.array_equal(oracle.topl(np.stack([zt, q])[:, None, :], L, T=T)["idx"],
+                              base["idx"])
+
+
+def test_topl_mass_grows_by_the_next_ranked_probability():
+    rng = np.random.default_rng(13)
+    V, T = 64, 0.5
+    w = rng.dirichlet(np.ones(V))
+    x = np.stack([_known_target(w, T), rng.normal(0, 1, V).astype(np.float32)])[:, None, :]
+    prev = oracle.topl(x, 1, T=T)
+    assert abs(prev["gamma"][0, 0] - w[prev["idx"][0, 0, 0]]) < 1e-6
+    for L in range(2, V + 1):
+        cur = oracle.topl(x, L, T=T)
+        assert np.array_equal(cur["idx"][0, 0, :L - 1], prev["idx"][0, 0])
+        assert abs(cur["gamma"][0, 0] - prev["gamma"][0, 0] - w[cur["idx"][0, 0, L - 1]]) < 1e-6
+        prev = cur
+    assert abs(prev["gamma"][0, 0] - 1.0) < 1e-6
+
+
+def test_topl_single_child_hit_is_greedy_agreement():
+    rng = np.random.default_rng(14)
+    x = _bf16(rng.normal(0, 2, (6, 3, 500)).astype(np.float32))
+    x[2] = x[0]           # a drafter that copies the target
+    x[3, :, 17] = 0x7F7F  # and one whose argmax is planted away from the target's
+    hit = oracle.topl(x, 1, want_mass=False)["hit"]
+    agree = oracle.evaluate(x, want_alpha=False)["agree"]
+    assert np.array_equal(hit, agree) and np.all(hit[:, 1] == 1) and np.all(hit[:, 2] == 0)
+
+
+def test_topl_rejects_bad_arguments():
+    x = np.zeros((2, 1, 8), dtype=np.float32)
+    with pytest.raises(ValueError):
+        oracle.topl(x, 9)
+    with pytest.raises(ValueError):
+        oracle.topl(x, 0)
+    with pytest.raises(ValueError):
+        oracle.topl(x, 2, T=0.0)
+    assert oracle.topl(x, 2, T=0.0, want_mass=False)["hit"][0, 0] == 1
