@@ -53,6 +53,7 @@ extern "C" {
 #define HS_MAX_DRAFTERS 64 /* N: one wave64 lane per drafter in the learner kernel  */
 #define HS_MAX_POSITIONS 64 /* K (chain positions) or M (tree nodes)                */
 #define HS_MAX_QUERIES 65535
+#define HS_MAX_TOPL 32      /* L: children per draft-tree node in hs_eval_topl           */
 /* V: at most 512 * 256 16-byte vectors per row (1048576 bf16 or 524288 fp32 logits), and
    the device must hold ceil(V / 2048) (bf16) or ceil(V / 1024) (fp32) evaluation
    workgroups at once: hs_eval_alpha returns HS_ERR_LIMIT otherwise. */
@@ -130,6 +131,39 @@ int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, in
                   int64_t V, int dtype, float temperature, int mode, float* alpha, uint8_t* agree,
                   int32_t* argmax_t, int32_t* argmax_d, void* workspace, size_t workspace_bytes,
                   void* stream);
+
+/* Bytes of device workspace hs_eval_topl needs for this shape (0 on invalid shapes). */
+size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dtype);
+
+/*
+ * hs_eval_topl - EAGLE acceptance probabilities of N drafters (Theorem 2; Section 2.3 and
+ * Section 3.2's gamma for EAGLE's greedy draft tree). The tree gives the node after a
+ * verified prefix the drafter's L highest-ranked tokens as children, Top_L(q_i), and the
+ * target accepts one of them with probability
+ *   gamma[b][i][k] = sum_{v in Top_L(drafter_i[b][k])} p(v),  p = softmax(target[b][k] / T),
+ * accumulated in fp32 and clamped to [0, 1]. The ranking is that of the raw drafter logits
+ * (a softmax at any temperature keeps it); equal logits rank lower token index first, and
+ * -0 ranks as +0. Logits must not be NaN.
+ *   hit[b][i][k]      = 1 if the target's argmax (lowest index of its row maximum) is in
+ *                       Top_L, else 0: gamma of greedy decoding (one-hot p).
+ *   children[b][i][k] = Top_L in rank order, L int32 token indices.
+ * target, drafters_host, N, B, K, V, dtype: as in hs_eval_alpha (K positions or tree nodes).
+ * L            : children per node, 1 <= L <= min(V, HS_MAX_TOPL) (EAGLE's default is 10).
+ * gamma        : [B][N][K] fp32 or NULL. Needs T finite and > 0 when non-NULL.
+ * hit          : [B][N][K] uint8 or NULL.
+ * children     : [B][N][K][L] int32 or NULL.
+ * mode         : HS_SAMPLE requires gamma, HS_GREEDY requires hit; any other non-NULL
+ *                output is filled as well.
+ * workspace    : at least hs_eval_topl_workspace_size() bytes of device memory, 256-byte
+ *                aligned; scratch only (no initialisation needed, contents undefined after).
+ * Two launches: each logit is read from HBM once, by the first; the second merges the
+ * per-slice candidates (about 12 L bytes per row slice). Deterministic for a given shape.
+ * Not covered: EAGLE-2's dynamic pruning, whose candidate set is the pruned subtree.
+ */
+int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
+                 int64_t V, int dtype, int L, float temperature, int mode, float* gamma,
+                 uint8_t* hit, int32_t* children, void* workspace, size_t workspace_bytes,
+                 void* stream);
 
 /*
  * hs_accept_len - Theorem 3's one-step counterfactual acceptance-length

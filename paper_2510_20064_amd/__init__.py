@@ -2,8 +2,8 @@
 
 Argument marshalling only: every step runs in the library's HIP kernels. PyTorch supplies
 device memory and the current HIP stream. The function names match the C ABI declared in
-include/hedgespec.h (hs_softmax_stats, hs_eval_alpha, hs_accept_len, hs_hedge_update,
-hs_normalhedge_update, hs_round). There is no CPU fallback: if the library is not built,
+include/hedgespec.h (hs_softmax_stats, hs_eval_alpha, hs_eval_topl, hs_accept_len,
+hs_hedge_update, hs_normalhedge_update, hs_delayed_update, hs_round). There is no CPU fallback: if the library is not built,
 loading raises.
 """
 from __future__ import annotations
@@ -70,6 +70,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_eval_alpha_workspace_size.argtypes = [I, I, I, I64, I]
     lib.hs_eval_alpha_workspace_size.restype = SZ
     lib.hs_eval_alpha.argtypes = [VP, VP, I, I, I, I64, I, F, I, P, P, P, P, P, SZ, P]
+    lib.hs_eval_topl_workspace_size.argtypes = [I, I, I, I64, I, I]
+    lib.hs_eval_topl_workspace_size.restype = SZ
+    lib.hs_eval_topl.argtypes = [VP, VP, I, I, I, I64, I, I, F, I, P, P, P, P, SZ, P]
     lib.hs_accept_len.argtypes = [P, P, I, I, I, I, P, P, P, P, I, P, P]
     lib.hs_hedge_update.argtypes = [P, P, P, I, I, I, D, P]
     lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
@@ -78,7 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
-    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_accept_len", "hs_hedge_update",
+    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_eval_topl", "hs_accept_len", "hs_hedge_update",
                  "hs_normalhedge_update", "hs_round", "hs_delayed_update", "hs_version"]:
         getattr(lib, name).restype = I
     _lib = lib
@@ -190,6 +193,43 @@ def eval_alpha(target: torch.Tensor, drafters=None, V: Optional[int] = None,
                              _ptr(o.get("alpha")), _ptr(o.get("agree")), _ptr(o.get("argmax_t")),
                              _ptr(o.get("argmax_d")), _ptr(workspace), workspace.numel(),
                              _stream(stream)))
+    return o
+
+
+def topl_workspace_size(B: int, N: int, K: int, V: int, L: int, dtype: int) -> int:
+    return int(load_library().hs_eval_topl_workspace_size(B, N, K, V, L, dtype))
+
+
+def eval_topl(target: torch.Tensor, drafters=None, L: int = 10, V: Optional[int] = None,
+              temperature: float = 1.0, mode: int = SAMPLE, want_gamma: Optional[bool] = None,
+              want_hit: Optional[bool] = None, want_children: bool = False,
+              workspace: Optional[torch.Tensor] = None, out: Optional[dict] = None, stream=None):
+    """hs_eval_topl (Theorem 2). Returns a dict of device tensors: gamma [B][N][K] f32,
+    hit [B][N][K] u8, children [B][N][K][L] i32 (those requested)."""
+    lib = load_library()
+    t, ds = _split_logits(target, drafters)
+    B, K, ld = t.shape
+    N = len(ds)
+    V = ld if V is None else V
+    dt = _dtype_code(t)
+    dev = t.device
+    want_gamma = (mode == SAMPLE) if want_gamma is None else want_gamma
+    want_hit = (mode == GREEDY) if want_hit is None else want_hit
+    o = {} if out is None else out
+    if want_gamma and "gamma" not in o:
+        o["gamma"] = torch.empty((B, N, K), dtype=torch.float32, device=dev)
+    if want_hit and "hit" not in o:
+        o["hit"] = torch.empty((B, N, K), dtype=torch.uint8, device=dev)
+    if want_children and "children" not in o:
+        o["children"] = torch.empty((B, N, K, L), dtype=torch.int32, device=dev)
+    if workspace is None:
+        n = topl_workspace_size(B, N, K, V, L, dt)
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+    tv = _view(t)
+    dv = (hs_view * N)(*[_view(d) for d in ds])
+    _check(lib.hs_eval_topl(ctypes.byref(tv), dv, N, B, K, V, dt, L, temperature, mode,
+                            _ptr(o.get("gamma")), _ptr(o.get("hit")), _ptr(o.get("children")),
+                            _ptr(workspace), workspace.numel(), _stream(stream)))
     return o
 
 

@@ -239,6 +239,90 @@ HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, in
   return rc ? rc : ok();
 }
 
+namespace {
+
+struct TopReq {
+  const hs_view* target;
+  const hs_view* drafters;
+  int N, B, K;
+  int64_t V;
+  int dtype, L;
+  float T;
+  int mode;
+  float* gamma;
+  uint8_t* hit;
+  int32_t* children;
+  void* ws;
+  size_t ws_bytes;
+};
+
+int validate_topl(const TopReq& q, hs::TeamGeom* g, hs::RowTable* rows) {
+  int rc = check_shape(q.B, q.N, q.K, q.V);
+  if (rc) return rc;
+  if (q.dtype != HS_F32 && q.dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
+  if (q.mode != HS_SAMPLE && q.mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", q.mode);
+  if (q.L < 1 || q.L > HS_MAX_TOPL || q.L > q.V)
+    return fail(HS_ERR_SHAPE, "need 1 <= L <= min(V, %d) (got L=%d, V=%lld)", HS_MAX_TOPL, q.L,
+                (long long)q.V);
+  if (!q.drafters) return fail(HS_ERR_NULL, "drafters_host is NULL");
+  if ((rc = check_view(q.target, q.dtype, "target"))) return rc;
+  for (int i = 0; i < q.N; ++i) {
+    char what[32];
+    snprintf(what, sizeof(what), "drafter %d", i);
+    if ((rc = check_view(&q.drafters[i], q.dtype, what))) return rc;
+  }
+  if (q.mode == HS_SAMPLE && !q.gamma) return fail(HS_ERR_NULL, "sample mode needs gamma");
+  if (q.mode == HS_GREEDY && !q.hit) return fail(HS_ERR_NULL, "greedy mode needs hit");
+  if (q.gamma && !(isfinite(q.T) && q.T > 0.0f))
+    return fail(HS_ERR_TEMPERATURE, "temperature must be finite and > 0 (got %g)", (double)q.T);
+  if (!hs::team_geom(q.B, q.N, q.K, q.V, q.dtype, g))
+    return fail(HS_ERR_LIMIT, "V = %lld is beyond the evaluation limit of %lld logits per row",
+                (long long)q.V, (long long)hs::kMaxTeamSlices * hs::kThreads * (16 / elem_bytes(q.dtype)));
+  const size_t need = hs::topl_ws_bytes(*g, q.L);
+  if (!q.ws) return fail(HS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (q.ws_bytes < need)
+    return fail(HS_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", q.ws_bytes, need);
+  if (((uintptr_t)q.ws & 255) != 0) return fail(HS_ERR_ALIGN, "workspace must be 256-byte aligned");
+  rows->ptr[0] = q.target->ptr;
+  rows->sb[0] = q.target->stride_b;
+  rows->sk[0] = q.target->stride_k;
+  for (int i = 0; i < q.N; ++i) {
+    rows->ptr[1 + i] = q.drafters[i].ptr;
+    rows->sb[1 + i] = q.drafters[i].stride_b;
+    rows->sk[1 + i] = q.drafters[i].stride_k;
+  }
+  for (int r = q.N + 1; r < hs::kMaxRows; ++r) {
+    rows->ptr[r] = nullptr;
+    rows->sb[r] = rows->sk[r] = 0;
+  }
+  return HS_OK;
+}
+
+}  // namespace
+
+HS_API size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dtype) {
+  hs::TeamGeom g;
+  if (L < 1 || L > HS_MAX_TOPL || L > V || !hs::team_geom(B, N, K, V, dtype, &g)) return 0;
+  return hs::topl_ws_bytes(g, L);
+}
+
+HS_API int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
+                        int64_t V, int dtype, int L, float temperature, int mode, float* gamma,
+                        uint8_t* hit, int32_t* children, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  TopReq q{target, drafters_host, N, B, K, V, dtype, L, temperature, mode, gamma, hit, children,
+           workspace, workspace_bytes};
+  hs::TeamGeom g;
+  hs::RowTable rows;
+  int rc = validate_topl(q, &g, &rows);
+  if (rc) return rc;
+  const float c = gamma ? (float)(1.4426950408889634 / (double)temperature) : 0.0f;
+  rc = hs::launch_topl(g, rows, L, c, gamma != nullptr, gamma, hit, children,
+                       reinterpret_cast<char*>(workspace), (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
 HS_API int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
                          const int32_t* parent_host, const int32_t* path_end, double* eal,
                          double* prefix, int loss_kind, double* loss, void* stream) {

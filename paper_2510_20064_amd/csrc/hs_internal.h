@@ -268,6 +268,11 @@ struct DelayArgs {
   int32_t* nloss;  // [B] or NULL: how many
 };
 int launch_delayed(const DelayArgs& a, hipStream_t stream);
+// EAGLE acceptance mass (hs_topl.hip): per-slice candidates, then the merge. Workspace bytes
+// for a shape, and the two launches.
+size_t topl_ws_bytes(const TeamGeom& g, int L);
+int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool want_sum,
+                float* gamma, uint8_t* hit, int32_t* idx, char* ws, hipStream_t stream);
 // Evaluation of one round: the team kernel (which also advances the workspace epoch) and, when
 // tail != nullptr, the learner step on its alpha or agreement.
 int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,

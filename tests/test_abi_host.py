@@ -164,3 +164,42 @@ def test_delayed_update_validation_codes():
     assert _delayed(lib, w=None) == 1
     assert _delayed(lib, c=None) == 1
     assert _delayed(lib, eta=float("inf")) == 10
+
+
+def _topl(lib, **kw):
+    a = dict(target=hs.hs_view(FAKE, 8 * 151936, 151936), N=8, B=1, K=8, V=151936, dtype=1,
+             L=10, T=1.0, mode=0, gamma=FAKE, hit=None, children=None, ws=FAKE * 16,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    d = kw.get("drafters", _views(a["N"]))
+    tv = a["target"]
+    return lib.hs_eval_topl(ctypes.byref(tv) if tv is not None else None, d, a["N"], a["B"],
+                            a["K"], a["V"], a["dtype"], a["L"], a["T"], a["mode"], a["gamma"],
+                            a["hit"], a["children"], a["ws"], a["ws_bytes"], None)
+
+
+def test_eval_topl_validation_codes():
+    lib = hs.load_library()
+    assert lib.hs_eval_topl_workspace_size(1, 8, 8, 151936, 10, 1) > 0
+    assert lib.hs_eval_topl_workspace_size(1, 8, 8, 151936, 33, 1) == 0
+    assert lib.hs_eval_topl_workspace_size(1, 8, 8, 5, 6, 1) == 0
+    assert lib.hs_eval_topl_workspace_size(1, 8, 8, 151936, 10, 7) == 0
+    assert _topl(lib, N=0) == 2
+    assert _topl(lib, L=0) == 2
+    assert _topl(lib, L=33) == 2
+    assert _topl(lib, V=9, L=10) == 2
+    assert _topl(lib, N=65, drafters=_views(65)) == 8
+    assert _topl(lib, dtype=5) == 3
+    assert _topl(lib, mode=3) == 10
+    assert _topl(lib, target=None) == 1
+    assert _topl(lib, drafters=None) == 1
+    assert _topl(lib, gamma=None) == 1  # sample mode needs gamma
+    assert _topl(lib, mode=1, gamma=None, hit=None) == 1
+    assert _topl(lib, T=0.0) == 5
+    assert _topl(lib, T=float("inf")) == 5
+    assert _topl(lib, target=hs.hs_view(FAKE + 2, 8 * 151936, 151936)) == 4
+    assert _topl(lib, drafters=_views(8, sk=3)) == 4
+    assert _topl(lib, V=1 << 22) == 8
+    assert _topl(lib, ws=None) == 7
+    assert _topl(lib, ws_bytes=1000) == 7
+    assert _topl(lib, ws=FAKE * 16 + 8) == 4

@@ -1,0 +1,135 @@
+"""GPU parity of hs_eval_topl (Theorem 2, EAGLE's top-L acceptance mass) against the oracle.
+
+Tolerances: the children (Top_L in rank order) and the greedy hit are bit-exact, since both
+sides rank the same stored logits by value and then by lower index; gamma, a sum of at most 32
+fp32 softmax terms against fp32 slice normalisers, within 2e-5 absolute (the alpha tolerance).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2510_20064_amd as hs
+import synth
+
+pytestmark = pytest.mark.gpu
+
+GAMMA_TOL = 2e-5
+WL = synth.workloads()
+
+
+def note(msg):
+    print("\n[case] " + msg, flush=True)
+
+
+def to_dev(x: np.ndarray) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if x.dtype == np.uint16:
+        t = t.view(torch.bfloat16)
+    return t.cuda()
+
+
+def run_topl(x, L, V=None, T=1.0, mode=hs.SAMPLE, children=True):
+    out = hs.eval_topl(to_dev(x), L=L, V=V, temperature=T, mode=mode,
+                       want_gamma=(mode == hs.SAMPLE), want_hit=True, want_children=children)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def check(x, L, V=None, T=1.0, mode=hs.SAMPLE, groups=None):
+    """GPU on the whole [R][B][K][ld] tensor; the oracle on `groups` ((b, k) list, None = all)."""
+    got = run_topl(x, L, V=V, T=T, mode=mode)
+    if groups is None:
+        B, K = x.shape[1], x.shape[2]
+        groups = [(b, k) for b in range(B) for k in range(K)]
+    sub = np.stack([x[:, b, k] for (b, k) in groups], axis=1)
+    ref = oracle.topl(sub, L, V=V, T=T, want_mass=(mode == hs.SAMPLE))
+    worst = 0.0
+    for gi, (b, k) in enumerate(groups):
+        assert np.array_equal(got["children"][b, :, k], ref["idx"][gi]), (b, k)
+        assert np.array_equal(got["hit"][b, :, k], ref["hit"][gi]), (b, k)
+        if mode == hs.SAMPLE:
+            worst = max(worst, float(np.abs(got["gamma"][b, :, k] - ref["gamma"][gi]).max()))
+    assert worst <= GAMMA_TOL, worst
+    return got
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
+@pytest.mark.parametrize("N", [1, 3, 8, 11])
+@pytest.mark.parametrize("L", [1, 10, 32])
+def test_topl_small_ragged(dtype, N, L):
+    # several slices and a ragged tail (V not a multiple of the 16-byte vector either)
+    w = synth.variant(WL["qwen3_8b_single"], B=2, K=3, N=N, V=5003, ld=5008, dtype=dtype,
+                      scales=[0.3 + 0.2 * i for i in range(N)], permute=False)
+    note("small ragged dtype=%d N=%d L=%d" % (dtype, N, L))
+    check(synth.generate(w), L, V=w.V, T=0.7)
+
+
+def test_topl_greedy_mode_hits_only():
+    w = synth.variant(WL["qwen3_8b_single"], B=2, K=4, V=9000)
+    x = synth.generate(w)
+    x[3] = x[0]  # a drafter identical to the target: every hit is 1
+    note("greedy hits")
+    got = check(x, 10, mode=hs.GREEDY)
+    assert np.all(got["hit"][:, 2, :] == 1)
+
+
+def _bf16(a):
+    u = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def test_topl_ties_signed_zeros_and_infinities():
+    rng = np.random.default_rng(21)
+    V = 6000
+    R, B, K = 7, 1, 4
+    z = rng.normal(0, 2, (R, B, K, V)).astype(np.float32)
+    z[1] = np.round(z[1])                 # few levels: ties across slices
+    z[2] = 0.0                            # one level: Top_L is the first L tokens
+    z[2, :, :, ::3] = -0.0                # ... with signed zeros among them
+    z[3] = -np.inf                        # fewer than L finite logits, all in the tail slice
+    z[3, :, :, 5990:5995] = rng.normal(0, 1, 5).astype(np.float32)
+    z[4, :, :, :] = -np.inf               # no finite logit at all
+    z[0, :, 1, ::2] = -np.inf             # a target with masked tokens
+    z[5] = z[0]                           # a copy of the target
+    z[6] = -z[0]
+    for x in (z, _bf16(z)):
+        note("ties, zeros, infinities dtype=%s" % x.dtype)
+        for L in (1, 7, 32):
+            check(x, L, T=0.9)
+
+
+def test_topl_full_size_single_query():
+    w = WL["qwen3_8b_single"]
+    note("qwen3_8b_single full, L=10")
+    check(synth.generate(w), 10, T=w.temperature)
+
+
+def test_topl_large_pool_sampled_groups():
+    w = WL["large_pool_stream"]
+    note("large_pool_stream full shape, sampled groups")
+    x = synth.generate(w)
+    check(x, 10, T=w.temperature, groups=[(0, 0), (7, 3), (31, 7)])
+
+
+def test_topl_longest_rows_and_crowded_merge():
+    # V at the limit (512 slices). The first token of every slice is the largest, so the merge
+    # sees more than its LDS holds above the first threshold and searches the lists in place.
+    V = 2048 * 512
+    rng = np.random.default_rng(22)
+    z = rng.normal(0, 1, (2, 1, 1, V)).astype(np.float32)
+    z[1, 0, 0, ::2048] = 100.0
+    x = _bf16(z)
+    note("V=%d crowded merge" % V)
+    got = check(x, 32, T=1.0)
+    assert list(got["children"][0, 0, 0]) == [2048 * s for s in range(32)]
+
+
+def test_topl_deterministic_and_workspace_reuse():
+    w = synth.variant(WL["qwen3_8b_single"], V=40000)
+    x = to_dev(synth.generate(w))
+    note("determinism")
+    a = hs.eval_topl(x, L=10, want_children=True)
+    b = hs.eval_topl(x, L=10, want_children=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a["gamma"], b["gamma"]) and torch.equal(a["children"], b["children"])
