@@ -278,6 +278,8 @@ int validate_topl(const TopReq& q, hs::TeamGeom* g, hs::RowTable* rows) {
   if (!hs::team_geom(q.B, q.N, q.K, q.V, q.dtype, g))
     return fail(HS_ERR_LIMIT, "V = %lld is beyond the evaluation limit of %lld logits per row",
                 (long long)q.V, (long long)hs::kMaxTeamSlices * hs::kThreads * (16 / elem_bytes(q.dtype)));
+  if (!hs::topl_fits(*g))
+    return fail(HS_ERR_LIMIT, "B * K * (N + 1) * ceil(V / slice) must stay below 2^31");
   const size_t need = hs::topl_ws_bytes(*g, q.L);
   if (!q.ws) return fail(HS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
   if (q.ws_bytes < need)

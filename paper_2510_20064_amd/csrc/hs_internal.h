@@ -271,6 +271,7 @@ int launch_delayed(const DelayArgs& a, hipStream_t stream);
 // EAGLE acceptance mass (hs_topl.hip): per-slice candidates, then the merge. Workspace bytes
 // for a shape, and the two launches.
 size_t topl_ws_bytes(const TeamGeom& g, int L);
+bool topl_fits(const TeamGeom& g);  // work units and rows index with 31 bits
 int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool want_sum,
                 float* gamma, uint8_t* hit, int32_t* idx, char* ws, hipStream_t stream);
 // Evaluation of one round: the team kernel (which also advances the workspace epoch) and, when

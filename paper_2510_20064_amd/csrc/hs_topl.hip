@@ -3,20 +3,21 @@
 // and the target accepts one of them with probability gamma = sum_{v in Top_L(q)} p(v).
 //
 // Two launches:
-//   1. hs_topl_slice_kernel, one workgroup per (query, position, row set, slice): every logit
-//      is read once. The target's slice goes to LDS and, for the first row set, into its
-//      softmax statistics (max, lowest argmax, exp2 sum). Each wave owns whole drafter-row
-//      slices and writes the slice's local Top_L as exact integer keys, with the target
-//      logit at each candidate gathered from LDS.
+//   1. hs_topl_slice_kernel: every logit is read once. A work unit is one slice (2048 bf16 or
+//      1024 fp32 logits) of one row of one (query, position), and one wave does it alone:
+//      for the target row, the slice's softmax statistics (max, lowest argmax, exp2 sum);
+//      for a drafter row, the slice's local Top_L as exact integer keys. The waves of a
+//      workgroup share nothing (no barrier), and the target row is read once per slice.
 //   2. hs_topl_merge_kernel, one wave per (query, drafter, position): the global Top_L among
-//      the slices' candidates, the target's normaliser from the slice statistics, and gamma,
-//      the greedy hit and the ranked children.
+//      the slices' candidates, the target's normaliser from the slice statistics, the target
+//      logits of the L winners (gathered from the logits), and gamma, the greedy hit and the
+//      ranked children.
 //
 // Ranking keys. A logit becomes a signed integer that orders like its value (-0 and +0 map to
 // the same integer), and its token index is appended so that equal logits rank lower index
-// first. Keys are therefore distinct, and "the L-th largest key" is found by a bitwise search
-// with wave ballots over just the bits in which the keys differ.
-#include "hs_rowstats.h"
+// first. Keys are therefore distinct: the L-th largest of a set of keys is the one with
+// exactly L - 1 larger ones, found by counting (or, for long lists, by a bitwise search with
+// wave ballots over the bits in which the keys differ).
 #include "hs_wave.h"
 
 namespace hs {
@@ -26,21 +27,58 @@ namespace {
 constexpr int kMaxTopL = HS_MAX_TOPL;
 constexpr int kMergeCap = 512;  // candidates per wave held in LDS by the merge
 
+// Division of a 32-bit value by a divisor fixed for the launch, by a multiply-high and two
+// shifts (Granlund and Montgomery, "Division by invariant integers using multiplication",
+// 1994): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// q = (t + ((n - t) >> 1)) >> (l - 1), t = mulhi(m, n); d = 1 uses shifts 0 and 0.
+struct FastDiv {
+  uint32_t d, m, s1, s2;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while (l < 32 && ((uint64_t)1 << l) < d) ++l;
+  FastDiv f;
+  f.d = d;
+  f.m = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1);
+  f.s1 = l > 0 ? 1 : 0;
+  f.s2 = l > 0 ? l - 1 : 0;
+  return f;
+}
+__device__ inline uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  const uint32_t t = __umulhi(f.m, n);
+  return (t + ((n - t) >> f.s1)) >> f.s2;
+}
+
 struct TopArgs {
   RowTable rows;
-  int B, N, K, D, nsub, S, L;
+  int B, N, K, S, L;
   int64_t V, nvec;
-  float c;       // log2(e) / T; 0 when no mass is wanted
-  int want_sum;  // target exp2 sums (the mass needs them)
-  int64_t* ckey; // [B*N*K][S][L] candidate keys of each slice (kNone64: no candidate)
-  float* czt;    // [B*N*K][S][L] target logit at the candidate's token
-  float4* tstat; // [B*K][S]: slice max, exp2 offset, exp2 sum, argmax (bits)
-  float* gamma;  // [B][N][K]
-  uint8_t* hit;  // [B][N][K]
-  int32_t* idx;  // [B][N][K][L]
+  uint32_t units;  // B * K * (N + 1) * S work units of the first launch
+  FastDiv divS, divR, divK, divNK;  // by S, N + 1, K and N * K
+  float c;         // log2(e) / T; 0 when no mass is wanted
+  int want_sum;    // target exp2 sums (the mass needs them)
+  int want_arg;    // target argmax (the greedy hit needs it)
+  int64_t* ckey;   // [B*N*K][S][L] candidate keys of each slice (kNone64: no candidate)
+  float4* tstat;   // [B*K][S]: slice max, exp2 offset, exp2 sum, argmax (bits)
+  float* gamma;    // [B][N][K]
+  uint8_t* hit;    // [B][N][K]
+  int32_t* idx;    // [B][N][K][L]
+#ifdef HS_TRACE
+  uint64_t* trace;  // per workgroup of each launch: 16 phase timestamps of wave 0, lane 0
+#endif
 };
 
+#ifdef HS_TRACE
+uint64_t* g_topl_trace = nullptr;
+#define HS_TSTAMP(base, i)                                                       \
+  if (threadIdx.x == 0 && A.trace)                                               \
+  A.trace[((size_t)(base) + blockIdx.x) * 16 + (i)] = __builtin_amdgcn_s_memrealtime()
+#else
+#define HS_TSTAMP(base, i)
+#endif
+
 constexpr int64_t kNone64 = INT64_MIN;
+constexpr uint64_t kFlip64 = 0x8000000000000000ull;
 
 // ---- integer images of logits --------------------------------------------------------------
 
@@ -63,10 +101,10 @@ __device__ inline int32_t f32_ordered(float f) {
   return (x ^ (m & 0x7FFFFFFF)) - m;
 }
 
-// Key layout per storage type. A lane's E logits of a row slice are vectors
-// q * 64 + lane (q = 0..3) of the slice, so element e of vector q has slice index
-// j = q * 64 * VE + lane * VE + e. The key is (ordered value, 0xFF..F - j); it is built
-// from a lane-independent part (0xFF..F - q * 64 * VE - e) and the lane's share lane * VE is
+// Key layout per storage type. A lane's E logits of a row slice are vectors i * 64 + lane
+// (i = 0..3) of the slice, so element e of vector i has slice index
+// j = i * 64 * VE + lane * VE + e. The key is (ordered value, 0xFF..F - j); it is built from a
+// lane-independent part (0xFF..F - i * 64 * VE - e) and the lane's share lane * VE is
 // subtracted once from the lane maximum, or added to a threshold.
 template <int DT>
 struct KeyOf;
@@ -76,18 +114,28 @@ struct KeyOf<HS_BF16> {
   using U = uint32_t;
   static constexpr int VE = 8;
   static constexpr int E = 4 * VE;
-  static constexpr int kBits = 16;            // index bits
   static constexpr K kNone = INT32_MIN + 1024;  // stays below every real key after - lane * VE
+  static constexpr K kMin = INT32_MIN;
   static constexpr K kValidMin = INT32_MIN + 65536;
   static constexpr U kFlip = 0x80000000u;
-  __device__ static inline void build(const uint4& x, int q, K (&k)[E]) {
+  // Both keys of a word by byte permutes: lo = (value of element 2h, index part of 2h),
+  // hi = (value of 2h + 1, index part of 2h + 1); the index parts are constants kept in scalar
+  // registers (a vector op cannot take a 32-bit literal here).
+  __device__ static inline void build(const uint4& x, int i, K (&k)[E]) {
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    uint32_t sel_lo, sel_hi;
+    asm volatile("s_mov_b32 %0, 0x05040100" : "=s"(sel_lo));
+    asm volatile("s_mov_b32 %0, 0x07060302" : "=s"(sel_hi));
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const uint32_t o = bf16x2_ordered(w[h]);
-      const uint32_t j0 = (uint32_t)(q * 64 * VE + 2 * h);
-      k[q * VE + 2 * h] = (K)((o << 16) | (0xFFFFu - j0));
-      k[q * VE + 2 * h + 1] = (K)((o & 0xFFFF0000u) | (0xFFFFu - j0 - 1));
+      const uint32_t j0 = (uint32_t)(i * 64 * VE + 2 * h);
+      uint32_t cc;  // (0xFFFF - j0 - 1) << 16 | (0xFFFF - j0)
+      asm volatile("s_mov_b32 %0, %1"
+                   : "=s"(cc)
+                   : "i"((int32_t)(((0xFFFFu - j0 - 1) << 16) | (0xFFFFu - j0))));
+      k[i * VE + 2 * h] = (K)__builtin_amdgcn_perm(o, cc, sel_lo);
+      k[i * VE + 2 * h + 1] = (K)__builtin_amdgcn_perm(o, cc, sel_hi);
     }
   }
   // slice index and global key of a true (lane share removed) key
@@ -102,16 +150,16 @@ struct KeyOf<HS_F32> {
   using U = uint64_t;
   static constexpr int VE = 4;
   static constexpr int E = 4 * VE;
-  static constexpr int kBits = 32;
   static constexpr K kNone = INT64_MIN + 1024;
+  static constexpr K kMin = INT64_MIN;
   static constexpr K kValidMin = INT64_MIN + ((int64_t)1 << 32);
   static constexpr U kFlip = 0x8000000000000000ull;
-  __device__ static inline void build(const float4& x, int q, K (&k)[E]) {
+  __device__ static inline void build(const float4& x, int i, K (&k)[E]) {
     const float f[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      k[q * VE + e] = (K)(((uint64_t)(int64_t)f32_ordered(f[e]) << 32) |
-                          (uint64_t)(0xFFFFFFFFu - (uint32_t)(q * 64 * VE + e)));
+      k[i * VE + e] = (K)(((uint64_t)(int64_t)f32_ordered(f[e]) << 32) |
+                          (uint64_t)(0xFFFFFFFFu - (uint32_t)(i * 64 * VE + e)));
   }
   __device__ static inline int slice_index(K k) { return (int)(0xFFFFFFFFu - (uint32_t)k); }
   __device__ static inline int64_t global_key(K k, int64_t g) {
@@ -141,6 +189,27 @@ __device__ inline uint64_t first_lane(uint64_t x) {
 }
 __device__ inline int highest_bit(uint32_t x) { return 31 - __builtin_clz(x); }
 __device__ inline int highest_bit(uint64_t x) { return 63 - __builtin_clzll(x); }
+__device__ inline int32_t bcast(int32_t x, int l) { return __builtin_amdgcn_readlane(x, l); }
+__device__ inline int64_t bcast(int64_t x, int l) {
+  return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)((uint64_t)x >> 32), l) << 32) |
+                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)x, l));
+}
+__device__ inline int mbcnt(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+// LDS written by some lanes of the wave, then read by others.
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+// The key of the neighbouring lane (lanes 2i and 2i + 1 swap).
+__device__ inline int32_t lane_swap(int32_t x) { return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, true); }
+__device__ inline int64_t lane_swap(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(uint64_t)x, 0xB1, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)((uint64_t)x >> 32), 0xB1, 0xF, 0xF, true);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 
 // The largest x with #{u >= x} >= L over the keys u (unsigned images, 0 = no key) spread over
 // the wave: u[j] for j < nu (wave-uniform) in every lane. The keys are distinct, so with at
@@ -181,17 +250,30 @@ __device__ inline U wave_kth(const U (&u)[NU], int nu, int L) {
   return cur;
 }
 
-// Inclusive prefix sum over the wave (lane l gets sum of lanes 0..l).
-__device__ inline int wave_incl_scan(int x) {
-  const int lane = threadIdx.x & 63;
+// How many of the keys buf[0..n) exceed `mine`, n <= 64 wave-uniform. buf is 16-byte aligned
+// and holds the smallest key value from n up to the next multiple of 16 (so no key needs a
+// bounds test). All lanes read the same addresses (broadcasts), 16 keys per batch.
+template <typename K>
+__device__ inline int rank_in(const K* buf, int n, K mine) {
+  constexpr int P = 16 / sizeof(K), CH = 16 / P;
+  typedef K KP __attribute__((ext_vector_type(P)));
+  int r = 0;
 #pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
+  for (int c0 = 0; c0 < 64; c0 += 16) {
+    if (c0 >= n) break;  // wave-uniform
+    KP v[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) v[i] = *reinterpret_cast<const KP*>(buf + c0 + i * P);
+#pragma unroll
+    for (int i = 0; i < CH; ++i)
+#pragma unroll
+      for (int p = 0; p < P; ++p) r += v[i][p] > mine ? 1 : 0;
   }
-  return x;
+  return r;
 }
 
+// A 16-byte vector of a row: a plain global load away from the row end; near it, only the
+// logits before V (the rest read as -inf) and nothing past the last vector.
 template <int DT>
 __device__ inline typename Vec<DT>::Raw load_vec(const char* rowp, int64_t vi, int64_t nvec,
                                                  int64_t V, bool tail) {
@@ -207,323 +289,443 @@ __device__ inline typename Vec<DT>::Raw load_vec(const char* rowp, int64_t vi, i
   return Vt::load_raw(rowp, vi, V);
 }
 
-__device__ inline float raw_logit(const void* lds_row, int dtype_bf16, int j) {
-  if (dtype_bf16) return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(lds_row)[j] << 16);
-  return reinterpret_cast<const float*>(lds_row)[j];
-}
-
 // ---- launch 1: per-slice statistics and candidates -------------------------------------------
 
-template <int DT, int D>
-__global__ __launch_bounds__(kThreads) void hs_topl_slice_kernel(TopArgs A) {
+// One work unit, decoded: slice s of row `row` (0 = target, 1 + i = drafter i) of group grp
+// = b * K + k. Every field is uniform over the wave.
+struct Unit {
+  int s, row, grp, b, k;
+  bool tail;
+  int64_t v0;        // first 16-byte vector of the slice
+  const char* rowp;  // the row's first logit
+};
+
+template <int DT>
+__device__ inline Unit decode_unit(const TopArgs& A, uint32_t u) {
+  Unit q;
+  const uint32_t rs = fdiv(u, A.divS);
+  q.s = (int)(u - rs * (uint32_t)A.S);
+  const uint32_t grp = fdiv(rs, A.divR);
+  q.row = (int)(rs - grp * (uint32_t)(A.N + 1));
+  q.grp = (int)grp;
+  q.b = (int)fdiv(grp, A.divK);
+  q.k = q.grp - q.b * A.K;
+  q.tail = q.s == A.S - 1;
+  q.v0 = (int64_t)q.s * kThreads;
+  q.rowp = reinterpret_cast<const char*>(A.rows.ptr[q.row]) +
+           ((int64_t)q.b * A.rows.sb[q.row] + (int64_t)q.k * A.rows.sk[q.row]) * Vec<DT>::kBytes;
+  return q;
+}
+
+template <int DT>
+__device__ inline void load_unit(const TopArgs& A, const Unit& q, int lane,
+                                 typename Vec<DT>::Raw (&x)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = load_vec<DT>(q.rowp, q.v0 + i * 64 + lane, A.nvec, A.V, q.tail);
+}
+
+// The target's slice statistics: max, lowest argmax (when the greedy hit is wanted), exp2
+// offset fl(max c) and the sum of exp2(z c - offset).
+template <int DT>
+__device__ inline void target_unit(const TopArgs& A, const Unit& q, const typename Vec<DT>::Raw (&x)[4],
+                                   int lane) {
   using Vt = Vec<DT>;
+  constexpr int VE = Vt::kElems;
+  float z[4 * VE];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) Vt::unpack(x[i], z + i * VE);
+  float m = -INFINITY;
+  int idx = INT_MAX;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t e0 = (q.v0 + i * 64 + lane) * VE;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const float v = z[i * VE + e];
+      if (A.want_arg) {
+        if (e0 + e < A.V && (idx == INT_MAX || v > m)) {  // lowest index of the max
+          m = v;
+          idx = (int)(e0 + e);
+        }
+      } else if (e0 + e < A.V) {
+        m = fmaxf(m, v);
+      }
+    }
+  }
+  float o = -INFINITY, sum = 0.0f;
+  if (A.want_sum && m != -INFINITY) {
+    o = m * A.c;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t e0 = (q.v0 + i * 64 + lane) * VE;
+#pragma unroll
+      for (int e = 0; e < VE; ++e)
+        if (e0 + e < A.V) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[i * VE + e], A.c, -o));
+    }
+    sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+  if (A.want_arg) wave_max<true>(m, idx);
+  else wave_max<false>(m, idx);
+  if (A.want_sum) wave_lse(o, sum);
+  if (lane == 0) A.tstat[(int64_t)q.grp * A.S + q.s] = make_float4(m, o, sum, __int_as_float(idx));
+}
+
+// A drafter row slice's local Top_L, as global keys in rank order (kNone64 past the slice's
+// tokens). cand and lm are this wave's LDS.
+template <int DT>
+__device__ inline void drafter_unit(const TopArgs& A, const Unit& q, typename Vec<DT>::Raw (&x)[4],
+                                    int lane, typename KeyOf<DT>::K* cand,
+                                    typename KeyOf<DT>::K* lm) {
   using KO = KeyOf<DT>;
   using Key = typename KO::K;
   using UKey = typename KO::U;
   constexpr int VE = KO::VE, E = KO::E;
-  constexpr int kCap = kMaxTopL * E;  // candidates of one row slice (see below)
-  constexpr int kRowsPerWave = (D + kWaves - 1) / kWaves;
-  __shared__ __attribute__((aligned(16))) char s_target[kThreads * 16];
-  __shared__ Key s_cand[kWaves][kCap];
-
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-  const int64_t item = blockIdx.x;
-  const int s = (int)(item % A.S);
-  const int64_t gs = item / A.S;
-  const int set = (int)(gs % A.nsub);
-  const int grp = (int)(gs / A.nsub);
-  const int b = grp / A.K, k = grp % A.K;
-  const int n = min(D, A.N - set * D);
-  const bool tail = s == A.S - 1;
-  const int64_t v0 = (int64_t)s * kThreads;  // first vector of the slice
-
-  // loads: the target's vector first (it is waited for first), then this wave's rows
-  const char* trow = reinterpret_cast<const char*>(A.rows.ptr[0]) +
-                     ((int64_t)b * A.rows.sb[0] + (int64_t)k * A.rows.sk[0]) * Vt::kBytes;
-  const typename Vt::Raw tv = load_vec<DT>(trow, v0 + t, A.nvec, A.V, tail);
-  typename Vt::Raw dv[kRowsPerWave][4];
+  constexpr int kCap = kMaxTopL * E;  // candidates of one row slice held in LDS
+  // the lane's keys (tokens at or past V get kNone)
+  auto row_keys = [&](Key (&key)[E]) {
 #pragma unroll
-  for (int h = 0; h < kRowsPerWave; ++h) {
-    const int r = wv + kWaves * h;
-    if (r < n) {
-      const int row = 1 + set * D + r;
-      const char* p = reinterpret_cast<const char*>(A.rows.ptr[row]) +
-                      ((int64_t)b * A.rows.sb[row] + (int64_t)k * A.rows.sk[row]) * Vt::kBytes;
+    for (int i = 0; i < 4; ++i) KO::build(x[i], i, key);
+    if (q.tail) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dv[h][q] = load_vec<DT>(p, v0 + q * 64 + lane, A.nvec, A.V, tail);
-    }
-  }
-
-  // target slice: to LDS for the gathers, and its statistics (first row set only)
-  *reinterpret_cast<typename Vt::Raw*>(s_target + t * 16) = tv;
-  if (set == 0) {
-    float z[VE];
-    Vt::unpack(tv, z);
-    float m = -INFINITY;
-    int idx = INT_MAX;
-    const int64_t e0 = (v0 + t) * VE;
-#pragma unroll
-    for (int e = 0; e < VE; ++e)
-      if (e0 + e < A.V && (idx == INT_MAX || z[e] > m)) {  // lowest index of the max
-        m = z[e];
-        idx = (int)(e0 + e);
-      }
-    float o = -INFINITY, sum = 0.0f;
-    if (A.want_sum && m != -INFINITY) {
-      o = m * A.c;
-#pragma unroll
-      for (int e = 0; e < VE; ++e)
-        if (e0 + e < A.V) sum += __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -o));
-    }
-    const SliceStat st = A.want_sum ? block_reduce_stat<true, true>(m, idx, o, sum)
-                                    : block_reduce_stat<false, true>(m, idx, o, sum);
-    if (t == 0)
-      A.tstat[(int64_t)grp * A.S + s] = make_float4(st.m, st.o, st.s, __int_as_float(st.idx));
-  }
-  __syncthreads();
-
-  const Key lane_share = (Key)(lane * VE);
-  Key* cand = s_cand[wv];
-#pragma unroll
-  for (int h = 0; h < kRowsPerWave; ++h) {
-    const int r = wv + kWaves * h;
-    if (r >= n) break;  // wave-uniform
-    Key key[E];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) KO::build(dv[h][q], q, key);
-    if (tail) {  // tokens at or past V are no candidates
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int e = 0; e < VE; ++e)
-          if ((v0 + q * 64 + lane) * VE + e >= A.V) key[q * VE + e] = KO::kNone;
+          if ((q.v0 + i * 64 + lane) * VE + e >= A.V) key[i * VE + e] = KO::kNone;
     }
+  };
+  const Key lane_share = (Key)(lane * VE);
+  Key thr;
+  int C = 0;
+  {
+    Key key[E];
+    row_keys(key);
     Key mk = key[0];
 #pragma unroll
     for (int e = 1; e < E; ++e) mk = max(mk, key[e]);
     mk -= lane_share;
 
-    // theta: the L-th largest lane maximum. Exactly L lanes hold a key >= theta (fewer when
-    // theta is clamped to the valid range), so at most L * E keys of the slice reach it, and
-    // the slice's Top_L is among them.
-    const UKey um[1] = {(UKey)mk ^ KO::kFlip};  // > 0: mk >= kNone - lane share
-    Key theta = (Key)(wave_kth<UKey, 1>(um, 1, A.L) ^ KO::kFlip);
+    // theta: the L-th largest of the 32 maxima of lane pairs, by rank counting (they are
+    // distinct: exactly one pair has L - 1 larger ones; L <= 32). Every key >= theta lies in
+    // one of those L pairs, so at most 2 L E keys of the slice reach it (usually about L),
+    // and the slice's Top_L is among them.
+    const Key pm = max(mk, lane_swap(mk));
+    if ((lane & 1) == 0) lm[lane >> 1] = pm;
+    wave_lds_sync();
+    const uint64_t sel = __ballot((lane & 1) == 0 && rank_in(lm, 32, pm) == A.L - 1);
+    Key theta = sel ? bcast(pm, __builtin_ctzll(sel)) : KO::kValidMin;
     if (theta < KO::kValidMin) theta = KO::kValidMin;
-    // per-lane threshold on the lane-independent key part (saturating)
-    const Key thr = theta > (Key)(~(UKey)0 >> 1) - lane_share ? (Key)(~(UKey)0 >> 1) : theta + lane_share;
-    int cnt = 0;
-#pragma unroll
-    for (int e = 0; e < E; ++e) cnt += key[e] >= thr ? 1 : 0;
-    const int incl = wave_incl_scan(cnt);
-    const int C = __builtin_amdgcn_readlane(incl, 63);
-    int pos = incl - cnt;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-      if (key[e] >= thr) {
-        if (pos < kCap) cand[pos] = key[e] - lane_share;
-        ++pos;
-      }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // exact Top_L among the C <= kCap candidates (C >= L unless the slice holds fewer tokens)
-    const int Cc = min(C, kCap);
-    constexpr int NU = kCap / 64;
-    const int nu = (Cc + 63) / 64;
-    UKey u[NU];  // candidate keys, 0 past the end (real keys are >= kValidMin, so never 0)
+    // the candidates, compacted to LDS one element position at a time
+    const Key kMaxKey = (Key)(~(UKey)0 >> 1);
+    thr = theta > kMaxKey - lane_share ? kMaxKey : theta + lane_share;  // saturating
 #pragma unroll
-    for (int j = 0; j < NU; ++j) {
-      const int x = j * 64 + lane;
-      u[j] = j < nu && x < Cc ? (UKey)cand[x] ^ KO::kFlip : 0;
+    for (int e = 0; e < E; ++e) {
+      const bool c = key[e] >= thr;
+      const uint64_t m = __ballot(c);
+      if (m != 0) {  // wave-uniform
+        const int pos = C + mbcnt(m);
+        if (c && pos < kCap) cand[pos] = key[e] - lane_share;
+        C += __builtin_popcountll(m);
+      }
     }
-    const UKey kth = wave_kth<UKey, NU>(u, nu, A.L);
-    const int64_t orow = (((int64_t)b * A.N + set * D + r) * A.K + k) * A.S + s;
-    int64_t* okey = A.ckey + orow * A.L;
-    float* ozt = A.czt + orow * A.L;
+    if (C <= kCap && lane < 16) cand[C + lane] = KO::kMin;  // padding for the rank counts
+    wave_lds_sync();
+  }
+
+  // exact Top_L among the C candidates (C >= L unless the slice holds fewer tokens)
+  const int64_t orow = (((int64_t)q.b * A.N + (q.row - 1)) * A.K + q.k) * A.S + q.s;
+  int64_t* okey = A.ckey + orow * A.L;
+  const int64_t g0 = (int64_t)q.s * kThreads * VE;  // first token of the slice
+  if (C <= 64) {  // ranks by counting, written in rank order
+    const bool have = lane < C;
+    const Key mine = have ? cand[lane] : (Key)0;
+    const int rk = rank_in(cand, C, mine);
+    if (have && rk < A.L) okey[rk] = KO::global_key(mine, g0 + KO::slice_index(mine));
+  } else {
+    // many candidates (long runs of equal logits): a bitwise search, output in scan order
+    constexpr int NU = kCap / 64;
+    constexpr int NR = NU > E ? NU : E;
+    const bool in_lds = C <= kCap;
+    // the candidates' unsigned images (0: none): u[j] = entry j * 64 + lane of the LDS list,
+    // or, when the list overflowed, u[e] = the lane's element e (the row slice is read again:
+    // a rare path, its loads are not overlapped)
+    UKey u[NR];
+    int nu;
+    if (in_lds) {
+      nu = (C + 63) / 64;
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+        const int xx = j * 64 + lane;
+        u[j] = j < nu && xx < C ? (UKey)cand[xx] ^ KO::kFlip : 0;
+      }
+    } else {
+      nu = E;
+      load_unit<DT>(A, q, lane, x);
+      Key key[E];
+      row_keys(key);
+#pragma unroll
+      for (int j = 0; j < NR; ++j)
+        u[j] = j < E && key[j < E ? j : 0] >= thr ? (UKey)(key[j < E ? j : 0] - lane_share) ^ KO::kFlip : 0;
+    }
+    const UKey kth = wave_kth<UKey, NR>(u, nu, A.L);
     int base = 0;
 #pragma unroll
-    for (int j = 0; j < NU; ++j) {
+    for (int j = 0; j < NR; ++j) {
       if (j >= nu) break;  // wave-uniform
       const bool win = u[j] != 0 && u[j] >= kth;
       const uint64_t wm = __ballot(win);
-      const int slot = base + __builtin_popcountll(wm & ((1ull << lane) - 1));
+      const int slot = base + mbcnt(wm);
       if (win && slot < A.L) {
         const Key kk = (Key)(u[j] ^ KO::kFlip);
-        const int jj = KO::slice_index(kk) & (kThreads * VE - 1);  // < kThreads * VE by construction
-        okey[slot] = KO::global_key(kk, (int64_t)s * kThreads * VE + jj);
-        ozt[slot] = raw_logit(s_target, DT == HS_BF16, jj);
+        okey[slot] = KO::global_key(kk, g0 + KO::slice_index(kk));
       }
       base += __builtin_popcountll(wm);
     }
-    for (int slot = base + lane; slot < A.L; slot += 64) {
-      okey[slot] = kNone64;
-      ozt[slot] = 0.0f;
-    }
-    __builtin_amdgcn_wave_barrier();  // the candidate buffer is reused by the next row
   }
+  for (int slot = C + lane; slot < A.L; slot += 64) okey[slot] = kNone64;  // fewer than L tokens
+  wave_lds_sync();  // the LDS lists are rewritten by the next unit
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void hs_topl_slice_kernel(TopArgs A) {
+  using Vt = Vec<DT>;
+  using KO = KeyOf<DT>;
+  using Key = typename KO::K;
+  constexpr int kCap = kMaxTopL * KO::E;
+  __shared__ __attribute__((aligned(16))) Key s_cand[kWaves][kCap + 16];  // + room for the padding
+  __shared__ __attribute__((aligned(16))) Key s_lmax[kWaves][32];
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform over the wave
+  const uint32_t u = blockIdx.x * kWaves + wv;
+  if (u >= A.units) return;  // wave-uniform; the waves share no barrier
+  HS_TSTAMP(0, 0);
+  typename Vt::Raw x[4];
+  const Unit q = decode_unit<DT>(A, u);
+  load_unit<DT>(A, q, lane, x);
+  if (q.row == 0) target_unit<DT>(A, q, x, lane);
+  else drafter_unit<DT>(A, q, x, lane, s_cand[wv], s_lmax[wv]);
+  HS_TSTAMP(0, 1);
 }
 
 // ---- launch 2: global Top_L and the mass ----------------------------------------------------
+// One wave per (query, drafter, position).
 
-__device__ inline bool ge_u64(uint64_t a, uint64_t b) { return a >= b; }
-
+template <int DT>
 __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
-  __shared__ int64_t s_key[kWaves][kMergeCap];
-  __shared__ int32_t s_ent[kWaves][kMergeCap];
-  __shared__ int64_t s_wkey[kWaves][kMaxTopL];
-  __shared__ int32_t s_went[kWaves][kMaxTopL];
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  constexpr int R = 16;   // candidates per lane held in registers
+  constexpr int RS = 8;   // slice statistics records per lane loaded up front
+  __shared__ __attribute__((aligned(16))) int64_t s_key[kWaves][kMergeCap + 16];  // + padding
+  __shared__ __attribute__((aligned(16))) int64_t s_lmax[kWaves][64];
+  __shared__ __attribute__((aligned(16))) int64_t s_wkey[kWaves][64];
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform over the wave
   const int64_t rows = (int64_t)A.B * A.N * A.K;
   const int64_t r = (int64_t)blockIdx.x * kWaves + wv;
   if (r >= rows) return;  // wave-uniform; no workgroup barrier below
-  const int k = (int)(r % A.K);
-  const int b = (int)(r / ((int64_t)A.N * A.K));
+  const uint32_t r32 = (uint32_t)r;  // rows < 2^31
+  const int k = (int)(r32 - fdiv(r32, A.divK) * (uint32_t)A.K);
+  const int b = (int)fdiv(r32, A.divNK);
   const int grp = b * A.K + k;
   const int L = A.L;
   const int nc = A.S * L;
   const int64_t* ck = A.ckey + r * nc;
-  const float* cz = A.czt + r * nc;
-  constexpr uint64_t kFlip = 0x8000000000000000ull;
+  HS_TSTAMP(A.units, 0);
 
-  // pass 1: lane maxima, theta = the L-th largest of them (clamped to real keys)
-  int64_t mk = kNone64;
-  for (int x = lane; x < nc; x += 64) mk = max(mk, ck[x]);
-  const uint64_t um[1] = {(uint64_t)mk ^ kFlip};  // 0 for a lane without candidates
-  int64_t theta = (int64_t)(wave_kth<uint64_t, 1>(um, 1, L) ^ kFlip);
-  if (theta < kNone64 + 1) theta = kNone64 + 1;
-
-  // pass 2: the candidates >= theta (at most L lanes hold any), compacted in LDS
-  int cnt = 0;
-  for (int x = lane; x < nc; x += 64) cnt += ck[x] >= theta ? 1 : 0;
-  const int incl = wave_incl_scan(cnt);
-  const int C = __builtin_amdgcn_readlane(incl, 63);
-  int64_t kth;
-  int64_t* key = s_key[wv];
-  int32_t* ent = s_ent[wv];
-  if (C <= kMergeCap) {
-    int pos = incl - cnt;
-    for (int x = lane; x < nc; x += 64) {
-      const int64_t v = ck[x];
-      if (v >= theta) {
-        key[pos] = v;
-        ent[pos] = x;
-        ++pos;
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    constexpr int NU = kMergeCap / 64;
-    const int nu = (C + 63) / 64;
-    uint64_t u[NU];
+  // loads up front: the target's statistics records, then the candidates (unconditional
+  // loads at a clamped index, then a select: no branch between the loads)
+  const int nst = A.S;
+  const float4* ts = A.tstat + (int64_t)grp * nst;
+  const float4 none_st = make_float4(-INFINITY, -INFINITY, 0.0f, __int_as_float(INT_MAX));
+  float4 st[RS];
 #pragma unroll
-    for (int j = 0; j < NU; ++j) {
-      const int x = j * 64 + lane;
-      u[j] = j < nu && x < C ? (uint64_t)key[x] ^ kFlip : 0;
+  for (int j = 0; j < RS; ++j) st[j] = ts[min(j * 64 + lane, nst - 1)];
+#pragma unroll
+  for (int j = 0; j < RS; ++j)
+    if (j * 64 + lane >= nst) st[j] = none_st;
+  const bool resident = nc <= 64 * R;
+  int64_t kr[R];
+  int64_t mk = kNone64;
+  for (int x0 = 0; x0 < nc; x0 += 64 * R) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) kr[j] = ck[min(x0 + j * 64 + lane, nc - 1)];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      if (x0 + j * 64 + lane >= nc) kr[j] = kNone64;
+      mk = max(mk, kr[j]);
     }
-    kth = (int64_t)(wave_kth<uint64_t, NU>(u, nu, L) ^ kFlip);
-  } else {
-    // more candidates than the LDS holds: search the lists in place (same result, slower)
-    uint64_t ref = (uint64_t)theta ^ kFlip;
-    uint64_t diff = 0;
-    for (int x = lane; x < nc; x += 64)
-      if (ck[x] >= theta) diff |= ((uint64_t)ck[x] ^ kFlip) ^ ref;
-    uint64_t vary = first_lane(wave_or(diff));
-    uint64_t cur = ref & ~vary;
-    while (vary) {
-      const int bit = highest_bit(vary);
-      const uint64_t bb = 1ull << bit;
-      vary &= ~bb;
-      const uint64_t cand = cur | bb;
-      int c = 0;
-      for (int x0 = 0; x0 < nc; x0 += 64) {
-        const int x = x0 + lane;
-        c += __builtin_popcountll(__ballot(x < nc && ck[x] >= theta && ((uint64_t)ck[x] ^ kFlip) >= cand));
-      }
-      if (c >= L) cur = cand;
-    }
-    kth = (int64_t)(cur ^ kFlip);
   }
-  __builtin_amdgcn_wave_barrier();
 
-  // the winners (exactly L: V >= L real tokens), moved to lanes 0 .. L-1
-  int64_t* wk = s_wkey[wv];
-  int32_t* we = s_went[wv];
-  int base = 0;
-  const bool in_lds = C <= kMergeCap;
-  const int nscan = in_lds ? C : nc;
-  for (int x0 = 0; x0 < nscan; x0 += 64) {
-    const int x = x0 + lane;
-    int64_t kv = kNone64;
-    int ev = 0;
-    if (x < nscan) {
-      kv = in_lds ? key[x] : ck[x];
-      ev = in_lds ? ent[x] : x;
-    }
-    const bool win = x < nscan && kv >= kth;
-    const uint64_t wm = __ballot(win);
-    const int slot = base + __builtin_popcountll(wm & ((1ull << lane) - 1));
-    if (win && slot < kMaxTopL) {
-      wk[slot] = kv;
-      we[slot] = ev;
-    }
-    base += __builtin_popcountll(wm);
-  }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const int W = min(base, L);
-  const bool mine = lane < W;
-  const int64_t wkey = mine ? wk[lane] : kNone64;
-  const float zt = mine ? cz[we[lane]] : 0.0f;
-  const int gidx = (int)(0xFFFFFFFFu - (uint32_t)(uint64_t)wkey);
-
-  // the target's softmax statistics from its slices
-  const float4* ts = A.tstat + (int64_t)grp * A.S;
+  // the target's softmax statistics
   float m = -INFINITY, o = -INFINITY, sm = 0.0f;
   int am = INT_MAX;
-  for (int x = lane; x < A.S; x += 64) {
-    const float4 st = ts[x];
-    argmax_combine(m, am, st.x, __float_as_int(st.w));
-    if (A.want_sum) lse2_combine(o, sm, st.y, st.z);
+#pragma unroll
+  for (int j = 0; j < RS; ++j) {
+    argmax_combine(m, am, st[j].x, __float_as_int(st[j].w));
+    if (A.want_sum) lse2_combine(o, sm, st[j].y, st[j].z);
+  }
+  for (int x = RS * 64 + lane; x < nst; x += 64) {
+    const float4 q = ts[x];
+    argmax_combine(m, am, q.x, __float_as_int(q.w));
+    if (A.want_sum) lse2_combine(o, sm, q.y, q.z);
   }
   wave_max<true>(m, am);
+  if (A.gamma) wave_lse(o, sm);
+  HS_TSTAMP(A.units, 1);
+
+  // theta: the L-th largest lane maximum, by rank counting. The lanes holding a real
+  // candidate are distinct and at least L (slice 0 lists L real tokens in L consecutive
+  // entries); lanes without one hold kNone64 and rank below all of them.
+  int64_t* lm = s_lmax[wv];
+  lm[lane] = mk;
+  wave_lds_sync();
+  const uint64_t sel = __ballot(mk != kNone64 && rank_in(lm, 64, mk) == L - 1);
+  const int64_t theta = sel ? bcast(mk, __builtin_ctzll(sel)) : kNone64 + 1;
+  HS_TSTAMP(A.units, 2);
+
+  // the candidates >= theta (at most L lanes hold any), compacted to LDS
+  int64_t* key = s_key[wv];
+  int C = 0;
+  for (int x0 = 0; x0 < nc; x0 += 64 * R) {
+    if (!resident) {
+#pragma unroll
+      for (int j = 0; j < R; ++j) kr[j] = ck[min(x0 + j * 64 + lane, nc - 1)];
+#pragma unroll
+      for (int j = 0; j < R; ++j)
+        if (x0 + j * 64 + lane >= nc) kr[j] = kNone64;
+    }
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const bool c = kr[j] >= theta;
+      const uint64_t mm = __ballot(c);
+      if (mm != 0) {  // wave-uniform
+        const int pos = C + mbcnt(mm);
+        if (c && pos < kMergeCap) key[pos] = kr[j];
+        C += __builtin_popcountll(mm);
+      }
+    }
+  }
+  if (C <= kMergeCap && lane < 16) key[C + lane] = kNone64;  // padding for the rank counts
+  wave_lds_sync();
+  HS_TSTAMP(A.units, 3);
+
+  // exact Top_L: per lane a winner flag, its key and its rank
+  bool win;
+  int64_t wkey;
+  int rank;
+  if (C <= 64) {
+    const bool have = lane < C;
+    wkey = have ? key[lane] : kNone64;
+    rank = rank_in(key, C, wkey);
+    win = have && rank < L;
+  } else {
+    int64_t kth;
+    if (C <= kMergeCap) {
+      constexpr int NU = kMergeCap / 64;
+      const int nu = (C + 63) / 64;
+      uint64_t u[NU];
+#pragma unroll
+      for (int j = 0; j < NU; ++j) {
+        const int x = j * 64 + lane;
+        u[j] = j < nu && x < C ? (uint64_t)key[x] ^ kFlip64 : 0;
+      }
+      kth = (int64_t)(wave_kth<uint64_t, NU>(u, nu, L) ^ kFlip64);
+    } else {
+      // more candidates than the LDS holds: search the lists in place (same result, slower)
+      const uint64_t ref = (uint64_t)theta ^ kFlip64;
+      uint64_t diff = 0;
+      for (int x = lane; x < nc; x += 64)
+        if (ck[x] >= theta) diff |= ((uint64_t)ck[x] ^ kFlip64) ^ ref;
+      uint64_t vary = first_lane(wave_or(diff));
+      uint64_t cur = ref & ~vary;
+      while (vary) {
+        const uint64_t bb = 1ull << highest_bit(vary);
+        vary &= ~bb;
+        const uint64_t cnd = cur | bb;
+        int c = 0;
+        for (int x0 = 0; x0 < nc; x0 += 64) {
+          const int x = x0 + lane;
+          c += __builtin_popcountll(
+              __ballot(x < nc && ck[x] >= theta && ((uint64_t)ck[x] ^ kFlip64) >= cnd));
+        }
+        if (c >= L) cur = cnd;
+      }
+      kth = (int64_t)(cur ^ kFlip64);
+    }
+    // the L winners to LDS in scan order, then ranked among themselves
+    int64_t* wk = s_wkey[wv];
+    const bool in_lds = C <= kMergeCap;
+    const int nscan = in_lds ? C : nc;
+    int base = 0;
+    for (int x0 = 0; x0 < nscan; x0 += 64) {
+      const int x = x0 + lane;
+      int64_t kv = kNone64;
+      if (x < nscan) kv = in_lds ? key[x] : ck[x];
+      const bool w = x < nscan && kv >= kth;
+      const uint64_t wm = __ballot(w);
+      const int slot = base + mbcnt(wm);
+      if (w && slot < kMaxTopL) wk[slot] = kv;
+      base += __builtin_popcountll(wm);
+    }
+    if (lane < 16) wk[min(base, kMaxTopL) + lane] = kNone64;  // padding for the rank counts
+    wave_lds_sync();
+    const int W = min(base, L);
+    win = lane < W;
+    wkey = win ? wk[lane] : kNone64;
+    rank = rank_in(wk, W, wkey);
+  }
+  HS_TSTAMP(A.units, 4);
+
+  // the target logits of the winners, gathered from the target row
+  const int gidx = (int)(0xFFFFFFFFu - (uint32_t)(uint64_t)wkey);
+  float zt = 0.0f;
+  if (win) {
+    const char* trow = reinterpret_cast<const char*>(A.rows.ptr[0]) +
+                       ((int64_t)b * A.rows.sb[0] + (int64_t)k * A.rows.sk[0]) * Vec<DT>::kBytes;
+    if (DT == HS_BF16)
+      zt = __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(trow)[gidx] << 16);
+    else
+      zt = reinterpret_cast<const float*>(trow)[gidx];
+  }
   if (A.gamma) {
-    wave_lse(o, sm);
-    const float e = mine ? __builtin_amdgcn_exp2f(fmaf(zt, A.c, -o)) : 0.0f;
+    const float e = win ? __builtin_amdgcn_exp2f(fmaf(zt, A.c, -o)) : 0.0f;
     const float tot = wave_sum_f(e);
     if (lane == 0) A.gamma[r] = fminf(tot / sm, 1.0f);
   }
   if (A.hit) {
-    const bool h = __ballot(mine && gidx == am) != 0;
+    const bool h = __ballot(win && gidx == am) != 0;
     if (lane == 0) A.hit[r] = h ? 1 : 0;
   }
-  if (A.idx) {
-    int rank = 0;
-    for (int q = 0; q < W; ++q) {
-      const int64_t kq = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(
-                                        (int)(uint32_t)((uint64_t)wkey >> 32), q) << 32) |
-                                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)wkey, q));
-      rank += kq > wkey ? 1 : 0;
-    }
-    if (mine) A.idx[r * L + rank] = gidx;
-  }
+  if (A.idx && win) A.idx[r * L + rank] = gidx;
+  HS_TSTAMP(A.units, 5);
 }
 
-template <int DT, int D>
-void launch_slice(const TopArgs& A, int64_t items, hipStream_t st) {
-  hs_topl_slice_kernel<DT, D><<<(unsigned)items, kThreads, 0, st>>>(A);
+// One wave per unit. (A resident grid looping over the units with the next unit's logits in
+// registers was measured slower: the extra registers halve the waves a SIMD holds.)
+template <int DT>
+void launch_t(const TopArgs& A, int64_t nrows, hipStream_t st) {
+  const int64_t wgs = ((int64_t)A.units + kWaves - 1) / kWaves;
+  hs_topl_slice_kernel<DT><<<(unsigned)wgs, kThreads, 0, st>>>(A);
+  if (hipGetLastError() != hipSuccess) return;
+  hs_topl_merge_kernel<DT><<<(unsigned)((nrows + kWaves - 1) / kWaves), kThreads, 0, st>>>(A);
 }
 
 }  // namespace
 
+#ifdef HS_TRACE
+extern "C" __attribute__((visibility("default"))) void hs_debug_set_topl_trace(void* p) {
+  g_topl_trace = reinterpret_cast<uint64_t*>(p);
+}
+#endif
+
 size_t topl_ws_bytes(const TeamGeom& g, int L) {
   const size_t rows = (size_t)g.B * g.N * g.K;
-  size_t off = align256(rows * g.S * L * 8);
-  off += align256(rows * g.S * L * 4);
-  off += align256((size_t)g.G * g.S * 16);
-  return off;
+  return align256(rows * g.S * L * 8) + align256((size_t)g.G * g.S * 16);
+}
+
+bool topl_fits(const TeamGeom& g) {
+  return (int64_t)g.G * (g.N + 1) * g.S < ((int64_t)1 << 31) &&
+         (int64_t)g.B * g.N * g.K < ((int64_t)1 << 31);
 }
 
 int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool want_sum,
@@ -533,43 +735,29 @@ int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool wa
   A.B = g.B;
   A.N = g.N;
   A.K = g.K;
-  A.D = g.D;
-  A.nsub = g.nsub;
   A.S = g.S;
   A.L = L;
   A.V = g.V;
   A.nvec = g.nvec;
+  A.units = (uint32_t)((int64_t)g.G * (g.N + 1) * g.S);
+  A.divS = make_fastdiv((uint32_t)g.S);
+  A.divR = make_fastdiv((uint32_t)(g.N + 1));
+  A.divK = make_fastdiv((uint32_t)g.K);
+  A.divNK = make_fastdiv((uint32_t)(g.N * g.K));
   A.c = c;
   A.want_sum = want_sum ? 1 : 0;
+  A.want_arg = hit != nullptr ? 1 : 0;
   const size_t nrows = (size_t)g.B * g.N * g.K;
-  size_t off = 0;
-  A.ckey = reinterpret_cast<int64_t*>(ws + off);
-  off += align256(nrows * g.S * L * 8);
-  A.czt = reinterpret_cast<float*>(ws + off);
-  off += align256(nrows * g.S * L * 4);
-  A.tstat = reinterpret_cast<float4*>(ws + off);
+  A.ckey = reinterpret_cast<int64_t*>(ws);
+  A.tstat = reinterpret_cast<float4*>(ws + align256(nrows * g.S * L * 8));
   A.gamma = gamma;
   A.hit = hit;
   A.idx = idx;
-  const int64_t items = g.items;
-  if (g.dtype == HS_BF16) {
-    switch (g.D) {
-      case 1: launch_slice<HS_BF16, 1>(A, items, stream); break;
-      case 2: launch_slice<HS_BF16, 2>(A, items, stream); break;
-      case 4: launch_slice<HS_BF16, 4>(A, items, stream); break;
-      default: launch_slice<HS_BF16, 8>(A, items, stream); break;
-    }
-  } else {
-    switch (g.D) {
-      case 1: launch_slice<HS_F32, 1>(A, items, stream); break;
-      case 2: launch_slice<HS_F32, 2>(A, items, stream); break;
-      case 4: launch_slice<HS_F32, 4>(A, items, stream); break;
-      default: launch_slice<HS_F32, 8>(A, items, stream); break;
-    }
-  }
-  if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
-  const int64_t wgs = ((int64_t)nrows + kWaves - 1) / kWaves;
-  hs_topl_merge_kernel<<<(unsigned)wgs, kThreads, 0, stream>>>(A);
+#ifdef HS_TRACE
+  A.trace = g_topl_trace;
+#endif
+  if (g.dtype == HS_BF16) launch_t<HS_BF16>(A, (int64_t)nrows, stream);
+  else launch_t<HS_F32>(A, (int64_t)nrows, stream);
   return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
 }
 

@@ -133,3 +133,25 @@ def test_topl_deterministic_and_workspace_reuse():
     b = hs.eval_topl(x, L=10, want_children=True)
     torch.cuda.synchronize()
     assert torch.equal(a["gamma"], b["gamma"]) and torch.equal(a["children"], b["children"])
+
+
+@pytest.mark.parametrize("L", [2, 3])
+def test_topl_candidate_list_overflow(L):
+    # In every slice the first lane pair holds the largest values and the second pair the next
+    # ones, so more keys reach the pair threshold than the slice's candidate list holds (L * 32
+    # for bf16, L * 16 for fp32) and the slice kernel searches its registers instead.
+    rng = np.random.default_rng(23)
+    V = 8192
+    z = rng.normal(0, 1, (3, 1, 2, V)).astype(np.float32)
+    for base in range(0, V, 2048):
+        for q in range(4):  # bf16 layout: lane l holds tokens q*512 + 8l .. 8l+7
+            z[1, :, :, base + q * 512: base + q * 512 + 16] = 100.0
+            z[1, :, :, base + q * 512 + 16: base + q * 512 + 32] = 50.0
+    for base in range(0, V, 1024):
+        for q in range(4):  # fp32 layout: lane l holds tokens q*256 + 4l .. 4l+3
+            z[2, :, :, base + q * 256: base + q * 256 + 8] = 100.0
+            z[2, :, :, base + q * 256 + 8: base + q * 256 + 16] = 50.0
+    for x in (_bf16(z), z):
+        note("candidate overflow L=%d dtype=%s" % (L, x.dtype))
+        got = check(x, L, T=1.0)
+        assert list(got["children"][0, 0, 0]) == list(range(L))
