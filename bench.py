@@ -66,6 +66,32 @@ def measured_traffic(workload: str):
     return rec["hbm_bytes_per_call"]
 
 
+TOPL_SOURCES = ["paper_2510_20064_amd/csrc/hs_topl.hip", "paper_2510_20064_amd/csrc/hs_wave.h",
+                "paper_2510_20064_amd/csrc/hs_internal.h"]
+
+
+def measured_topl_traffic(workload: str):
+    """HBM bytes per hs_eval_topl call (both launches) from the committed counter summary of this
+    workload, or None when there is none or the kernel sources changed since it was taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hs_eval_topl_%s.md" % workload)
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for ln in f:
+            if ln.startswith("traffic-record: "):
+                rec = json.loads(ln[len("traffic-record: "):])
+    h = hashlib.sha256()
+    for rel in TOPL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if not rec or rec.get("kernel_sources_sha256") != h.hexdigest():
+        return None
+    return rec["hbm_bytes_per_call"]
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -77,6 +103,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--topl", type=int, default=0, metavar="L",
+                    help="time hs_eval_topl (EAGLE's top-L acceptance mass, Theorem 2) with L "
+                         "children per node on the workload instead")
     ap.add_argument("--delayed", action="store_true",
                     help="time hs_delayed_update (token-level delayed feedback) on the workload's "
                          "B, N, K instead, K new tokens per query per round")
@@ -138,6 +167,105 @@ def bench_delayed(args, w, hs, torch, dev):
     print(json.dumps(line), flush=True)
 
 
+def bench_topl(args, w, hs, torch, dev, np, synth):
+    """hs_eval_topl on distinct rounds resident in HBM (>= 512 MB, rotated), in a HIP graph.
+    A call is two launches (per-slice candidates, then the merge); the roofline prices the whole
+    call against every logit read once."""
+    L = args.topl
+    copies = max(1, math.ceil(ROTATE_BYTES / w.input_bytes))
+    if w.input_bytes * copies > 64e9:
+        copies = max(1, int(64e9 // w.input_bytes))
+    bufs = []
+    for r in range(copies):
+        t = torch.from_numpy(synth.generate(w, round=r))
+        if w.dtype == synth.BF16:
+            t = t.view(torch.bfloat16)
+        bufs.append(t.to(dev))
+    ws = torch.empty(hs.topl_workspace_size(w.B, w.N, w.K, w.V, L, w.dtype), dtype=torch.uint8,
+                     device=dev)
+    greedy = w.mode == hs.GREEDY
+    out = {}
+    stream = torch.cuda.Stream()
+
+    def call(i):
+        hs.eval_topl(bufs[i % copies], L=L, V=w.V, temperature=w.temperature, mode=w.mode,
+                     workspace=ws, out=out, stream=torch.cuda.current_stream())
+
+    with torch.cuda.stream(stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // copies)
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup // copies)):
+            g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+    achieved = w.input_bytes / (us * 1e-6) / 1e9
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+
+        x = synth.generate(w, round=0)
+        t1 = time.perf_counter()
+        n_done = 0
+        G = w.B * w.K
+        xg = x.reshape(x.shape[0], G, x.shape[-1])
+        while True:  # one (query, position) group at a time: all N drafters of it
+            gi = n_done % G
+            oracle.topl(xg[:, gi:gi + 1], L, V=w.V, T=w.temperature, want_mass=not greedy)
+            n_done += 1
+            el = time.perf_counter() - t1
+            if el >= args.cpu_seconds:
+                break
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        threads = min(threads, os.cpu_count() or threads)
+        cpu = {"value": w.N * n_done / el, "unit": "drafter-positions/s", "cores": threads,
+               "kind": "oracle",
+               "sample": "%d (query, position) groups of the same workload, all %d drafters each, "
+                         "float64 C oracle (L passes per row) with OpenMP over rows, %.1f s"
+                         % (n_done, w.N, el)}
+    line = {"metric": "EAGLE top-L acceptance mass: " + METRIC,
+            "value": w.positions / (us * 1e-6), "unit": "drafter-positions/s", "n_gpus": 1,
+            "steps": reps * copies, "warmup": max(1, args.warmup // copies) * copies,
+            "ms_per_step": us * 1e-3, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "i32 keys, f32 mass", "data": "synthetic",
+            "config": {"workload": w.name, "B": w.B, "N": w.N, "K": w.K, "V": w.V, "L": L,
+                       "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
+                       "temperature": w.temperature, "mode": "greedy" if greedy else "sample",
+                       "rotation_copies": copies, "input_bytes_per_step": w.input_bytes,
+                       "hip_graph": True, "wall_s": round(wall, 4)},
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                         "traffic": measured_topl_traffic(w.name),
+                         "kernel": "hs_eval_topl = hs_topl_slice_kernel + hs_topl_merge_kernel "
+                                   "(one call, both launches timed)",
+                         "kernel_us": us, "algorithmic_bytes_per_launch": w.input_bytes},
+            "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -158,6 +286,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.delayed:
         bench_delayed(args, w, hs, torch, dev)
+        return
+    if args.topl:
+        bench_topl(args, w, hs, torch, dev, np, synth)
         return
 
     # ---- inputs: distinct rounds, resident in HBM -----------------------------------------
