@@ -156,8 +156,10 @@ size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dt
  *                output is filled as well.
  * workspace    : at least hs_eval_topl_workspace_size() bytes of device memory, 256-byte
  *                aligned; scratch only (no initialisation needed, contents undefined after).
- * Two launches: each logit is read from HBM once, by the first; the second merges the
- * per-slice candidates (about 12 L bytes per row slice). Deterministic for a given shape.
+ * Two launches: each logit is read from HBM once, by the first (per 2048-logit slice of each
+ * row: the target's softmax statistics, or a drafter's L best keys, 8 L bytes); the second
+ * merges each drafter row's candidates and reads the target logits of its L winners.
+ * Deterministic for a given shape.
  * Not covered: EAGLE-2's dynamic pruning, whose candidate set is the pruned subtree.
  */
 int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
