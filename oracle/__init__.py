@@ -49,6 +49,8 @@ def _load():
         lib.or_eval.restype = I
         lib.or_topl.argtypes = [P, I, I64, I, I64, I64, I, D, I, P, P, P]
         lib.or_topl.restype = I
+        lib.or_hybrid_losses.argtypes = [P, I, I, I, I64, P]
+        lib.or_hybrid_losses.restype = I
         lib.or_softmax_stats.argtypes = [P, I, I64, I64, I64, D, P, P, P]
         lib.or_softmax_stats.restype = I
         lib.or_path.argtypes = [P, I, I, P]
@@ -240,20 +242,31 @@ def window_losses(gamma: np.ndarray, K: int) -> np.ndarray:
     return out
 
 
+def hybrid_losses(gamma: np.ndarray, K: int, H: int) -> np.ndarray:
+    """Hybrid token losses [n][N] known after the T tokens of gamma [T][N]: acceptance loss for
+    the first H tokens, the window-K length loss after them."""
+    g = np.ascontiguousarray(gamma, dtype=np.float64)
+    T, N = g.shape
+    out = np.zeros((T, N))
+    n = _load().or_hybrid_losses(_p(g), T, N, K, int(H), _p(out))
+    return out[:n]
+
+
 class QfiD:
     """Queued Full-Information with Delays (Appendix, algorithm QFI-D) with Hedge and
-    NormalHedge as base learners, one learner pair per query, fed the token-level length loss.
+    NormalHedge as base learners, one learner pair per query, fed the token-level length loss
+    (or, with hybrid = H > 0, the acceptance loss for each query's first H tokens).
 
     push(gamma, count): query b's token stream grows by gamma[b, :, :count[b]] (the feedback of
-    its next count[b] tokens, [N] each). Every window of K tokens that is complete and not yet
-    used gives one loss vector; they enter the FIFO in token order and the base learners take
-    them all, in that order, before the next prediction. Returns the loss vectors used per
-    query (a list of [L_b][N] arrays)."""
+    its next count[b] tokens, [N] each). Every token whose loss is known and not yet used gives
+    one loss vector; they enter the FIFO in token order and the base learners take them all, in
+    that order, before the next prediction. Returns the loss vectors used per query (a list of
+    [L_b][N] arrays)."""
 
-    def __init__(self, B: int, N: int, K: int, eta: float):
-        self.B, self.N, self.K, self.eta = B, N, K, eta
+    def __init__(self, B: int, N: int, K: int, eta: float, hybrid: int = 0):
+        self.B, self.N, self.K, self.eta, self.hybrid = B, N, K, eta, hybrid
         self.stream = [np.zeros((0, N)) for _ in range(B)]
-        self.done = [0] * B  # windows already used
+        self.done = [0] * B  # loss vectors already used
         self.w = np.full((B, N), 1.0 / N)
         self.R = np.zeros((B, N))
         self.p = np.full((B, N), 1.0 / N)
@@ -264,7 +277,7 @@ class QfiD:
         for b in range(self.B):
             m = int(count[b])
             self.stream[b] = np.concatenate([self.stream[b], np.asarray(gamma[b, :, :m]).T])
-            ls = window_losses(self.stream[b], self.K)[self.done[b]:]
+            ls = hybrid_losses(self.stream[b], self.K, self.hybrid)[self.done[b]:]
             self.done[b] += ls.shape[0]
             if ls.shape[0]:
                 lb = ls[:, None, :]  # [L][1][N]
@@ -273,4 +286,3 @@ class QfiD:
                 self.R[b:b + 1], self.p[b:b + 1], self.c[b] = R, p, c[0]
             used.append(ls)
         return used
-

@@ -23,6 +23,8 @@
  *                             enumeration of the dominating L-subset, ties and signed
  *                             zeros by index, invariance under exact rescaling of the
  *                             drafter, L = 1 greedy hit equals argmax agreement).
+ *   or_hybrid_losses        : pinned (H = 0 is the window loss, H >= T the acceptance loss,
+ *                             the appendix's K = 8 example with a first chunk of 4 tokens).
  *   or_window_losses        : pinned (all-accept and all-reject windows, K = 1, constant
  *                             gamma geometric sum, the censoring appendix's worked example).
  *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
@@ -278,15 +280,43 @@ int or_window_losses(const double* gamma, int T, int N, int K, double* loss) {
 }
 
 /*
+ * Hybrid losses (Appendix "Practical heuristics: hybrid losses, skipping update"): the first H
+ * tokens of a stream take the acceptance-probability loss 1 - gamma_s, known as soon as token
+ * s's feedback is in; later tokens take the token-level length loss of or_window_losses, known
+ * once the K tokens of their window are in. gamma: [T][N]; loss: [T][N]. Writes, in token
+ * order, the losses of every token whose loss is known after T tokens and returns their number
+ * (they form a prefix of the stream: min(T, H) + max(0, T - K + 1 - H) when T > H).
+ */
+int or_hybrid_losses(const double* gamma, int T, int N, int K, int64_t H, double* loss) {
+  int n = 0;
+  for (int s = 0; s < T; ++s) {
+    if (s < H) {
+      for (int i = 0; i < N; ++i) loss[(size_t)n * N + i] = 1.0 - gamma[(size_t)s * N + i];
+    } else {
+      if (s + K > T) break;
+      double g[4096];
+      for (int i = 0; i < N; ++i) {
+        for (int j = 0; j < K; ++j) g[j] = gamma[(size_t)(s + j) * N + i];
+        loss[(size_t)n * N + i] = 1.0 - or_eal_path(g, K) / (double)(K + 1);
+      }
+    }
+    ++n;
+  }
+  return n;
+}
+
+/*
  * Expected acceptance length and losses for B queries and N drafters.
  * gamma   : [B][N][M] feedback per node (chain: M = K positions).
  * parent  : [M] or NULL for a chain (parent[k] = k - 1).
- * path_end: [B] or NULL (node M - 1).
+ * path_end: [B] or NULL (node M - 1). For a chain this is the chunk's verified length:
+ *           k_h = path_end[b] + 1 (Appendix "Chunk-Level vs Token-Level", chunks of length k_h).
  * eal     : [B][N] Theorem 3 along the path root -> path_end[b].
  * prefix  : [B][N][M] or NULL: product of gamma over the path root -> n, for every node n.
  * loss    : [L][B][N] or NULL, by loss_kind:
  *   LENGTH        : 1 - EAL / (K_path + 1)                      (chunk length loss, Appendix "Chunk-Level Games")
- *   ACCEPT_TOKEN  : L = M vectors, l_k = 1 - gamma_k (chain only) (acceptance-probability loss, Section 3.3)
+ *   ACCEPT_TOKEN  : L = M vectors, l_k = 1 - gamma_k for the k_h tokens of the chunk and zero
+ *                   vectors after them (chain only) (acceptance-probability loss, Section 3.3)
  *   ACCEPT_CHUNK  : (1/K_path) sum_k (1 - gamma_k)               (chunk acceptance loss, Appendix "Chunk-Level Games")
  * Returns 0, or -1 on an invalid path.
  */
@@ -309,7 +339,12 @@ int or_accept_len(const double* gamma, int B, int N, int M, const int32_t* paren
       if (len < 1) {
         bad = 1;
         eal[b * N + i] = NAN;
-        if (loss) loss[b * N + i] = NAN;
+        if (loss) {
+          if (loss_kind == OR_LOSS_ACCEPT_TOKEN)
+            for (int k = 0; k < M; ++k) loss[((size_t)k * B + b) * N + i] = NAN;
+          else
+            loss[b * N + i] = NAN;
+        }
         continue;
       }
       double gp[4096];
@@ -333,7 +368,9 @@ int or_accept_len(const double* gamma, int B, int N, int M, const int32_t* paren
           for (int j = 0; j < len; ++j) s += 1.0 - gp[j];
           loss[b * N + i] = s / (double)len;
         } else {
-          for (int k = 0; k < M; ++k) loss[((size_t)k * B + b) * N + i] = 1.0 - g[k];
+          /* chains only: one vector per verified token of the chunk (k_h = end + 1 of them);
+             the rows past the chunk are zero vectors, which leave both learners unchanged */
+          for (int k = 0; k < M; ++k) loss[((size_t)k * B + b) * N + i] = k <= end ? 1.0 - g[k] : 0.0;
         }
       }
     }

@@ -587,3 +587,85 @@ def test_topl_rejects_bad_arguments():
     with pytest.raises(ValueError):
         oracle.topl(x, 2, T=0.0)
     assert oracle.topl(x, 2, T=0.0, want_mass=False)["hit"][0, 0] == 1
+
+
+# ------------------------------------------------------------------------------------------
+# Chunks of ragged verified length k_h (Appendix "Chunk-Level vs Token-Level")
+# ------------------------------------------------------------------------------------------
+
+def test_ragged_chunk_lengths_closed_forms_and_token_rows():
+    rng = np.random.default_rng(31)
+    B, N, K = 4, 3, 6
+    alpha = np.array([0.3, 0.6, 0.9])
+    g = np.broadcast_to(alpha[None, :, None], (B, N, K)).copy()  # constant gamma per drafter
+    ends = np.array([0, 2, 5, 3], dtype=np.int32)  # k_h = 1, 3, 6, 4
+    out = oracle.accept_len(g, path_end=ends, loss_kind=oracle.LOSS_LENGTH)
+    for b, e in enumerate(ends):
+        k = e + 1
+        want = (1 - alpha ** (k + 1)) / (1 - alpha)  # constant-gamma closed form with K = k_h
+        assert np.allclose(out["eal"][b], want, rtol=1e-13, atol=0)
+        assert np.allclose(out["loss"][0, b], 1 - want / (k + 1), rtol=1e-13, atol=0)
+    ch = oracle.accept_len(g, path_end=ends, loss_kind=oracle.LOSS_ACCEPT_CHUNK)
+    assert np.allclose(ch["loss"][0], (1 - alpha)[None, :].repeat(B, 0), rtol=1e-13, atol=0)
+    # token losses: one vector per verified token, zero vectors past the chunk
+    gr = rng.random((B, N, K))
+    tok = oracle.accept_len(gr, path_end=ends, loss_kind=oracle.LOSS_ACCEPT_TOKEN)["loss"]
+    for b, e in enumerate(ends):
+        assert np.array_equal(tok[: e + 1, b], (1 - gr[b]).T[: e + 1])
+        assert np.all(tok[e + 1:, b] == 0.0)
+    # zero vectors change neither learner: the first k_h vectors alone give the same state
+    w0 = np.full((B, N), 1.0 / N)
+    w_all = oracle.hedge(w0, tok, 0.5)
+    for b, e in enumerate(ends):
+        w_b = oracle.hedge(w0[b:b + 1], tok[: e + 1, b:b + 1], 0.5)
+        assert np.allclose(w_all[b], w_b[0], rtol=0, atol=1e-15)
+    R0, p0 = np.zeros((B, N)), np.full((B, N), 1.0 / N)
+    R_all, p_all, _ = oracle.normalhedge(R0, p0, tok)
+    for b, e in enumerate(ends):
+        Rb, pb, _ = oracle.normalhedge(R0[b:b + 1], p0[b:b + 1], tok[: e + 1, b:b + 1])
+        assert np.array_equal(R_all[b], Rb[0]) and np.allclose(p_all[b], pb[0], rtol=0, atol=1e-12)
+
+
+def test_ragged_chunk_invalid_length_is_nan_in_every_token_row():
+    g = np.full((2, 2, 4), 0.5)
+    tok = oracle.accept_len(g, path_end=np.array([4, 1], np.int32), loss_kind=oracle.LOSS_ACCEPT_TOKEN)
+    assert np.all(np.isnan(tok["loss"][:, 0])) and not np.any(np.isnan(tok["loss"][:, 1]))
+    assert not tok["ok"]
+
+
+# ------------------------------------------------------------------------------------------
+# Hybrid losses (Appendix "Practical heuristics")
+# ------------------------------------------------------------------------------------------
+
+def test_hybrid_losses_limits_and_the_appendix_example():
+    rng = np.random.default_rng(51)
+    T, N, K = 20, 4, 8
+    g = rng.random((T, N))
+    assert np.array_equal(oracle.hybrid_losses(g, K, 0), oracle.window_losses(g, K))
+    assert np.array_equal(oracle.hybrid_losses(g, K, T), 1.0 - g)
+    h = oracle.hybrid_losses(g, K, 5)
+    assert h.shape[0] == 5 + (T - K + 1 - 5)
+    assert np.array_equal(h[:5], 1.0 - g[:5])
+    assert np.array_equal(h[5:], oracle.window_losses(g, K)[5:])
+    # the appendix's example: K = 8 and a first chunk of 4 tokens. The acceptance loss can
+    # already update the learner 4 times; the length loss cannot update it at all yet.
+    first = g[:4]
+    assert oracle.hybrid_losses(first, 8, 4).shape[0] == 4
+    assert oracle.hybrid_losses(first, 8, 0).shape[0] == 0
+
+
+def test_hybrid_qfid_chunking_invariance():
+    rng = np.random.default_rng(52)
+    B, N, K, H, rounds = 3, 5, 4, 6, 9
+    gam = rng.random((rounds, B, N, K))
+    cnt = rng.integers(0, K + 1, (rounds, B))
+    a = oracle.QfiD(B, N, K, 0.5, hybrid=H)
+    for r in range(rounds):
+        a.push(gam[r], cnt[r])
+    streams = [np.concatenate([gam[r, b, :, :cnt[r, b]].T for r in range(rounds)]) for b in range(B)]
+    for b in range(B):
+        ls = oracle.hybrid_losses(streams[b], K, H)
+        w = oracle.hedge(np.full((1, N), 1.0 / N), ls[:, None, :], 0.5)
+        R, p, _ = oracle.normalhedge(np.zeros((1, N)), np.full((1, N), 1.0 / N), ls[:, None, :])
+        assert np.allclose(a.w[b], w[0], rtol=0, atol=1e-13)
+        assert np.allclose(a.p[b], p[0], rtol=0, atol=1e-12)
