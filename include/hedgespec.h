@@ -179,11 +179,15 @@ int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int N, int
  *   prefix[n] = gamma[n] * prefix[parent[n]] (root: gamma[0]); the path is
  *   root -> path_end[b]; EAL = 1 + sum of prefix over the path's K_path nodes.
  * path_end     : [B] int32 device array or NULL (node K-1). An index outside
- *                [0, K) gives NaN for that query's EAL and loss.
+ *                [0, K) gives NaN for that query's EAL and loss. For a chain it is the
+ *                chunk's verified length k_h - 1 (Appendix "Chunk-Level vs Token-Level":
+ *                chunks of ragged length k_h use Theorem 3 with K = k_h).
  * eal          : [B][N] fp64 (required).
  * prefix       : [B][N][K] fp64 or NULL.
  * loss         : [L][B][N] fp64 or NULL; L = K for HS_LOSS_ACCEPT_TOKEN (chains
- *                only), else L = 1. See HS_LOSS_* for the definitions.
+ *                only: rows past a query's k_h verified tokens are zero vectors, which
+ *                leave Hedge and NormalHedge unchanged), else L = 1. See HS_LOSS_* for the
+ *                definitions.
  */
 int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
                   const int32_t* parent_host, const int32_t* path_end, double* eal,
@@ -233,6 +237,13 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
  * alpha / agree : [B][N][K] gamma of this round (HS_SAMPLE: alpha fp32; HS_GREEDY:
  *                 agree uint8); token j of the call is position j, j < count[b].
  * count         : [B] int32 device; values outside [0, K] are clamped to it.
+ * hybrid_tokens : H >= 0. Hybrid losses (Appendix "Practical heuristics: hybrid losses"): the
+ *                 first H tokens of every query's stream take the acceptance-probability loss
+ *                 1 - gamma_s instead, known as soon as the token's feedback arrives (against
+ *                 the cold start); 0 = the length loss throughout. The tokens whose loss is
+ *                 known always form a prefix of the stream, so the FIFO order is unchanged.
+ *                 Use the same H for every call of a stream (a change shifts the switch; a
+ *                 call then uses at most K of the losses that became known, the rest later).
  * hist          : [B][2K][N] fp32 device, the history ring (caller-owned, zero-filled
  *                 before the first call of a stream, not read by the caller).
  * clock         : [B][2] int64 device, zero-filled before the first call: tokens
@@ -241,15 +252,15 @@ int hs_normalhedge_update(double* R, double* p, double* c, const double* loss, i
  *                 none), as in hs_hedge_update / hs_normalhedge_update.
  * loss          : [K][B][N] fp64 or NULL: the window losses used by this call, in
  *                 order (rows past nloss[b] are not written).
- * nloss         : [B] int32 or NULL: how many windows each query used (at most count[b]).
+ * nloss         : [B] int32 or NULL: how many loss vectors each query used (at most count[b]).
  * One launch, one wave per query. Errors: HS_ERR_SHAPE / HS_ERR_LIMIT on B, N, K;
  * HS_ERR_ARG on mode or a non-finite eta; HS_ERR_NULL on missing inputs or unpaired
  * learner state. Nothing is enqueued on error.
  */
 int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
-                      const int32_t* count, float* hist, int64_t* clock, double* logw,
-                      double* w, double eta, double* R, double* p, double* c, double* loss,
-                      int32_t* nloss, void* stream);
+                      const int32_t* count, int64_t hybrid_tokens, float* hist, int64_t* clock,
+                      double* logw, double* w, double eta, double* R, double* p, double* c,
+                      double* loss, int32_t* nloss, void* stream);
 
 /*
  * hs_round - one verification round of the whole path, enqueued as two launches

@@ -77,7 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_hedge_update.argtypes = [P, P, P, I, I, I, D, P]
     lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
     lib.hs_round.argtypes = [ctypes.POINTER(hs_round_args), P]
-    lib.hs_delayed_update.argtypes = [P, P, I, I, I, I, P, P, P, P, P, D, P, P, P, P, P, P]
+    lib.hs_delayed_update.argtypes = [P, P, I, I, I, I, P, I64, P, P, P, P, D, P, P, P, P, P, P]
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
@@ -302,21 +302,63 @@ class DelayedState:
 
 def delayed_update(state: DelayedState, gamma: torch.Tensor, count: torch.Tensor, eta: float,
                    mode: int = SAMPLE, hedge: bool = True, normalhedge: bool = True,
-                   stream=None) -> None:
+                   hybrid_tokens: int = 0, stream=None) -> None:
     """hs_delayed_update: append query b's next count[b] tokens of feedback (gamma [B][N][K]:
-    alpha fp32 in SAMPLE mode, agree uint8 in GREEDY mode) and feed every newly complete
-    K-token window's length loss to the learners. The losses used are left in state.loss
-    (first state.nloss[b] rows per query)."""
+    alpha fp32 in SAMPLE mode, agree uint8 in GREEDY mode) and feed every token loss that is
+    now known (the K-token window's length loss; the acceptance loss for each query's first
+    hybrid_tokens tokens) to the learners. The losses used are left in state.loss (first
+    state.nloss[b] rows per query)."""
     B, N, K = gamma.shape
     st = state.learners
     alpha = gamma if mode == SAMPLE else None
     agree = gamma if mode == GREEDY else None
     _check(load_library().hs_delayed_update(
-        _ptr(alpha), _ptr(agree), mode, B, N, K, _ptr(count), _ptr(state.hist),
-        _ptr(state.clock), _ptr(st.logw if hedge else None), _ptr(st.w if hedge else None),
-        eta, _ptr(st.R if normalhedge else None), _ptr(st.p if normalhedge else None),
-        _ptr(st.c if normalhedge else None), _ptr(state.loss), _ptr(state.nloss),
-        _stream(stream)))
+        _ptr(alpha), _ptr(agree), mode, B, N, K, _ptr(count), int(hybrid_tokens),
+        _ptr(state.hist), _ptr(state.clock), _ptr(st.logw if hedge else None),
+        _ptr(st.w if hedge else None), eta, _ptr(st.R if normalhedge else None),
+        _ptr(st.p if normalhedge else None), _ptr(st.c if normalhedge else None),
+        _ptr(state.loss), _ptr(state.nloss), _stream(stream)))
+
+
+class UpdateCadence:
+    """Batched delayed feedback (Appendix "Practical heuristics: skipping update"): the
+    learners are updated every round during a warm-up, then only once every `batch` rounds,
+    with all the feedback gathered since the last update. QFI-D applies the queued losses in
+    token order either way, so after an update the learners hold exactly the state that
+    per-round updates would give; only the predictions in between are older.
+
+    push(gamma, count) keeps a device copy of the round's feedback (gamma [B][N][K], count [B])
+    and, when the round is due, replays every kept round through hs_delayed_update in order.
+    Returns whether the learners were updated. Scheduling only: the losses and the learner
+    steps run in the library's kernel."""
+
+    def __init__(self, state: DelayedState, eta: float, warmup: int = 6, batch: int = 12,
+                 mode: int = SAMPLE, hybrid_tokens: int = 0):
+        if warmup < 0 or batch < 1:
+            raise ValueError("need warmup >= 0 and batch >= 1")
+        self.state, self.eta, self.warmup, self.batch = state, eta, warmup, batch
+        self.mode, self.hybrid_tokens = mode, hybrid_tokens
+        self.rounds = 0
+        self.pending = []
+
+    def due(self, r: int) -> bool:
+        """Whether round r (0-based) ends with an update of the learners."""
+        return r < self.warmup or (r + 1 - self.warmup) % self.batch == 0
+
+    def push(self, gamma: torch.Tensor, count: torch.Tensor, stream=None) -> bool:
+        self.pending.append((gamma.clone(), count.clone()))
+        r = self.rounds
+        self.rounds += 1
+        if not self.due(r):
+            return False
+        self.flush(stream)
+        return True
+
+    def flush(self, stream=None) -> None:
+        for g, c in self.pending:
+            delayed_update(self.state, g, c, self.eta, mode=self.mode,
+                           hybrid_tokens=self.hybrid_tokens, stream=stream)
+        self.pending = []
 
 
 class Round:

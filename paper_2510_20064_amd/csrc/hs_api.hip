@@ -389,7 +389,8 @@ HS_API int hs_normalhedge_update(double* R, double* p, double* c, const double* 
 }
 
 HS_API int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode, int B, int N,
-                             int K, const int32_t* count, float* hist, int64_t* clock,
+                             int K, const int32_t* count, int64_t hybrid_tokens, float* hist,
+                             int64_t* clock,
                              double* logw, double* w, double eta, double* R, double* p,
                              double* c, double* loss, int32_t* nloss, void* stream) {
   int rc = check_shape(B, N, K, 1);
@@ -403,6 +404,7 @@ HS_API int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode,
   if (!((R == nullptr) == (p == nullptr) && (R == nullptr) == (c == nullptr)))
     return fail(HS_ERR_NULL, "R, p and c must be given together");
   if (logw && !isfinite(eta)) return fail(HS_ERR_ARG, "eta must be finite");
+  if (hybrid_tokens < 0) return fail(HS_ERR_ARG, "hybrid_tokens must be >= 0");
   hs::DelayArgs a{};
   a.alpha = alpha;
   a.agree = agree;
@@ -411,6 +413,7 @@ HS_API int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode,
   a.N = N;
   a.K = K;
   a.count = count;
+  a.hybrid = hybrid_tokens;
   a.hist = hist;
   a.clock = clock;
   a.logw = logw;

@@ -256,6 +256,7 @@ struct DelayArgs {
   int gamma_src;
   int B, N, K;
   const int32_t* count;  // [B]: tokens whose feedback arrives now (positions 0 .. count - 1)
+  int64_t hybrid;        // tokens 0 .. hybrid - 1 of each stream take the acceptance loss
   float* hist;           // [B][2K][N]: feedback of the last 2K tokens, by token index mod 2K
   int64_t* clock;        // [B][2]: tokens received, windows used
   double* logw;

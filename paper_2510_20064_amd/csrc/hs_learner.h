@@ -5,6 +5,7 @@
 //                 k (1 - gamma_k) prod_{j<k} gamma_j by parts (gamma_{K+1} = 0) gives this form.
 //   loss        : HS_LOSS_LENGTH 1 - EAL/(K_path + 1); HS_LOSS_ACCEPT_CHUNK mean of
 //                 (1 - gamma) over the path; HS_LOSS_ACCEPT_TOKEN the K vectors 1 - gamma_k
+//                 (zero vectors past a chain's k_h = end + 1 verified tokens)
 //   Hedge       : logw -= eta * loss for each vector in order; w = softmax(logw)
 //   NormalHedge : per vector, R_i += l_A - l_i; c solves (1/N) sum exp([R]_+^2 / 2c) = e;
 //                 p_i ~ ([R_i]_+ / c) exp([R_i]_+^2 / 2c)
@@ -226,7 +227,9 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
       double pp = 1.0, sp = 0.0;
       for (int n = 0; n < M; ++n) {
         const double g = gamma_at(n);
-        if (a.loss_kind == HS_LOSS_ACCEPT_TOKEN) lossv[n * N + i] = 1.0 - g;
+        // one token loss per verified token of the chunk (k_h = end + 1 of them), zero
+        // vectors (no change to either learner) after them
+        if (a.loss_kind == HS_LOSS_ACCEPT_TOKEN) lossv[n * N + i] = !ok ? NAN : n <= end ? 1.0 - g : 0.0;
         pp *= g;
         if (a.prefix) a.prefix[((int64_t)b * N + i) * M + n] = pp;
         if (n <= end) {

@@ -141,12 +141,12 @@ def test_round_validation_codes():
 
 
 def _delayed(lib, **kw):
-    a = dict(alpha=FAKE, agree=None, mode=0, B=4, N=8, K=8, count=FAKE, hist=FAKE, clock=FAKE,
-             logw=FAKE, w=FAKE, eta=0.5, R=FAKE, p=FAKE, c=FAKE, loss=None, nloss=None)
+    a = dict(alpha=FAKE, agree=None, mode=0, B=4, N=8, K=8, count=FAKE, hybrid=0, hist=FAKE,
+             clock=FAKE, logw=FAKE, w=FAKE, eta=0.5, R=FAKE, p=FAKE, c=FAKE, loss=None, nloss=None)
     a.update(kw)
     return lib.hs_delayed_update(a["alpha"], a["agree"], a["mode"], a["B"], a["N"], a["K"],
-                                 a["count"], a["hist"], a["clock"], a["logw"], a["w"], a["eta"],
-                                 a["R"], a["p"], a["c"], a["loss"], a["nloss"], None)
+                                 a["count"], a["hybrid"], a["hist"], a["clock"], a["logw"], a["w"],
+                                 a["eta"], a["R"], a["p"], a["c"], a["loss"], a["nloss"], None)
 
 
 def test_delayed_update_validation_codes():
@@ -164,6 +164,7 @@ def test_delayed_update_validation_codes():
     assert _delayed(lib, w=None) == 1
     assert _delayed(lib, c=None) == 1
     assert _delayed(lib, eta=float("inf")) == 10
+    assert _delayed(lib, hybrid=-1) == 10
 
 
 def _topl(lib, **kw):

@@ -20,10 +20,10 @@ def note(msg):
     print("\n[case] " + msg, flush=True)
 
 
-def _run(B, N, K, rounds, eta, mode, seed, max_count=None):
+def _run(B, N, K, rounds, eta, mode, seed, max_count=None, hybrid=0):
     rng = np.random.default_rng(seed)
     st = hs.DelayedState(B, N, K, "cuda")
-    q = oracle.QfiD(B, N, K, eta)
+    q = oracle.QfiD(B, N, K, eta, hybrid=hybrid)
     mc = K if max_count is None else max_count
     for r in range(rounds):
         if mode == hs.SAMPLE:
@@ -33,7 +33,8 @@ def _run(B, N, K, rounds, eta, mode, seed, max_count=None):
             g32 = (rng.random((B, N, K)) < 0.7).astype(np.uint8)
             gd = torch.from_numpy(g32).cuda()
         cnt = rng.integers(0, mc + 1, B).astype(np.int32)
-        hs.delayed_update(st, gd, torch.from_numpy(cnt).cuda(), eta, mode=mode)
+        hs.delayed_update(st, gd, torch.from_numpy(cnt).cuda(), eta, mode=mode,
+                          hybrid_tokens=hybrid)
         used = q.push(g32.astype(np.float64), cnt)
         torch.cuda.synchronize()
         nl = st.nloss.cpu().numpy()
@@ -110,3 +111,34 @@ def test_delayed_chunking_invariance():
     assert torch.equal(s1.learners.R, s2.learners.R) and torch.equal(s1.learners.p, s2.learners.p)
     assert torch.equal(s1.learners.c, s2.learners.c)
     assert torch.allclose(s1.learners.w, s2.learners.w, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("hybrid", [3, 7, 1000])
+def test_delayed_hybrid_losses(hybrid):
+    # acceptance losses for the first H tokens of each stream, then window length losses
+    note("hybrid H=%d, B=4 N=6 K=5, 30 rounds" % hybrid)
+    _run(4, 6, 5, 30, 0.5, hs.SAMPLE, seed=11, hybrid=hybrid)
+
+
+def test_update_cadence_matches_per_round_updates_at_every_update():
+    rng = np.random.default_rng(12)
+    B, N, K, rounds = 3, 7, 4, 40
+    gam = [torch.from_numpy(rng.random((B, N, K)).astype(np.float32)).cuda() for _ in range(rounds)]
+    cnt = [torch.from_numpy(rng.integers(0, K + 1, B).astype(np.int32)).cuda() for _ in range(rounds)]
+    note("update cadence: warm-up 6, batches of 12, hybrid 5")
+    every = hs.DelayedState(B, N, K, "cuda")
+    batched = hs.DelayedState(B, N, K, "cuda")
+    cad = hs.UpdateCadence(batched, 0.5, warmup=6, batch=12, hybrid_tokens=5)
+    prev_w = batched.learners.w.clone()
+    for r in range(rounds):
+        hs.delayed_update(every, gam[r], cnt[r], 0.5, hybrid_tokens=5)
+        updated = cad.push(gam[r], cnt[r])
+        torch.cuda.synchronize()
+        assert updated == cad.due(r)
+        if updated:  # the same kernel calls in the same order: the same bits
+            for f in ("logw", "w", "R", "p", "c"):
+                assert torch.equal(getattr(batched.learners, f), getattr(every.learners, f)), (r, f)
+            prev_w = batched.learners.w.clone()
+        else:
+            assert torch.equal(batched.learners.w, prev_w), r
+    assert [r for r in range(rounds) if cad.due(r)] == [0, 1, 2, 3, 4, 5, 17, 29]
