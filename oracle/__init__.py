@@ -51,6 +51,10 @@ def _load():
         lib.or_topl.restype = I
         lib.or_hybrid_losses.argtypes = [P, I, I, I, I64, P]
         lib.or_hybrid_losses.restype = I
+        lib.or_play.argtypes = [P, I, I, I, P, P]
+        lib.or_play.restype = None
+        lib.or_regret_update.argtypes = [P, I, I, I, P, P, P, P, P, P]
+        lib.or_regret_update.restype = None
         lib.or_softmax_stats.argtypes = [P, I, I64, I64, I64, D, P, P, P]
         lib.or_softmax_stats.restype = I
         lib.or_path.argtypes = [P, I, I, P]
@@ -240,6 +244,37 @@ def window_losses(gamma: np.ndarray, K: int) -> np.ndarray:
     n = _load().or_window_losses(_p(g), T, N, K, _p(out))
     assert n == out.shape[0]
     return out
+
+
+def play(weights: np.ndarray, how: int = 0, u: Optional[np.ndarray] = None) -> np.ndarray:
+    """Drafter choice per query from weights [B][N]: argmax (how 0) or an inverse-CDF sample
+    with the uniform draws u [B] (how 1); -1 for a row without positive total weight."""
+    w = np.ascontiguousarray(weights, dtype=np.float64)
+    B, N = w.shape
+    uu = None if u is None else np.ascontiguousarray(u, dtype=np.float64)
+    out = np.zeros(B, dtype=np.int32)
+    _load().or_play(_p(w), B, N, how, _p(uu), _p(out))
+    return out
+
+
+class Regret:
+    """Regret bookkeeping for B queries and N drafters (see or_regret_update)."""
+
+    def __init__(self, B: int, N: int):
+        self.cum = np.zeros((B, N))
+        self.played = np.zeros(B)
+        self.regret = np.zeros(B)
+        self.eal_sum = np.zeros(B)
+
+    def update(self, loss: np.ndarray, played: np.ndarray, eal: Optional[np.ndarray] = None):
+        """loss [L][B][N] in order, played [L][B] int32 (the drafter played for each vector)."""
+        lo = np.ascontiguousarray(loss, dtype=np.float64)
+        L, B, N = lo.shape
+        pl = np.ascontiguousarray(played, dtype=np.int32).reshape(L, B)
+        ea = None if eal is None else np.ascontiguousarray(eal, dtype=np.float64)
+        _load().or_regret_update(_p(lo), L, B, N, _p(pl), _p(self.cum), _p(self.played),
+                                 _p(self.regret), _p(ea), _p(self.eal_sum if ea is not None else None))
+        return self.regret
 
 
 def hybrid_losses(gamma: np.ndarray, K: int, H: int) -> np.ndarray:

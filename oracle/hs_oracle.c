@@ -25,6 +25,10 @@
  *                             drafter, L = 1 greedy hit equals argmax agreement).
  *   or_hybrid_losses        : pinned (H = 0 is the window loss, H >= T the acceptance loss,
  *                             the appendix's K = 8 example with a first chunk of 4 tokens).
+ *   or_play                 : pinned (point masses, empirical frequencies on a uniform grid
+ *                             of draws, argmax ties by index, zero rows).
+ *   or_regret_update        : pinned (hand-computed stream, always playing one drafter,
+ *                             Hedge's expected-regret bound ln N / eta + eta T / 8).
  *   or_window_losses        : pinned (all-accept and all-reject windows, K = 1, constant
  *                             gamma geometric sum, the censoring appendix's worked example).
  *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
@@ -303,6 +307,71 @@ int or_hybrid_losses(const double* gamma, int T, int N, int K, int64_t H, double
     ++n;
   }
   return n;
+}
+
+/*
+ * Drafter play (Appendix, algorithm QFI-D: play action a_t according to p, by sampling from p
+ * or by taking its argmax). weights: [B][N], non-negative, not necessarily normalised.
+ *   how = 0: choice = the lowest index of the largest weight;
+ *   how = 1: choice = the smallest i with w_0 + ... + w_i > u[b] (w_0 + ... + w_{N-1}), the
+ *            prefix sums taken left to right; u[b] in [0, 1) is the query's uniform draw.
+ * A row whose weights sum to 0 (or are not finite) gives -1.
+ */
+void or_play(const double* weights, int B, int N, int how, const double* u, int32_t* choice) {
+  for (int b = 0; b < B; ++b) {
+    const double* w = weights + (size_t)b * N;
+    double tot = 0.0;
+    for (int i = 0; i < N; ++i) tot += w[i];
+    int c = -1;
+    if (tot > 0.0 && isfinite(tot)) {
+      if (how == 0) {
+        c = 0;
+        for (int i = 1; i < N; ++i)
+          if (w[i] > w[c]) c = i;
+      } else {
+        const double thr = u[b] * tot;
+        double acc = 0.0;
+        c = N - 1;  /* rounding can leave the last prefix at or below thr */
+        for (int i = 0; i < N; ++i) {
+          acc += w[i];
+          if (acc > thr) {
+            c = i;
+            break;
+          }
+        }
+      }
+    }
+    choice[b] = c;
+  }
+}
+
+/*
+ * Regret bookkeeping (Section 3.1): Regret_T = sum_t f_t[i_t] - min_i sum_t f_t[i], with the
+ * drafter i_t that was played when loss vector f_t applied. For each of the L vectors in order:
+ * cum[b][i] += f[b][i]; played_sum[b] += f[b][i_t]. Then regret[b] = played_sum[b] -
+ * min_i cum[b][i]. A played index outside [0, N) makes that query's sums NaN. With eal [B][N]
+ * given, eal_sum[b] += eal[b][i] for the drafter i played with the last vector (the round's
+ * expected accepted length, whose mean over rounds is the mean accepted length).
+ */
+void or_regret_update(const double* loss, int L, int B, int N, const int32_t* played,
+                      double* cum, double* played_sum, double* regret, const double* eal,
+                      double* eal_sum) {
+  for (int b = 0; b < B; ++b) {
+    for (int l = 0; l < L; ++l) {
+      const double* f = loss + ((size_t)l * B + b) * N;
+      const int it = played[(size_t)l * B + b];
+      for (int i = 0; i < N; ++i) cum[(size_t)b * N + i] += f[i];
+      played_sum[b] += (it >= 0 && it < N) ? f[it] : NAN;
+    }
+    double mn = INFINITY;
+    for (int i = 0; i < N; ++i)
+      if (cum[(size_t)b * N + i] < mn) mn = cum[(size_t)b * N + i];
+    regret[b] = played_sum[b] - mn;
+    if (eal && eal_sum && L > 0) {
+      const int it = played[(size_t)(L - 1) * B + b];
+      eal_sum[b] += (it >= 0 && it < N) ? eal[(size_t)b * N + it] : NAN;
+    }
+  }
 }
 
 /*

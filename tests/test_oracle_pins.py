@@ -669,3 +669,59 @@ def test_hybrid_qfid_chunking_invariance():
         R, p, _ = oracle.normalhedge(np.zeros((1, N)), np.full((1, N), 1.0 / N), ls[:, None, :])
         assert np.allclose(a.w[b], w[0], rtol=0, atol=1e-13)
         assert np.allclose(a.p[b], p[0], rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------------
+# Drafter play and regret bookkeeping (Section 3.1; Appendix, algorithm QFI-D)
+# ------------------------------------------------------------------------------------------
+
+def test_play_argmax_ties_point_masses_and_empty_rows():
+    w = np.array([[0.2, 0.5, 0.5, 0.1], [0, 0, 1.0, 0], [0, 0, 0, 0], [1, np.nan, 0, 0]])
+    assert list(oracle.play(w, 0)) == [1, 2, -1, -1]
+    for u in (0.0, 0.3, 0.999999):
+        assert oracle.play(w[1:2], 1, np.array([u]))[0] == 2
+
+
+def test_play_sampling_frequencies_on_a_grid_of_draws_are_the_weights():
+    # integer weights k_i summing to M and draws u = m / M: exactly k_i draws pick drafter i
+    k = np.array([3, 0, 7, 1, 0, 5, 0, 24], dtype=np.float64)
+    M = int(k.sum())
+    u = np.arange(M) / M
+    ch = oracle.play(np.tile(k, (M, 1)), 1, u)
+    assert np.array_equal(np.bincount(ch, minlength=len(k)), k.astype(int))
+    assert list(ch[:4]) == [0, 0, 0, 2]  # inverse CDF: the draws fill the drafters in order
+
+
+def test_regret_hand_computed_and_fixed_play():
+    f = np.array([[[0.2, 0.5]], [[0.7, 0.1]], [[0.3, 0.3]]])  # [L=3][B=1][N=2]
+    r = oracle.Regret(1, 2)
+    reg = r.update(f, np.array([[1], [0], [1]], dtype=np.int32))
+    assert abs(r.played[0] - 1.5) < 1e-15 and np.allclose(r.cum[0], [1.2, 0.9], atol=1e-15)
+    assert abs(reg[0] - 0.6) < 1e-15
+    rng = np.random.default_rng(61)
+    L, B, N = 50, 3, 6
+    f = rng.random((L, B, N))
+    best = f.sum(0).argmin(1)
+    for j in range(N):
+        rj = oracle.Regret(B, N)
+        reg = rj.update(f, np.full((L, B), j, dtype=np.int32))
+        assert np.allclose(reg, f.sum(0)[:, j] - f.sum(0).min(1), rtol=0, atol=1e-12)
+        assert np.all(reg >= 0) and np.all(reg[best == j] == 0.0)
+    # chunked updates give the same sums
+    rc = oracle.Regret(B, N)
+    pl = rng.integers(0, N, (L, B)).astype(np.int32)
+    for l0 in range(0, L, 7):
+        rc.update(f[l0:l0 + 7], pl[l0:l0 + 7])
+    ro = oracle.Regret(B, N)
+    ro.update(f, pl)
+    assert np.allclose(rc.regret, ro.regret, rtol=0, atol=1e-12)
+
+
+def test_regret_eal_of_the_played_drafter_and_bad_indices():
+    r = oracle.Regret(2, 3)
+    eal = np.array([[1.5, 2.5, 3.5], [4.0, 5.0, 6.0]])
+    r.update(np.zeros((2, 2, 3)), np.array([[0, 2], [1, 0]], dtype=np.int32), eal=eal)
+    assert list(r.eal_sum) == [2.5, 4.0]  # the drafter played with the last vector
+    rb = oracle.Regret(1, 3)
+    rb.update(np.zeros((1, 1, 3)), np.array([[3]], dtype=np.int32))
+    assert np.isnan(rb.regret[0])
