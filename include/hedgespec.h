@@ -65,6 +65,9 @@ extern "C" {
 #define HS_SAMPLE 0 /* gamma = alpha, speculative sampling at temperature T (Theorem 1)        */
 #define HS_GREEDY 1 /* gamma = argmax agreement, Theorem 1 with one-hot p and q (greedy)       */
 
+#define HS_PLAY_ARGMAX 0 /* play the drafter of largest weight (lowest index on ties)   */
+#define HS_PLAY_SAMPLE 1 /* sample the drafter from the weights with a given draw        */
+
 #define HS_LOSS_LENGTH 0       /* 1 - EAL/(K_path + 1): chunk length loss (Appendix "Chunk-Level Games") */
 #define HS_LOSS_ACCEPT_TOKEN 1 /* K vectors 1 - gamma_k, in order (Section 3.3, acceptance loss)         */
 #define HS_LOSS_ACCEPT_CHUNK 2 /* (1/K_path) sum_k (1 - gamma_k) (Appendix "Chunk-Level Games")           */
@@ -261,6 +264,39 @@ int hs_delayed_update(const float* alpha, const uint8_t* agree, int mode, int B,
                       const int32_t* count, int64_t hybrid_tokens, float* hist, int64_t* clock,
                       double* logw, double* w, double eta, double* R, double* p, double* c,
                       double* loss, int32_t* nloss, void* stream);
+
+/*
+ * hs_play - the drafter each query plays next (Appendix, algorithm QFI-D, "Queued
+ * Full-Information with Delays": after the queued losses are in, play a_t according to p, by
+ * sampling from p or by its argmax).
+ * weights : [B][N] fp64 device, non-negative (Hedge's w or NormalHedge's p; need not sum to 1).
+ * how     : HS_PLAY_ARGMAX, or HS_PLAY_SAMPLE: the smallest i with w_0 + ... + w_i >
+ *           u[b] * (w_0 + ... + w_{N-1}), prefix sums taken left to right in fp64.
+ * u       : [B] fp64 device uniform draws in [0, 1) (required for HS_PLAY_SAMPLE; the caller
+ *           owns the random stream).
+ * choice  : [B] int32 device out; -1 for a row whose weights do not sum to a positive finite
+ *           number. One launch, one wave per query.
+ */
+int hs_play(const double* weights, int B, int N, int how, const double* u, int32_t* choice,
+            void* stream);
+
+/*
+ * hs_regret_update - regret bookkeeping (Section 3.1): Regret_T = sum_t f_t[i_t] -
+ * min_i sum_t f_t[i], with i_t the drafter played when loss vector f_t applied. For each of
+ * the L loss vectors in order: cum_loss[b][i] += f[b][i] and played_loss[b] += f[b][i_t]; then
+ * regret[b] = played_loss[b] - min_i cum_loss[b][i] (the sums run in loss order, in fp64).
+ * loss        : [L][B][N] fp64 device (as hs_accept_len writes it), L >= 1.
+ * played      : [L][B] int32 device: the drafter played for each vector. An index outside
+ *               [0, N) makes that query's played_loss and regret NaN from then on.
+ * cum_loss    : [B][N] fp64 in/out, played_loss: [B] fp64 in/out (zero-fill to start);
+ *               regret: [B] fp64 out.
+ * eal, eal_sum: both or neither. eal [B][N] (this round's expected accepted lengths);
+ *               eal_sum[b] += eal[b][i] for the drafter played with the last vector, so that
+ *               eal_sum / rounds is the played drafters' mean accepted length.
+ */
+int hs_regret_update(const double* loss, int L, int B, int N, const int32_t* played,
+                     double* cum_loss, double* played_loss, double* regret, const double* eal,
+                     double* eal_sum, void* stream);
 
 /*
  * hs_round - one verification round of the whole path, enqueued as two launches

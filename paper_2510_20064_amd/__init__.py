@@ -3,7 +3,8 @@
 Argument marshalling only: every step runs in the library's HIP kernels. PyTorch supplies
 device memory and the current HIP stream. The function names match the C ABI declared in
 include/hedgespec.h (hs_softmax_stats, hs_eval_alpha, hs_eval_topl, hs_accept_len,
-hs_hedge_update, hs_normalhedge_update, hs_delayed_update, hs_round). There is no CPU fallback: if the library is not built,
+hs_hedge_update, hs_normalhedge_update, hs_delayed_update, hs_play, hs_regret_update,
+hs_round). There is no CPU fallback: if the library is not built,
 loading raises.
 """
 from __future__ import annotations
@@ -73,6 +74,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_eval_topl_workspace_size.argtypes = [I, I, I, I64, I, I]
     lib.hs_eval_topl_workspace_size.restype = SZ
     lib.hs_eval_topl.argtypes = [VP, VP, I, I, I, I64, I, I, F, I, P, P, P, P, SZ, P]
+    lib.hs_play.argtypes = [P, I, I, I, P, P, P]
+    lib.hs_regret_update.argtypes = [P, I, I, I, P, P, P, P, P, P, P]
     lib.hs_accept_len.argtypes = [P, P, I, I, I, I, P, P, P, P, I, P, P]
     lib.hs_hedge_update.argtypes = [P, P, P, I, I, I, D, P]
     lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
@@ -81,7 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
-    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_eval_topl", "hs_accept_len", "hs_hedge_update",
+    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_eval_topl", "hs_play", "hs_regret_update",
+                 "hs_accept_len", "hs_hedge_update",
                  "hs_normalhedge_update", "hs_round", "hs_delayed_update", "hs_version"]:
         getattr(lib, name).restype = I
     _lib = lib
@@ -318,6 +322,40 @@ def delayed_update(state: DelayedState, gamma: torch.Tensor, count: torch.Tensor
         _ptr(st.w if hedge else None), eta, _ptr(st.R if normalhedge else None),
         _ptr(st.p if normalhedge else None), _ptr(st.c if normalhedge else None),
         _ptr(state.loss), _ptr(state.nloss), _stream(stream)))
+
+
+PLAY_ARGMAX, PLAY_SAMPLE = 0, 1
+
+
+def play(weights: torch.Tensor, how: int = PLAY_ARGMAX, u: Optional[torch.Tensor] = None,
+         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """hs_play: the drafter each query plays, from weights [B][N] fp64 (argmax, or an
+    inverse-CDF sample with the uniform draws u [B] fp64). Returns choice [B] int32."""
+    B, N = weights.shape
+    if out is None:
+        out = torch.empty((B,), dtype=torch.int32, device=weights.device)
+    _check(load_library().hs_play(_ptr(weights), B, N, how, _ptr(u), _ptr(out), _stream(stream)))
+    return out
+
+
+class RegretState:
+    """Device regret bookkeeping for B queries and N drafters (hs_regret_update)."""
+
+    def __init__(self, B: int, N: int, device):
+        self.cum = torch.zeros((B, N), dtype=torch.float64, device=device)
+        self.played = torch.zeros((B,), dtype=torch.float64, device=device)
+        self.regret = torch.zeros((B,), dtype=torch.float64, device=device)
+        self.eal_sum = torch.zeros((B,), dtype=torch.float64, device=device)
+
+    def update(self, loss: torch.Tensor, played: torch.Tensor, eal: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+        """loss [L][B][N] fp64, played [L][B] (or [B] for L = 1) int32."""
+        L, B, N = loss.shape
+        _check(load_library().hs_regret_update(
+            _ptr(loss), L, B, N, _ptr(played), _ptr(self.cum), _ptr(self.played),
+            _ptr(self.regret), _ptr(eal), _ptr(self.eal_sum if eal is not None else None),
+            _stream(stream)))
+        return self.regret
 
 
 class UpdateCadence:

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhedgespec.so")
-SOURCES = ["hs_api.hip", "hs_stats.hip", "hs_team.hip", "hs_tail.hip", "hs_delayed.hip", "hs_topl.hip"]
+SOURCES = ["hs_api.hip", "hs_stats.hip", "hs_team.hip", "hs_tail.hip", "hs_delayed.hip", "hs_topl.hip", "hs_play.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

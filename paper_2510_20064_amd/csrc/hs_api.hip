@@ -325,6 +325,34 @@ HS_API int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int
   return ok();
 }
 
+HS_API int hs_play(const double* weights, int B, int N, int how, const double* u,
+                   int32_t* choice, void* stream) {
+  int rc = check_shape(B, N, 1, 1);
+  if (rc) return rc;
+  if (how != HS_PLAY_ARGMAX && how != HS_PLAY_SAMPLE) return fail(HS_ERR_ARG, "unknown play rule %d", how);
+  if (!weights || !choice) return fail(HS_ERR_NULL, "weights and choice are required");
+  if (how == HS_PLAY_SAMPLE && !u) return fail(HS_ERR_NULL, "sampling needs the uniform draws u");
+  rc = hs::launch_play(weights, B, N, how, u, choice, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
+HS_API int hs_regret_update(const double* loss, int L, int B, int N, const int32_t* played,
+                            double* cum_loss, double* played_loss, double* regret,
+                            const double* eal, double* eal_sum, void* stream) {
+  int rc = check_shape(B, N, 1, 1);
+  if (rc) return rc;
+  if (L < 1) return fail(HS_ERR_SHAPE, "L must be >= 1");
+  if (!loss || !played || !cum_loss || !played_loss || !regret)
+    return fail(HS_ERR_NULL, "loss, played, cum_loss, played_loss and regret are required");
+  if ((eal == nullptr) != (eal_sum == nullptr))
+    return fail(HS_ERR_NULL, "eal and eal_sum must be given together");
+  rc = hs::launch_regret(loss, L, B, N, played, cum_loss, played_loss, regret, eal, eal_sum,
+                         (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
 HS_API int hs_accept_len(const float* alpha, const uint8_t* agree, int mode, int B, int N, int K,
                          const int32_t* parent_host, const int32_t* path_end, double* eal,
                          double* prefix, int loss_kind, double* loss, void* stream) {

@@ -275,6 +275,12 @@ size_t topl_ws_bytes(const TeamGeom& g, int L);
 bool topl_fits(const TeamGeom& g);  // work units and rows index with 31 bits
 int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool want_sum,
                 float* gamma, uint8_t* hit, int32_t* idx, char* ws, hipStream_t stream);
+// Drafter play and regret bookkeeping (hs_play.hip).
+int launch_play(const double* w, int B, int N, int how, const double* u, int32_t* choice,
+                hipStream_t stream);
+int launch_regret(const double* loss, int L, int B, int N, const int32_t* played, double* cum,
+                  double* played_sum, double* regret, const double* eal, double* eal_sum,
+                  hipStream_t stream);
 // Evaluation of one round: the team kernel (which also advances the workspace epoch) and, when
 // tail != nullptr, the learner step on its alpha or agreement.
 int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum, bool need_arg,

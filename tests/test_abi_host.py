@@ -204,3 +204,21 @@ def test_eval_topl_validation_codes():
     assert _topl(lib, ws=None) == 7
     assert _topl(lib, ws_bytes=1000) == 7
     assert _topl(lib, ws=FAKE * 16 + 8) == 4
+
+
+def test_play_and_regret_validation_codes():
+    lib = hs.load_library()
+    assert lib.hs_play(FAKE, 0, 8, 0, None, FAKE, None) == 2
+    assert lib.hs_play(FAKE, 4, 65, 0, None, FAKE, None) == 8
+    assert lib.hs_play(FAKE, 4, 8, 2, None, FAKE, None) == 10
+    assert lib.hs_play(None, 4, 8, 0, None, FAKE, None) == 1
+    assert lib.hs_play(FAKE, 4, 8, 1, None, FAKE, None) == 1  # sampling needs u
+    reg = lambda **kw: lib.hs_regret_update(*[kw.get(k, d) for k, d in (
+        ("loss", FAKE), ("L", 1), ("B", 4), ("N", 8), ("played", FAKE), ("cum", FAKE),
+        ("pl", FAKE), ("regret", FAKE), ("eal", None), ("eal_sum", None), ("s", None))])
+    assert reg(L=0) == 2
+    assert reg(B=0) == 2
+    assert reg(N=65) == 8
+    assert reg(played=None) == 1
+    assert reg(regret=None) == 1
+    assert reg(eal=FAKE) == 1
