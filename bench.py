@@ -106,6 +106,11 @@ def parse():
     ap.add_argument("--topl", type=int, default=0, metavar="L",
                     help="time hs_eval_topl (EAGLE's top-L acceptance mass, Theorem 2) with L "
                          "children per node on the workload instead")
+    ap.add_argument("--hybrid", type=int, default=0, metavar="H",
+                    help="with --delayed: the acceptance loss for each query's first H tokens")
+    ap.add_argument("--bookkeeping", action="store_true",
+                    help="time one round of drafter play (argmax of NormalHedge's p) and regret "
+                         "bookkeeping (hs_play + hs_regret_update) on the workload's B, N")
     ap.add_argument("--delayed", action="store_true",
                     help="time hs_delayed_update (token-level delayed feedback) on the workload's "
                          "B, N, K instead, K new tokens per query per round")
@@ -125,7 +130,8 @@ def bench_delayed(args, w, hs, torch, dev):
     stream = torch.cuda.Stream()
 
     def call(i):
-        hs.delayed_update(st, gam[i % copies], cnt, w.eta, stream=torch.cuda.current_stream())
+        hs.delayed_update(st, gam[i % copies], cnt, w.eta, hybrid_tokens=args.hybrid,
+                          stream=torch.cuda.current_stream())
 
     with torch.cuda.stream(stream):
         for i in range(copies):  # past the first K tokens: every later call completes K windows
@@ -158,12 +164,68 @@ def bench_delayed(args, w, hs, torch, dev):
             "steps": reps * copies, "warmup": max(1, args.warmup // copies) * copies,
             "us_per_call": us, "higher_is_better": True, "dtype": "f64", "data": "synthetic",
             "config": {"workload": w.name, "B": B, "N": N, "K": K, "eta": w.eta,
-                       "tokens_per_call": K, "hip_graph": True},
+                       "tokens_per_call": K, "hybrid_tokens": args.hybrid, "hip_graph": True},
             "roofline": {"bound": "latency", "achieved": nbytes / (us * 1e-6) / 1e9,
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                          "kernel": "hs_delayed_kernel (one wave per query, K sequential window "
                                    "updates each)", "bytes_per_call": nbytes}}
+    print(json.dumps(line), flush=True)
+
+
+def bench_bookkeeping(args, w, hs, torch, dev):
+    """One round of play and bookkeeping: hs_play (argmax of NormalHedge's p) and
+    hs_regret_update with the round's loss vector, in a HIP graph."""
+    B, N = w.B, w.N
+    copies = 16
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed)
+    p = torch.rand((B, N), generator=gen, device=dev, dtype=torch.float64)
+    loss = [torch.rand((1, B, N), generator=gen, device=dev, dtype=torch.float64)
+            for _ in range(copies)]
+    eal = torch.rand((B, N), generator=gen, device=dev, dtype=torch.float64) * (w.K + 1)
+    choice = torch.empty((B,), dtype=torch.int32, device=dev)
+    reg = hs.RegretState(B, N, dev)
+    stream = torch.cuda.Stream()
+
+    def call(i):
+        cs = torch.cuda.current_stream()
+        hs.play(p, hs.PLAY_ARGMAX, out=choice, stream=cs)
+        reg.update(loss[i % copies], choice.view(1, B), eal, stream=cs)
+
+    with torch.cuda.stream(stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // copies)
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup // copies)):
+            g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+    nbytes = B * N * 8 * 5 + B * 4 * 2 + B * 8 * 4  # p, loss, eal, cum in/out; choice; sums
+    line = {"metric": "drafter play and regret bookkeeping: rounds per second",
+            "value": 1.0 / (us * 1e-6), "unit": "rounds/s", "n_gpus": 1, "steps": reps * copies,
+            "warmup": max(1, args.warmup // copies) * copies, "us_per_call": us,
+            "higher_is_better": True, "dtype": "f64", "data": "synthetic",
+            "config": {"workload": w.name, "B": B, "N": N, "play": "argmax", "hip_graph": True},
+            "roofline": {"bound": "latency", "achieved": nbytes / (us * 1e-6) / 1e9,
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                         "kernel": "hs_play_kernel + hs_regret_kernel (one wave per query each)",
+                         "bytes_per_call": nbytes}}
     print(json.dumps(line), flush=True)
 
 
@@ -289,6 +351,9 @@ def main():
         return
     if args.topl:
         bench_topl(args, w, hs, torch, dev, np, synth)
+        return
+    if args.bookkeeping:
+        bench_bookkeeping(args, w, hs, torch, dev)
         return
 
     # ---- inputs: distinct rounds, resident in HBM -----------------------------------------

@@ -4,46 +4,58 @@
 //   hs_regret_kernel : Regret_T = sum_t f_t[i_t] - min_i sum_t f_t[i] (Section 3.1), and the
 //                      played drafter's expected accepted length summed over rounds.
 // Every sum whose value decides an integer or is compared with a reference runs left to right
-// in fp64 (the prefix sums of the sample in one lane, the cumulative losses per lane in loss
-// order), so it is reproducible bit for bit.
+// in fp64 (the total and prefix sums of the play over the drafters, the cumulative losses per
+// drafter in loss order), so it is reproducible bit for bit.
 #include "hs_internal.h"
 
 namespace hs {
 
 namespace {
 
+__device__ inline double lane_d(double x, int l) {
+  const uint64_t u = __double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | lo);
+}
+
+// One coalesced load of the query's weights (lane i: drafter i), then every lane walks them
+// left to right from broadcasts, so each lane forms the same fp64 sums in the order the
+// definition gives.
 __global__ __launch_bounds__(64) void hs_play_kernel(const double* w, int B, int N, int how,
                                                      const double* u, int32_t* choice) {
-  const int b = blockIdx.x;
-  if (threadIdx.x != 0) return;
-  const double* wb = w + (int64_t)b * N;
+  const int b = blockIdx.x, i = threadIdx.x;
+  const double wi = i < N ? w[(int64_t)b * N + i] : 0.0;
+  const double ub = how == HS_PLAY_SAMPLE ? u[b] : 0.0;
   double tot = 0.0;
-  for (int i = 0; i < N; ++i) tot += wb[i];
+  for (int j = 0; j < N; ++j) tot += lane_d(wi, j);
   int c = -1;
   if (tot > 0.0 && isfinite(tot)) {
     if (how == HS_PLAY_ARGMAX) {
       c = 0;
-      double best = wb[0];
-      for (int i = 1; i < N; ++i)
-        if (wb[i] > best) {  // strict: the lowest index of the largest weight
-          best = wb[i];
-          c = i;
+      double best = lane_d(wi, 0);
+      for (int j = 1; j < N; ++j) {
+        const double x = lane_d(wi, j);
+        if (x > best) {  // strict: the lowest index of the largest weight
+          best = x;
+          c = j;
         }
+      }
     } else {
       // inverse CDF: the smallest i whose prefix sum exceeds u * total
-      const double thr = u[b] * tot;
+      const double thr = ub * tot;
       double acc = 0.0;
       c = N - 1;  // rounding can leave the last prefix at or below thr
-      for (int i = 0; i < N; ++i) {
-        acc += wb[i];
+      for (int j = 0; j < N; ++j) {
+        acc += lane_d(wi, j);
         if (acc > thr) {
-          c = i;
+          c = j;
           break;
         }
       }
     }
   }
-  choice[b] = c;
+  if (i == 0) choice[b] = c;
 }
 
 __global__ __launch_bounds__(64) void hs_regret_kernel(const double* loss, int L, int B, int N,
