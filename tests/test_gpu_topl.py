@@ -155,3 +155,27 @@ def test_topl_candidate_list_overflow(L):
         note("candidate overflow L=%d dtype=%s" % (L, x.dtype))
         got = check(x, L, T=1.0)
         assert list(got["children"][0, 0, 0]) == list(range(L))
+
+
+def test_topl_merge_long_candidate_list():
+    # every slice holds the same 32 large values, so about 31 of each slice's 32 listed keys
+    # reach the merge's first threshold: some 500 candidates, searched bitwise in LDS
+    rng = np.random.default_rng(24)
+    V = 16 * 2048
+    z = rng.normal(0, 1, (2, 1, 1, V)).astype(np.float32)
+    for s in range(16):
+        z[1, 0, 0, s * 2048 + 64 * np.arange(32)] = 100.0 + np.arange(32)
+    x = _bf16(z)
+    note("merge long candidate list")
+    got = check(x, 32, T=1.0)
+    want = [s * 2048 + 64 * 31 for s in range(16)] + [s * 2048 + 64 * 30 for s in range(16)]
+    assert list(got["children"][0, 0, 0]) == want
+
+
+def test_topl_fp32_full_vocabulary():
+    w = synth.variant(WL["qwen3_8b_single"], K=2, N=3, dtype=synth.F32,
+                      scales=[0.4, 0.8, 1.6], permute=False)
+    note("fp32 V=151936, N=3, K=2, L=10 and 32")
+    x = synth.generate(w)
+    for L in (10, 32):
+        check(x, L, T=0.8)
