@@ -101,6 +101,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--greedy", action="store_true",
+                    help="evaluate in greedy argmax-agreement mode (the workload's second run)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--topl", type=int, default=0, metavar="L",
@@ -344,6 +346,8 @@ def main():
 
     hs.load_library()
     w = synth.workloads()[args.workload]
+    if args.greedy:
+        w = synth.variant(w, mode=synth.GREEDY)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.delayed:
@@ -436,7 +440,9 @@ def main():
 
     # ---- evaluation kernel alone, live, on the same stream --------------------------------
     ev_ws = [hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, dev)]
-    outs = [{"alpha": torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=dev)}]
+    greedy = w.mode == hs.GREEDY
+    outs = [{"agree": torch.empty((w.B, w.N, w.K), dtype=torch.uint8, device=dev)} if greedy else
+            {"alpha": torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=dev)}]
 
     def eval_fn(i):
         hs.eval_alpha(bufs[i % copies], V=w.V, temperature=w.temperature, mode=w.mode,
@@ -489,8 +495,8 @@ def main():
         n_done = 0
         while True:
             x = xs[n_done % len(xs)]
-            ref = oracle.evaluate(x, V=w.V, T=w.temperature)
-            gam = ref["alpha"].transpose(0, 2, 1)
+            ref = oracle.evaluate(x, V=w.V, T=w.temperature, want_alpha=not greedy)
+            gam = (ref["agree"].astype(np.float64) if greedy else ref["alpha"]).transpose(0, 2, 1)
             acc = oracle.accept_len(gam, parent=par, path_end=path_end, loss_kind=w.loss)
             wo = oracle.hedge(wo, acc["loss"], w.eta)
             Ro, po, _ = oracle.normalhedge(Ro, po, acc["loss"])
@@ -512,7 +518,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "N": w.N, "K": w.K, "V": w.V,
                    "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
-                   "temperature": w.temperature, "loss": "length",
+                   "temperature": w.temperature, "mode": "greedy" if greedy else "sample",
+                   "loss": ("length", "accept_token", "accept_chunk")[w.loss],
                    "learners": "hedge+normalhedge", "rotation_copies": copies,
                    "input_bytes_per_step": w.input_bytes, "hip_graph": use_graph,
                    "wall_s": round(wall, 4)},
