@@ -249,9 +249,9 @@ struct TeamLds {
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
   float o[2][D + 1];                          // slice offsets fl(m c)
   float no[2][D + 1];                         // -exp_offset(o): the addend of the exponents
-  float dl[D];                                // a_t - a_d, a_x = (o_x - hi_x) - lo_x
-  float G[D];                                 // 2^(a_t - a_d)
-  float F[D];                                 // 2^(a_d)
+  float nw[D];     // from the logits: -exp_offset(o_d) - (a_t - a_d), a_x = (o_x - hi_x) - lo_x
+  float G[D];      // kept e_v: 2^(a_t - a_d)
+  float F[D];      // factor of drafter d's group sum: 2^(a_d) (kept e_v), else 2^(a_t)
   uint32_t next;  // a row set of the team's coming items, posted by thread 0
   // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
   // chain of dependent scalar loads per item)
@@ -434,12 +434,14 @@ __device__ __forceinline__ void thread_sums(const TeamArgs& A, const ItemPos& q,
     float z[E];
     Vec<DT>::unpack(raw[r], z);
     const float no = sh.no[bf][r];
-    float a0 = 0.0f, a1 = 0.0f;
+    float v[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const float v = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, no));
-      if (e & 1) a1 += v;
-      else a0 += v;
+    for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, no));
+    float a0 = v[0], a1 = v[1];
+#pragma unroll
+    for (int e = 2; e < E; ++e) {
+      if (e & 1) a1 += v[e];
+      else a0 += v[e];
     }
     sh.xt[r][t] = a0 + a1;
   }
@@ -464,9 +466,9 @@ __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, u
 }
 
 // ---- 5. normalisers (wave 0; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
-// lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, a_t - a_r and 2^(a_r) to
-// LDS ----
-template <int D, typename L>
+// lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, the constants of its
+// min-sum to LDS: G and F = 2^(a_r) for kept e_v (6'), else the exponent addend and 2^(a_t) (6) ----
+template <int D, bool KEPT, typename L>
 __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
                                             L& sh, int bf, int lane) {
   float h = 0.0f;
@@ -478,9 +480,13 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
   const float at = lane_f(a, 0);
   if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
     const int d = (lane >> 1) - 1;
-    sh.dl[d] = at - a;
-    sh.G[d] = __builtin_amdgcn_exp2f(at - a);
-    sh.F[d] = __builtin_amdgcn_exp2f(a);
+    if (KEPT) {
+      sh.G[d] = __builtin_amdgcn_exp2f(at - a);
+      sh.F[d] = __builtin_amdgcn_exp2f(a);
+    } else {
+      sh.nw[d] = sh.no[bf][d + 1] - (at - a);
+      sh.F[d] = __builtin_amdgcn_exp2f(at);
+    }
   }
 }
 
@@ -498,10 +504,11 @@ __device__ __forceinline__ void thread_exps_kept(const TeamArgs& A, const ItemPo
     launder(raw[r]);
     Vec<DT>::unpack(raw[r], x[r]);
     const float no = sh.no[0][r];
-    float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, no));
+    for (int e = 0; e < E; ++e) x[r][e] = __builtin_amdgcn_exp2f(fmaf(x[r][e], A.c, no));
+    float a0 = x[r][0], a1 = x[r][1];
+#pragma unroll
+    for (int e = 2; e < E; ++e) {
       if (e & 1) a1 += x[r][e];
       else a0 += x[r][e];
     }
@@ -520,21 +527,25 @@ __device__ __forceinline__ void thread_minsums_kept(const ItemPos& q,
   for (int d = 0; d < D; ++d) {
     if (d >= q.n) continue;
     const float G = sh.G[d];
-    float a0 = 0.0f, a1 = 0.0f;
+    float y[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const float y = min_pos(x[0][e] * G, x[d + 1][e]);
-      if (e & 1) a1 += y;
-      else a0 += y;
+    for (int e = 0; e < E; ++e) y[e] = min_pos(x[0][e] * G, x[d + 1][e]);
+    float a0 = y[0], a1 = y[1];
+#pragma unroll
+    for (int e = 2; e < E; ++e) {
+      if (e & 1) a1 += y[e];
+      else a0 += y[e];
     }
     sh.xp[d][t] = a0 + a1;
   }
 }
 
 // ---- 6. per-thread min-sums, from the logits again: with u_v = z_t,v c - o_t and
-// w_v = z_d,v c - o_d (formed exactly as for the sums), p_v = 2^(u_v + a_t) and
-// q_v = 2^(w_v + a_d), so min(p_v, q_v) = 2^(a_d) 2^min(u_v + a_t - a_d, w_v); the factor
-// 2^(a_d) is applied to the group sum ----
+// w_v = z_d,v c - o_d, p_v = 2^(u_v + a_t) and q_v = 2^(w_v + a_d), so
+// min(p_v, q_v) = 2^(a_t) 2^min(u_v, w_v - (a_t - a_d)), and w_v - (a_t - a_d) is one fma
+// z_d,v c + nw_d; one fma, one min, one exp2 and one add per drafter logit. The factor 2^(a_t)
+// is applied to the group sum. Identical rows give nw_d = -o_t, so both operands agree
+// bitwise ----
 template <int DT, int D, typename L>
 __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos& q,
                                                typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
@@ -552,16 +563,21 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
     float w[E];
     launder(raw[d + 1]);
     Vec<DT>::unpack(raw[d + 1], w);
-    const float nd = sh.no[bf][d + 1];
-    const float dl = sh.dl[d];
-    float a0 = 0.0f, a1 = 0.0f;
+    const float nw = sh.nw[d];
+    float y[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      // both operands are results of arithmetic, so fminf needs no canonicalising; a NaN
-      // (-inf + inf when a whole slice is -inf) loses to the other operand, which is then -inf
-      const float y = __builtin_amdgcn_exp2f(fminf(u[e] + dl, fmaf(w[e], A.c, nd)));
-      if (e & 1) a1 += y;
-      else a0 += y;
+      // both operands are results of arithmetic, so fminf needs no canonicalising. A slice
+      // with no finite logit has every u_v (target) or w_v (drafter) at -inf; nw_d is then
+      // infinite or NaN, and where the other operand becomes NaN it loses to the -inf
+      y[e] = __builtin_amdgcn_exp2f(fminf(u[e], fmaf(w[e], A.c, nw)));
+    }
+    // two interleaved sums, started from the first terms (no additions of zero)
+    float a0 = y[0], a1 = y[1];
+#pragma unroll
+    for (int e = 2; e < E; ++e) {
+      if (e & 1) a1 += y[e];
+      else a0 += y[e];
     }
     sh.xp[d][t] = a0 + a1;
   }
@@ -827,7 +843,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
       __builtin_amdgcn_s_setprio(0);
       HS_STAMP(2);
-      if (wv == 0) await_norms<D>(A, q, tag, sh, 0, lane);
+      if (wv == 0) await_norms<D, true>(A, q, tag, sh, 0, lane);
       __syncthreads();
       HS_STAMP(3);
       thread_minsums_kept<DT, D>(q, x, sh, t);
@@ -875,7 +891,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       // alpha of the previous item, whose partials were stored an iteration ago
       if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv);
       if (set2 < nsets) post_set(j + 3);
-      if (wv == 0) await_norms<D>(A, q, tag, sh, bf, lane);
+      if (wv == 0) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
       HS_STAMP(3);
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
