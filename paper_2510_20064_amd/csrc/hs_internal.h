@@ -99,6 +99,27 @@ struct Vec<HS_BF16> {
   }
 };
 
+// Division of a 32-bit value by a divisor fixed for the launch, by a multiply-high and two
+// shifts (Granlund and Montgomery, "Division by invariant integers using multiplication",
+// 1994): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// q = (t + ((n - t) >> 1)) >> (l - 1), t = mulhi(m, n); d = 1 uses shifts 0 and 0.
+struct FastDiv {
+  uint32_t m, s1, s2;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while (l < 32 && ((uint64_t)1 << l) < d) ++l;
+  FastDiv f;
+  f.m = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1);
+  f.s1 = l > 0 ? 1 : 0;
+  f.s2 = l > 0 ? l - 1 : 0;
+  return f;
+}
+__device__ inline uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  const uint32_t t = __umulhi(f.m, n);
+  return (t + ((n - t) >> f.s1)) >> f.s2;
+}
+
 // The R = N + 1 logits rows of a (query, position) group: row 0 target, row 1 + i drafter i.
 struct RowTable {
   const void* ptr[kMaxRows];

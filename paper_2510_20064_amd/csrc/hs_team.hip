@@ -45,15 +45,25 @@ constexpr int kPollSleep = HS_POLL_SLEEP;  // s_sleep units (64 clocks) between 
 #endif
 
 struct TeamArgs {
-  RowTable rows;
+  // What every workgroup reads before its first loads comes first: the first 128 bytes of the
+  // kernel arguments, two scalar-cache lines, requested together at entry. The row table
+  // follows at the end.
+  int B, N, K, nsub, S, items;
+  int teams;         // workgroups of the launch / S
   // drafter rows at one constant distance (uni != 0): row bases from these scalars instead of
   // the row table, so the kernel does not wait for the table at its start
   int uni;
-  int64_t dd;  // bytes from drafter i's row (b, k) to drafter i + 1's
-  int B, N, K, nsub, S, items;
-  int64_t V, nvec;
-  float c;
+  FastDiv divS, divK;  // by S and K
+  int64_t V;
+  int64_t dd;          // bytes from drafter i's row (b, k) to drafter i + 1's
+  const void* base0;   // the target's rows (rows.ptr[0] and its strides)
+  const void* base1;   // drafter 0's rows (rows.ptr[1] and its strides)
+  int64_t sb0, sk0, sb1, sk1;
   uint32_t* epoch;     // advanced by the last workgroup to finish
+  // ---- 128 bytes ----
+  int64_t nvec;
+  float c;
+  FastDiv divNsub;     // by nsub
   uint64_t* fail;      // set, with the call's tag, by the first wait that gives up
   uint32_t* next_set;  // row sets claimed beyond each team's fixed ones
   uint32_t* finished;  // teams of this launch that have finished
@@ -74,6 +84,7 @@ struct TeamArgs {
 #ifdef HS_TRACE
   uint64_t* trace;  // [items][8] phase timestamps of workgroup thread 0
 #endif
+  RowTable rows;
 };
 
 #ifdef HS_TRACE
@@ -228,10 +239,10 @@ __device__ inline ItemPos item_pos(const TeamArgs& A, uint32_t set, int slot, in
     q.g = q.set;
     q.sub = 0;
   } else {
-    q.g = q.set / A.nsub;
+    q.g = (int)fdiv(set, A.divNsub);
     q.sub = q.set - q.g * A.nsub;
   }
-  q.b = q.g / A.K;
+  q.b = (int)fdiv((uint32_t)q.g, A.divK);
   q.k = q.g - q.b * A.K;
   q.n = min(D, A.N - q.sub * D);
   q.vi = q.s * kThreads + (int)threadIdx.x;
@@ -278,12 +289,12 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, 
   uint64_t rb[D + 1];
   if (UNI && A.uni) {
     // drafters at a constant distance: uniform scalar arithmetic
-    rb[0] = valid ? reinterpret_cast<uint64_t>(A.rows.ptr[0]) +
-                        (uint64_t)(((int64_t)q.b * A.rows.sb[0] + (int64_t)q.k * A.rows.sk[0]) *
+    rb[0] = valid ? reinterpret_cast<uint64_t>(A.base0) +
+                        (uint64_t)(((int64_t)q.b * A.sb0 + (int64_t)q.k * A.sk0) *
                                    Vt::kBytes)
                   : dummy;
-    const uint64_t d0 = reinterpret_cast<uint64_t>(A.rows.ptr[1]) +
-                        (uint64_t)(((int64_t)q.b * A.rows.sb[1] + (int64_t)q.k * A.rows.sk[1]) *
+    const uint64_t d0 = reinterpret_cast<uint64_t>(A.base1) +
+                        (uint64_t)(((int64_t)q.b * A.sb1 + (int64_t)q.k * A.sk1) *
                                    Vt::kBytes) +
                         (uint64_t)((int64_t)q.sub * D * A.dd);
 #pragma unroll
@@ -693,9 +704,15 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   const int gi = t >> 4, gl = t & 15;  // 16-lane group gi reduces row gi; gl: lane in it
   HS_STAMP_WG(0);
   const int S = A.S;
-  const int teams = gridDim.x / S;
-  const int T = blockIdx.x / S, slot = blockIdx.x - T * S;
-  const uint32_t nsets = (uint32_t)(A.items / S);
+  // every scalar the first loads depend on, requested in one round at entry (otherwise each
+  // is loaded just before its first use, one scalar-cache round trip apiece)
+  asm volatile("" ::"s"(A.N), "s"(A.K), "s"(A.nsub), "s"(A.S), "s"(A.items), "s"(A.teams),
+               "s"(A.uni), "s"(A.divS.m), "s"(A.divS.s1), "s"(A.divS.s2), "s"(A.divK.m),
+               "s"(A.divK.s1), "s"(A.divK.s2), "s"(A.V), "s"(A.dd), "s"(A.base0), "s"(A.base1),
+               "s"(A.sb0), "s"(A.sk0), "s"(A.sb1), "s"(A.sk1), "s"(A.epoch));
+  const int teams = A.teams;
+  const int T = (int)fdiv(blockIdx.x, A.divS), slot = blockIdx.x - T * S;
+  const uint32_t nsets = fdiv((uint32_t)A.items, A.divS);
   constexpr int kStatic = NEED_SUM ? 3 : 2;  // items per team with a fixed row set
   // slot 0 folds row 0 of every item, so it waits for the whole team each item: it can never
   // be more than one item ahead of any member, which keeps a ring of 4 mailbox words safe
@@ -961,6 +978,7 @@ int launch_t(TeamArgs A, const TeamGeom& g, hipStream_t stream, bool* learned) {
     if (!NS || need > sizeof(TeamLds<D, NA>)) A.learn = 0;
   }
   *learned = A.learn != 0;
+  A.teams = (int)teams;
   if (single) hs_team_kernel<DT, D, NS, NA, NS><<<(unsigned)P, kThreads, 0, stream>>>(A);
   else hs_team_kernel<DT, D, NS, NA, false><<<(unsigned)P, kThreads, 0, stream>>>(A);
 #ifdef HS_TRACE
@@ -1016,6 +1034,12 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   const TeamWs L = team_ws(g);
   TeamArgs A{};
   A.rows = rows;
+  A.base0 = rows.ptr[0];
+  A.base1 = rows.ptr[1];
+  A.sb0 = rows.sb[0];
+  A.sk0 = rows.sk[0];
+  A.sb1 = rows.sb[1];
+  A.sk1 = rows.sk[1];
   // drafters at one constant distance with equal strides (e.g. one [N][B][K][V] tensor)
   A.uni = 1;
   A.dd = g.N > 1 ? reinterpret_cast<const char*>(rows.ptr[2]) -
@@ -1031,6 +1055,9 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.K = g.K;
   A.nsub = g.nsub;
   A.S = g.S;
+  A.divS = make_fastdiv((uint32_t)g.S);
+  A.divNsub = make_fastdiv((uint32_t)g.nsub);
+  A.divK = make_fastdiv((uint32_t)g.K);
   A.items = (int)g.items;
   A.V = g.V;
   A.nvec = g.nvec;
