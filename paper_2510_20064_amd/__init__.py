@@ -24,6 +24,7 @@ SAMPLE, GREEDY = 0, 1
 LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
 MAX_DRAFTERS = 64
 MAX_POSITIONS = 64
+MAX_TOPL = 32  # HS_MAX_TOPL
 
 
 class HsError(RuntimeError):

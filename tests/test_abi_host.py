@@ -222,3 +222,18 @@ def test_play_and_regret_validation_codes():
     assert reg(played=None) == 1
     assert reg(regret=None) == 1
     assert reg(eal=FAKE) == 1
+
+
+def test_binding_constants_match_the_header():
+    import os
+    import re
+    head = open(os.path.join(os.path.dirname(__file__), "..", "include", "hedgespec.h")).read()
+    defs = {m.group(1): int(m.group(2)) for m in re.finditer(r"^#define (HS_\w+) (\d+)", head, re.M)}
+    pairs = {"HS_OK": hs.HS_OK, "HS_F32": hs.HS_F32, "HS_BF16": hs.HS_BF16,
+             "HS_SAMPLE": hs.SAMPLE, "HS_GREEDY": hs.GREEDY, "HS_LOSS_LENGTH": hs.LOSS_LENGTH,
+             "HS_LOSS_ACCEPT_TOKEN": hs.LOSS_ACCEPT_TOKEN,
+             "HS_LOSS_ACCEPT_CHUNK": hs.LOSS_ACCEPT_CHUNK, "HS_MAX_DRAFTERS": hs.MAX_DRAFTERS,
+             "HS_MAX_POSITIONS": hs.MAX_POSITIONS, "HS_MAX_TOPL": hs.MAX_TOPL,
+             "HS_PLAY_ARGMAX": hs.PLAY_ARGMAX, "HS_PLAY_SAMPLE": hs.PLAY_SAMPLE}
+    for name, value in pairs.items():
+        assert defs[name] == value, name

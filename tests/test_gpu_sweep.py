@@ -1,0 +1,121 @@
+"""GPU parity over a seeded sweep of shapes: hs_eval_alpha and hs_eval_topl against the oracle.
+
+Each case draws B, N, K, V, the dtype, the temperature and the mode from its seed, so that
+together the cases cross the launch geometry's edges:
+- one and several row sets per group (N up to 20, sets of at most 8 drafters);
+- one and several slices per row, with ragged tails (V not a multiple of the 2048-logit slice
+  or of the 16-byte vector);
+- teams that hold one item and teams that run several;
+- drafter rows at a constant distance and rows in separate allocations (the row table).
+Tolerances as in the other parity tests: indices bit-exact, alpha and gamma within 2e-5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2510_20064_amd as hs
+import synth
+
+pytestmark = pytest.mark.gpu
+
+ALPHA_TOL = 2e-5
+BASE = synth.workloads()["qwen3_8b_single"]
+
+
+def note(msg):
+    print("\n[case] " + msg, flush=True)
+
+
+def draw(seed):
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.integers(1, 5))
+    N = int(rng.integers(1, 21))
+    K = int(rng.integers(1, 6))
+    V = int(rng.choice([1, 7, 2048, 2049, 4095, int(rng.integers(8, 30000))]))
+    dtype = int(rng.choice([synth.F32, synth.BF16]))
+    step = 8 if dtype == synth.BF16 else 4  # 16-byte row starts
+    ld = (V + step - 1) // step * step + step * int(rng.integers(0, 2))
+    T = float(rng.choice([0.4, 1.0, 3.0]))
+    mode = int(rng.choice([hs.SAMPLE, hs.GREEDY]))
+    scattered = bool(seed % 3 == 2)
+    w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=ld, dtype=dtype,
+                      scales=[0.2 + 0.3 * i for i in range(N)], permute=True, seed=seed,
+                      nboost=min(BASE.nboost, V // 4))
+    return w, T, mode, scattered
+
+
+def to_dev(w, x):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if w.dtype == synth.BF16:
+        t = t.view(torch.bfloat16)
+    return t.cuda()
+
+
+def split(xd, scattered):
+    """The target and the list of drafter tensors; when scattered, each drafter is a copy in
+    an allocation of its own, with allocations of uneven size between them."""
+    if not scattered:
+        return xd[0], list(xd[1:])
+    keep, ds = [], []
+    for i in range(1, xd.shape[0]):
+        keep.append(torch.empty(4096 + 53 * i, dtype=torch.uint8, device="cuda"))
+        ds.append(xd[i].clone())
+    return xd[0], ds
+
+
+# Many row sets over few slices, so that each team runs several items (the pipelined kernel
+# with dynamically claimed row sets): (B, N, K, V, dtype, mode, scattered).
+MANY = [(64, 12, 6, 4099, synth.BF16, hs.SAMPLE, False),
+        (64, 5, 8, 2056, synth.F32, hs.GREEDY, True),
+        (40, 9, 4, 6001, synth.BF16, hs.SAMPLE, True)]
+
+
+def many(i):
+    B, N, K, V, dtype, mode, scattered = MANY[i]
+    step = 8 if dtype == synth.BF16 else 4
+    w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=(V + step - 1) // step * step, dtype=dtype,
+                      scales=[0.2 + 0.3 * j for j in range(N)], permute=True, seed=50 + i)
+    return w, 0.8, mode, scattered
+
+
+@pytest.mark.parametrize("seed", range(16 + len(MANY)))
+def test_eval_alpha_sweep(seed):
+    w, T, mode, scattered = draw(seed) if seed < 16 else many(seed - 16)
+    note("alpha seed=%d B=%d N=%d K=%d V=%d ld=%d dtype=%d T=%g mode=%d scattered=%d"
+         % (seed, w.B, w.N, w.K, w.V, w.row_ld, w.dtype, T, mode, scattered))
+    x = synth.generate(w)
+    t, ds = split(to_dev(w, x), scattered)
+    out = hs.eval_alpha(t, ds, V=w.V, temperature=T, mode=mode, want_alpha=(mode == hs.SAMPLE),
+                        want_agree=True, want_argmax=True)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.evaluate(x, V=w.V, T=T, want_alpha=(mode == hs.SAMPLE))
+    if mode == hs.SAMPLE:
+        err = np.abs(got["alpha"] - ref["alpha"].transpose(0, 2, 1)).max()
+        assert err <= ALPHA_TOL, err
+    assert np.array_equal(got["agree"], ref["agree"].transpose(0, 2, 1))
+    assert np.array_equal(got["argmax_t"], ref["argmax"][:, :, 0])
+    assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_eval_topl_sweep(seed):
+    w, T, mode, _ = draw(100 + seed)
+    L = int(np.random.default_rng(seed).integers(1, min(w.V, hs.MAX_TOPL) + 1))
+    note("topl seed=%d B=%d N=%d K=%d V=%d ld=%d dtype=%d T=%g mode=%d L=%d"
+         % (seed, w.B, w.N, w.K, w.V, w.row_ld, w.dtype, T, mode, L))
+    x = synth.generate(w)
+    out = hs.eval_topl(to_dev(w, x), L=L, V=w.V, temperature=T, mode=mode,
+                       want_gamma=(mode == hs.SAMPLE), want_hit=True, want_children=True)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.topl(x.reshape(x.shape[0], w.B * w.K, -1), L, V=w.V, T=T,
+                      want_mass=(mode == hs.SAMPLE))
+    for b in range(w.B):
+        for k in range(w.K):
+            g = b * w.K + k
+            assert np.array_equal(got["children"][b, :, k], ref["idx"][g]), (b, k)
+            assert np.array_equal(got["hit"][b, :, k], ref["hit"][g]), (b, k)
+            if mode == hs.SAMPLE:
+                assert np.abs(got["gamma"][b, :, k] - ref["gamma"][g]).max() <= ALPHA_TOL, (b, k)
