@@ -299,11 +299,12 @@ int hs_regret_update(const double* loss, int L, int B, int N, const int32_t* pla
                      double* eal_sum, void* stream);
 
 /*
- * hs_round - one verification round of the whole path, enqueued as two launches
- * (the evaluation; then, per query, the learner step on its alpha or agreement): the
- * work of hs_eval_alpha, then per query hs_accept_len's work, the loss, and the
- * Hedge and NormalHedge updates with that loss (same workspace contract as
- * hs_eval_alpha). Arguments mean what they mean in the calls above. Learner
+ * hs_round - one verification round of the whole path: the work of hs_eval_alpha,
+ * then per query hs_accept_len's work, the loss, and the Hedge and NormalHedge
+ * updates with that loss (same workspace contract as hs_eval_alpha). In sample mode
+ * the learner step runs inside the evaluation launch when its LDS (gamma, losses and
+ * scratch of one query) fits in the evaluation kernel's: one launch. Otherwise, and
+ * in greedy mode, it is a second launch, one wave per query. Arguments mean what they mean in the calls above. Learner
  * state pointers may be NULL to skip that learner (logw and w together; R, p
  * and c together). eal is required; alpha/agree as hs_eval_alpha requires them for `mode`.
  */
