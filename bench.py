@@ -4,7 +4,8 @@
 A step is one verification round of the whole path on one batch of synthetic logits:
 temperature softmax statistics, alpha = sum min(p, q_i) for every drafter and position,
 Theorem 3's expected acceptance length, the length loss, and the Hedge and NormalHedge
-updates (hs_round: the evaluation kernel, the fold into alpha, then the learner kernel).
+updates (hs_round: one launch of the evaluation kernel, which folds the slice sums into alpha
+and runs each query's learner step once its alpha is complete).
 
 Workload: the Qwen3-8B-shaped single query (B=1 query, N=8 drafters, K=8 positions,
 V=151936, bf16 logits, T=1). Inputs are resident in HBM before timing starts; successive
@@ -12,8 +13,8 @@ steps rotate through >= 512 MB of distinct rounds so that the 256 MB Infinity Ca
 serve them. Steps are captured in a HIP graph (the path is launch-bound at this size).
 
 Prints one JSON line (rank 0). `value` = drafter-positions evaluated per second (B*N*K per
-step). `roofline` prices one hs_eval_alpha call (the team kernel and the fold of its slice
-sums, timed together with HIP events on the stream they run on) against HBM bandwidth with
+step). `roofline` prices one hs_eval_alpha call (one launch of the team kernel, timed with
+HIP events on the stream it runs on) against HBM bandwidth with
 algorithmic bytes (every logit read once); `traffic` is the counter-measured HBM bytes of that
 call from the committed FETCH_SIZE / WRITE_SIZE summary, null if the kernel sources changed
 since it was taken. `cpu_baseline` times the float64 oracle on the host.

@@ -1,5 +1,6 @@
-// Drafter evaluation with one read of every logit: softmax statistics, alpha =
-// sum_v min(p, q_i) for every drafter (Theorem 1), greedy argmax and agreement.
+// Drafter evaluation with one read of every logit, in one launch: softmax statistics,
+// alpha = sum_v min(p, q_i) for every drafter (Theorem 1), greedy argmax and agreement, and
+// for hs_round the learner step.
 //
 // min(p_v, q_v) needs both rows' normalisers, which depend on the whole row, so the
 // slices of a row have to meet before any min can be taken. Here they meet on chip: a
@@ -8,24 +9,24 @@
 // 256-thread workgroup (thread t owns vector t of every row). The S items of a row set form
 // a team that is resident at the same time:
 //   1. every item reduces its rows (max, lowest argmax, exp2 sum against the slice offset
-//      o = fl(m c), c = log2(e) / T) and publishes them; it keeps e_v = exp2(z_v c - o);
+//      o = fl(m c), c = log2(e) / T) and publishes them as tagged words;
 //   2. item s folds the S slice statistics of row s (rows s, s + S, ... when S is smaller
 //      than the row count) into the row's log2 normaliser L = hi + lo and publishes it;
-//   3. every item reads the normalisers and takes, per drafter,
-//      sum_v min(p_v, q_v) = F_d sum_v min(e_t,v G, e_d,v), with a_x = o_x - L_x,
-//      F_d = 2^(a_d) and G = 2^(a_t - a_d): one multiply, one min and one add per drafter
-//      logit, no second exponential;
-//   4. a second launch sums each drafter's S slice partials in slice order into alpha.
+//   3. every item reads the normalisers and forms its slice's part of sum_v min(p_v, q_v)
+//      for each drafter: from the e_v kept in registers when the workgroup holds one item
+//      (one multiply, one min and one add per drafter logit), else from the logits again
+//      (one fma, one min, one exp2 and one add); the partials are published;
+//   4. slot d mod S sums drafter d's S slice partials in slice order into alpha.
 // Within a workgroup every reduction over the slice goes through LDS: each thread stores its
 // per-row value, then one 16-lane group per row reduces the row's 256 values and the result
 // is known to the whole group, so no wave reduces all rows on its own.
-// The loads of an item's successor are issued right after its logits are unpacked, so HBM
-// stays busy while the team reduces and exchanges.
+// A workgroup with several items overlaps them: while item j's normalisers are exchanged it
+// runs the statistics of item j + 1, and the loads of item j + 2 are in flight.
 //
 // The grid holds as many teams as the device keeps resident at once, so all members of a
 // team run together and waiting on one cannot deadlock. Words crossing workgroups carry the
-// call's epoch as tag; the fold launch advances the epoch. Every wait is bounded: a word that
-// never arrives yields NaN (argmax -2), no hang.
+// call's tag; the last team to finish advances the epoch the tag derives from. Every wait is
+// bounded: a word that never arrives yields NaN (argmax -2), no hang.
 #include <algorithm>
 #include <atomic>
 #include <cstdio>
