@@ -84,6 +84,9 @@ def test_eval_alpha_validation_codes():
     bad[3] = hs.hs_view(None, 0, 0)
     assert _eval(lib, drafters=bad) == 1
     assert b"drafter 3" in lib.hs_last_error()
+    # 512 slices of 256 16-byte vectors per row at most: V = 2^20 bf16 or 2^19 fp32
+    assert _eval(lib, V=(1 << 20) + 1) == 8
+    assert _eval(lib, V=(1 << 19) + 1, dtype=0) == 8
 
 
 def test_accept_len_validation_codes():

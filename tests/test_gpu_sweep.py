@@ -119,3 +119,30 @@ def test_eval_topl_sweep(seed):
             assert np.array_equal(got["hit"][b, :, k], ref["hit"][g]), (b, k)
             if mode == hs.SAMPLE:
                 assert np.abs(got["gamma"][b, :, k] - ref["gamma"][g]).max() <= ALPHA_TOL, (b, k)
+
+
+# The largest rows the evaluation takes (512 slices: V = 2^20 bf16, 2^19 fp32): one item per
+# team, and one team of 512 workgroups running several items with claimed row sets.
+LIMIT = [(1, 3, 1, 1 << 20, synth.BF16, hs.SAMPLE),
+         (2, 3, 2, 1 << 20, synth.BF16, hs.SAMPLE),
+         (1, 9, 2, 1 << 19, synth.F32, hs.GREEDY)]
+
+
+@pytest.mark.parametrize("case", range(len(LIMIT)))
+def test_eval_alpha_at_the_vocabulary_limit(case):
+    B, N, K, V, dtype, mode = LIMIT[case]
+    note("alpha at the limit B=%d N=%d K=%d V=%d dtype=%d mode=%d" % (B, N, K, V, dtype, mode))
+    w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=V, dtype=dtype,
+                      scales=[0.2 + 0.3 * j for j in range(N)], permute=False, seed=70 + case)
+    x = synth.generate(w)
+    xd = to_dev(w, x)
+    out = hs.eval_alpha(xd[0], list(xd[1:]), V=V, temperature=1.0, mode=mode,
+                        want_alpha=(mode == hs.SAMPLE), want_agree=True, want_argmax=True)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.evaluate(x, V=V, T=1.0, want_alpha=(mode == hs.SAMPLE))
+    if mode == hs.SAMPLE:
+        assert np.abs(got["alpha"] - ref["alpha"].transpose(0, 2, 1)).max() <= ALPHA_TOL
+    assert np.array_equal(got["agree"], ref["agree"].transpose(0, 2, 1))
+    assert np.array_equal(got["argmax_t"], ref["argmax"][:, :, 0])
+    assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
