@@ -86,10 +86,12 @@ void or_row_stats(const void* row, int dtype, int64_t V, double T, double* max_o
  * Acceptance probability of speculative sampling (Theorem 1, Leviathan et al.
  * Thm 3.5, restated in Section 2.2): alpha = sum_v min(p(v), q(v)) = 1 - TV(p, q),
  * with p = softmax(z_t / T) and q = softmax(z_i / T). Clamped to [0, 1].
- * lse_t / lse_i are the row log-normalisers from or_row_stats.
+ * lse_t / lse_i are the row log-normalisers from or_row_stats. Theorem 1 takes two
+ * distributions: a row with no finite logit has none (lse = NaN), and alpha is NaN.
  */
 double or_alpha(const void* zt, const void* zi, int dtype, int64_t V, double T, double lse_t,
                 double lse_i) {
+  if (isnan(lse_t) || isnan(lse_i)) return NAN;
   double a = 0.0;
   for (int64_t v = 0; v < V; ++v) {
     double p = exp(or_decode(zt, dtype, v) / T - lse_t);

@@ -479,7 +479,10 @@ __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, u
 
 // ---- 5. normalisers (wave 0; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
 // lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, the constants of its
-// min-sum to LDS: G and F = 2^(a_r) for kept e_v (6'), else the exponent addend and 2^(a_t) (6) ----
+// min-sum to LDS: G and F = 2^(a_r) for kept e_v (6'), else the exponent addend and 2^(a_t) (6).
+// A row with no finite logit folds to hi = -inf, lo = NaN, so its a is NaN: it has no
+// distribution, and F is NaN whenever a_t or a_d is, which makes that drafter's alpha NaN in
+// either form ----
 template <int D, bool KEPT, typename L>
 __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
                                             L& sh, int bf, int lane) {
@@ -492,12 +495,13 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
   const float at = lane_f(a, 0);
   if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
     const int d = (lane >> 1) - 1;
+    const bool undefined = at != at || a != a;
     if (KEPT) {
       sh.G[d] = __builtin_amdgcn_exp2f(at - a);
-      sh.F[d] = __builtin_amdgcn_exp2f(a);
+      sh.F[d] = undefined ? NAN : __builtin_amdgcn_exp2f(a);
     } else {
       sh.nw[d] = sh.no[bf][d + 1] - (at - a);
-      sh.F[d] = __builtin_amdgcn_exp2f(at);
+      sh.F[d] = undefined ? NAN : __builtin_amdgcn_exp2f(at);
     }
   }
 }

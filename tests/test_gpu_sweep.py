@@ -146,3 +146,50 @@ def test_eval_alpha_at_the_vocabulary_limit(case):
     assert np.array_equal(got["agree"], ref["agree"].transpose(0, 2, 1))
     assert np.array_equal(got["argmax_t"], ref["argmax"][:, :, 0])
     assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
+
+
+def _dead_rows_case(B, N, K, V, dtype, dead):
+    """Logits with whole rows at -inf: dead = list of (row, b, k), row 0 the target."""
+    step = 8 if dtype == synth.BF16 else 4
+    w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=(V + step - 1) // step * step, dtype=dtype,
+                      scales=[0.3 + 0.4 * j for j in range(N)], permute=False, seed=90)
+    x = synth.generate(w)
+    ninf = np.uint16(0xFF80) if dtype == synth.BF16 else np.float32(-np.inf)
+    for r, b, k in dead:
+        x[r, b, k, :V] = ninf
+    return w, x
+
+
+@pytest.mark.parametrize("shape", ["one item per team", "several items per team"])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype):
+    # Theorem 1 needs two distributions: a row of -inf logits has none, so alpha is NaN for
+    # every drafter when the target's row is dead and for the dead drafter alone otherwise;
+    # agreement and argmax keep their rule (lowest index of the max).
+    if shape == "one item per team":
+        B, N, K, V = 1, 3, 3, 5000
+        dead = [(0, 0, 0), (2, 0, 1)]
+    else:
+        B, N, K, V = 64, 3, 8, 2056
+        dead = [(0, 5, 3), (1, 17, 0), (3, 40, 7), (0, 63, 7), (2, 63, 7)]
+    note("dead rows: %s dtype=%d" % (shape, dtype))
+    w, x = _dead_rows_case(B, N, K, V, dtype, dead)
+    out = hs.eval_alpha(to_dev(w, x)[0], list(to_dev(w, x)[1:]), V=V, temperature=1.0,
+                        mode=hs.SAMPLE, want_alpha=True, want_agree=True, want_argmax=True)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.evaluate(x, V=V, T=1.0, want_alpha=True)
+    ra = ref["alpha"].transpose(0, 2, 1)
+    nan = np.isnan(ra)
+    want = np.zeros((B, N, K), bool)  # [B][N][K]: the pairs with a dead row
+    for r, b, k in dead:
+        if r == 0:
+            want[b, :, k] = True
+        else:
+            want[b, r - 1, k] = True
+    assert np.array_equal(nan, want)
+    assert np.array_equal(np.isnan(got["alpha"]), nan)
+    assert np.abs(got["alpha"][~nan] - ra[~nan]).max() <= ALPHA_TOL
+    assert np.array_equal(got["agree"], ref["agree"].transpose(0, 2, 1))
+    assert np.array_equal(got["argmax_t"], ref["argmax"][:, :, 0])
+    assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))

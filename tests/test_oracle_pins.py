@@ -58,6 +58,24 @@ def test_alpha_disjoint_supports_is_exactly_zero():
     assert oracle.alpha_pair(zt, zi, 1.0) == 0.0
 
 
+def test_alpha_of_a_row_without_a_distribution_is_nan():
+    # Theorem 1 takes two distributions; a row of -inf logits has no softmax. Either side
+    # degenerate gives NaN, and the same row in a pair with itself too. The argmax of such a
+    # row is the lowest index (all entries attain the max), and its normaliser is NaN.
+    rng = np.random.default_rng(21)
+    V = 3000
+    z = rng.normal(0, 1, V).astype(np.float32)
+    dead = np.full(V, -np.inf, np.float32)
+    assert math.isnan(oracle.alpha_pair(dead, z, 1.0))
+    assert math.isnan(oracle.alpha_pair(z, dead, 1.0))
+    assert math.isnan(oracle.alpha_pair(dead, dead, 1.0))
+    assert oracle.alpha_pair(z, z, 1.0) == pytest.approx(1.0, abs=1e-12)
+    x = np.stack([z, dead, z])[:, None, None, :]  # target, a dead drafter, a copy
+    ref = oracle.evaluate(x, V=V, T=1.0, want_alpha=True)
+    assert math.isnan(ref["alpha"][0, 0, 0]) and ref["alpha"][0, 0, 1] == pytest.approx(1.0)
+    assert ref["argmax"][0, 0, 1] == 0
+
+
 @pytest.mark.parametrize("T", [1.0, 0.5, 3.0])
 def test_alpha_symmetric_bounded_and_equals_one_minus_tv(T):
     rng = np.random.default_rng(3)
