@@ -108,7 +108,7 @@ size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
  *   alpha[b][i][k] = sum_v min(p(v), q_i(v)) = 1 - TV(p, q_i)      (Theorem 1)
  *     with p = softmax(target[b][k] / T), q_i = softmax(drafter_i[b][k] / T),
  *     accumulated in fp32 and clamped to [0, 1]; NaN when either row has no finite
- *     logit (it defines no distribution);
+ *     logit or holds a NaN logit (it defines no distribution);
  *   agree[b][i][k]  = 1 if argmax target[b][k] == argmax drafter_i[b][k] else 0;
  *   argmax_t[b][k], argmax_d[b][i][k] = lowest index of the row maximum (raw logits).
  * target       : host pointer to one view; drafters_host: host array of N views.

@@ -148,32 +148,39 @@ def test_eval_alpha_at_the_vocabulary_limit(case):
     assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
 
 
-def _dead_rows_case(B, N, K, V, dtype, dead):
-    """Logits with whole rows at -inf: dead = list of (row, b, k), row 0 the target."""
+def _dead_rows_case(B, N, K, V, dtype, dead, nan_logit=False):
+    """Logits with whole rows at -inf (or, nan_logit, one NaN logit in each such row plus a
+    large logit elsewhere): dead = list of (row, b, k), row 0 the target."""
     step = 8 if dtype == synth.BF16 else 4
     w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=(V + step - 1) // step * step, dtype=dtype,
                       scales=[0.3 + 0.4 * j for j in range(N)], permute=False, seed=90)
     x = synth.generate(w)
-    ninf = np.uint16(0xFF80) if dtype == synth.BF16 else np.float32(-np.inf)
-    for r, b, k in dead:
-        x[r, b, k, :V] = ninf
+    bf = dtype == synth.BF16
+    for j, (r, b, k) in enumerate(dead):
+        if nan_logit:
+            x[r, b, k, (37 * j + 11) % V] = np.uint16(0x7FC0) if bf else np.float32(np.nan)
+            x[r, b, k, (53 * j + 5) % V] = np.uint16(0x4248) if bf else np.float32(50.0)
+        else:
+            x[r, b, k, :V] = np.uint16(0xFF80) if bf else np.float32(-np.inf)
     return w, x
 
 
+@pytest.mark.parametrize("nan_logit", [False, True])
 @pytest.mark.parametrize("shape", ["one item per team", "several items per team"])
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
-def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype):
-    # Theorem 1 needs two distributions: a row of -inf logits has none, so alpha is NaN for
-    # every drafter when the target's row is dead and for the dead drafter alone otherwise;
-    # agreement and argmax keep their rule (lowest index of the max).
+def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype, nan_logit):
+    # Theorem 1 needs two distributions: a row of -inf logits has none, and neither has a row
+    # holding a NaN logit. Alpha is NaN for every drafter when the target's row is such a row
+    # and for that drafter alone otherwise; agreement and argmax keep their rule (lowest index
+    # of the max, a NaN never being larger).
     if shape == "one item per team":
         B, N, K, V = 1, 3, 3, 5000
         dead = [(0, 0, 0), (2, 0, 1)]
     else:
         B, N, K, V = 64, 3, 8, 2056
         dead = [(0, 5, 3), (1, 17, 0), (3, 40, 7), (0, 63, 7), (2, 63, 7)]
-    note("dead rows: %s dtype=%d" % (shape, dtype))
-    w, x = _dead_rows_case(B, N, K, V, dtype, dead)
+    note("dead rows: %s dtype=%d nan_logit=%d" % (shape, dtype, nan_logit))
+    w, x = _dead_rows_case(B, N, K, V, dtype, dead, nan_logit)
     out = hs.eval_alpha(to_dev(w, x)[0], list(to_dev(w, x)[1:]), V=V, temperature=1.0,
                         mode=hs.SAMPLE, want_alpha=True, want_agree=True, want_argmax=True)
     torch.cuda.synchronize()
