@@ -151,6 +151,8 @@ size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dt
  *   hit[b][i][k]      = 1 if the target's argmax (lowest index of its row maximum) is in
  *                       Top_L, else 0: gamma of greedy decoding (one-hot p).
  *   children[b][i][k] = Top_L in rank order, L int32 token indices.
+ * A drafter row holding a NaN logit has no ranking: its children, hit and gamma are
+ * unspecified. A target row holding one gives gamma = NaN.
  * target, drafters_host, N, B, K, V, dtype: as in hs_eval_alpha (K positions or tree nodes).
  * L            : children per node, 1 <= L <= min(V, HS_MAX_TOPL) (EAGLE's default is 10).
  * gamma        : [B][N][K] fp32 or NULL. Needs T finite and > 0 when non-NULL.
