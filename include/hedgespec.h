@@ -147,7 +147,7 @@ size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dt
  *   gamma[b][i][k] = sum_{v in Top_L(drafter_i[b][k])} p(v),  p = softmax(target[b][k] / T),
  * accumulated in fp32 and clamped to [0, 1]. The ranking is that of the raw drafter logits
  * (a softmax at any temperature keeps it); equal logits rank lower token index first, and
- * -0 ranks as +0. Logits must not be NaN.
+ * -0 ranks as +0.
  *   hit[b][i][k]      = 1 if the target's argmax (lowest index of its row maximum) is in
  *                       Top_L, else 0: gamma of greedy decoding (one-hot p).
  *   children[b][i][k] = Top_L in rank order, L int32 token indices.
