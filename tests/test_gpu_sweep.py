@@ -23,6 +23,14 @@ ALPHA_TOL = 2e-5
 BASE = synth.workloads()["qwen3_8b_single"]
 
 
+def _bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even bf16 bit patterns of fp32 values (NaN stays a NaN pattern)."""
+    u = np.asarray(a, np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    r[np.isnan(a)] = 0x7FC0
+    return r
+
+
 def note(msg):
     print("\n[case] " + msg, flush=True)
 
@@ -200,3 +208,32 @@ def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype, nan_logit):
     assert np.array_equal(got["agree"], ref["agree"].transpose(0, 2, 1))
     assert np.array_equal(got["argmax_t"], ref["argmax"][:, :, 0])
     assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_softmax_stats_of_rows_without_a_distribution(dtype):
+    # hs_softmax_stats on rows of -inf and rows holding a NaN: the normaliser is NaN, the max
+    # and argmax skip the NaN (an all -inf row has max -inf at index 0); the other rows as usual
+    note("softmax stats, dead and NaN rows, dtype=%d" % dtype)
+    V, rows = 9001, 6
+    ld = (V + 7) // 8 * 8
+    rng = np.random.default_rng(5)
+    z = rng.normal(0, 2, (rows, ld)).astype(np.float32)
+    z[:, V:] = 0.0
+    z[1, :V] = -np.inf
+    z[3, 4000] = np.nan
+    z[3, 77] = 30.0
+    z[4, [0, 8999]] = np.nan
+    x = _bf16_bits(z) if dtype == synth.BF16 else z
+    t = torch.from_numpy(x)
+    t = (t.view(torch.bfloat16) if dtype == synth.BF16 else t).cuda()
+    for T in (1.0, 0.6):
+        mx, lse, am = hs.softmax_stats(t, V=V, temperature=T)
+        torch.cuda.synchronize()
+        rm, ra, rl = oracle.softmax_stats(x, V=V, T=T)
+        assert np.array_equal(am.cpu().numpy(), ra)
+        assert np.array_equal(mx.cpu().numpy().astype(np.float64), rm)
+        got = lse.cpu().numpy()
+        assert np.array_equal(np.isnan(got), np.isnan(rl)) and np.isnan(rl[[1, 3, 4]]).all()
+        ok = ~np.isnan(rl)
+        assert np.allclose(got[ok], rl[ok], rtol=2e-6, atol=1e-5)
