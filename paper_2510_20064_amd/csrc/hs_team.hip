@@ -9,7 +9,7 @@
 // 256-thread workgroup (thread t owns vector t of every row). The S items of a row set form
 // a team that is resident at the same time:
 //   1. every item reduces its rows (max, lowest argmax, exp2 sum against the slice offset
-//      o = fl(m c), c = log2(e) / T) and publishes them as tagged words;
+//      o = ceil(m c), c = log2(e) / T, an integer) and publishes them as tagged words;
 //   2. item s folds the S slice statistics of row s (rows s, s + S, ... when S is smaller
 //      than the row count) into the row's log2 normaliser L = hi + lo and publishes it;
 //   3. every item reads the normalisers and forms its slice's part of sum_v min(p_v, q_v)
@@ -191,7 +191,7 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
         }
         if (NEED_SUM) {
           if ((uint32_t)w[h][1] != tag) w[h][1] = await_word(base + 3 * j + 1, tag, A.fail);
-          lse2_combine(o, sum, ms * A.c, word_f(w[h][1]));
+          lse2_combine(o, sum, ceilf(ms * A.c), word_f(w[h][1]));
         }
       }
     }
@@ -254,12 +254,14 @@ __device__ inline ItemPos item_pos(const TeamArgs& A, uint32_t set, int slot, in
 // so that one 16-lane group reduces one row (group_read) instead of every wave reducing every
 // row on its own. Slice offsets are double-buffered by item parity: an item's min-sum runs
 // after the statistics of its successor.
-template <int D, bool NEED_ARG>
+template <int D, bool NEED_ARG, bool PT = false>
 struct TeamLds {
   float xt[D + 1][kThreads];                  // per-thread max keys / maxima, then exp2 sums
   int xi[NEED_ARG ? D + 1 : 1][kThreads];     // per-thread argmax
+  float xs[PT ? D + 1 : 1][kThreads];         // per-thread exp2 sums against the thread's offset
+  int xo[PT ? D + 1 : 1][kThreads];           // that offset (an integer)
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
-  float o[2][D + 1];                          // slice offsets fl(m c)
+  float o[2][D + 1];                          // slice offsets ceil(m c)
   float no[2][D + 1];                         // -exp_offset(o): the addend of the exponents
   float nw[D];     // from the logits: -exp_offset(o_d) - (a_t - a_d), a_x = (o_x - hi_x) - lo_x
   float G[D];      // kept e_v: 2^(a_t - a_d)
@@ -347,8 +349,9 @@ __device__ __forceinline__ void mask_tail(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// The offset a slice is exponentiated against: fl(m c) for a slice whose max m is finite,
-// 0 for a slice with no finite logit (every e_v is then exp2(-inf) = 0).
+// The offset a slice is exponentiated against: ceil(m c) for a slice whose max m is finite (an
+// integer, so that sums against different offsets rescale exactly), 0 for a slice with no
+// finite logit (every e_v is then exp2(-inf) = 0).
 __device__ inline float exp_offset(float o) { return o != -INFINITY ? o : 0.0f; }
 
 // min of two values that are >= 0 or +NaN (0 * inf): the unsigned order of the bits is their
@@ -402,6 +405,56 @@ __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
     } else {
       sh.xt[r][t] = __int_as_float(fkey(m));  // integer key: the group max needs no NaN care
     }
+  }
+}
+
+// ---- 1''. per-thread statistics of every row of item q in one pass (several items per
+// workgroup): the max, the thread's own offset o_t = ceil(m_t c) (0 when its logits are all
+// -inf), and the exp2 sum against it; max keys, sums and offsets to LDS. The offsets are
+// integers, so the group's rescaling of the sums to the slice offset is exact ----
+template <int DT, int D, bool NEED_ARG, typename L>
+__device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos& q,
+                                                typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                                int t) {
+  constexpr int E = Vec<DT>::kElems;
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    if (r > q.n) continue;
+    launder(raw[r]);
+    float z[E];
+    Vec<DT>::unpack(raw[r], z);
+    float m = -INFINITY;
+    int idx = INT_MAX;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if (NEED_ARG) {
+        if (z[e] > m) {
+          m = z[e];
+          idx = q.vi * E + e;
+        }
+      } else {
+        m = fmaxf(m, z[e]);
+      }
+    }
+    const float of = m != -INFINITY ? ceilf(m * A.c) : 0.0f;
+    float v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -of));
+    float a0 = v[0], a1 = v[1];
+#pragma unroll
+    for (int e = 2; e < E; ++e) {
+      if (e & 1) a1 += v[e];
+      else a0 += v[e];
+    }
+    if (NEED_ARG) {
+      if (idx == INT_MAX && q.vi < A.nvec) idx = q.vi * E;
+      sh.xt[r][t] = m;
+      sh.xi[r][t] = idx;
+    } else {
+      sh.xt[r][t] = __int_as_float(fkey(m));
+    }
+    sh.xs[r][t] = a0 + a1;
+    sh.xo[r][t] = (int)of;
   }
 }
 
@@ -704,7 +757,7 @@ template <int DT, int D, bool NEED_SUM, bool NEED_ARG, bool SINGLE>
 __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   using Raw = typename Vec<DT>::Raw;
   constexpr int RM = D + 1;
-  __shared__ TeamLds<D, NEED_ARG> sh;
+  __shared__ TeamLds<D, NEED_ARG, NEED_SUM && !SINGLE> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int gi = t >> 4, gl = t & 15;  // 16-lane group gi reduces row gi; gl: lane in it
   HS_STAMP_WG(0);
@@ -788,27 +841,33 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     auto stats = [&](const ItemPos& q, Raw (&raw)[RM], int bf) __attribute__((always_inline)) {
       __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
       mask_tail<DT, D>(A, q, raw);
-      thread_max<DT, D, NEED_ARG>(A, q, raw, sh, t);
+      thread_stats_pt<DT, D, NEED_ARG>(A, q, raw, sh, t);
       __syncthreads();
-      const bool rows = wv * 4 <= q.n;  // this wave holds the group of a row
-      float m = 0.0f;
-      int idx = 0;
-      if (rows) {
+      if (wv * 4 <= q.n) {  // this wave holds the group of a row
+        float m;
+        int idx;
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
+        const int r = min(gi, q.n);
+        const float o = ceilf(m * A.c);  // -inf for a slice without a finite logit
+        const int oi = m != -INFINITY ? (int)o : 0;
+        // the 16 sums of this lane rescaled to the slice offset (exact: powers of two) and
+        // added in sum16's order, four at a time (one 16-byte read of sums and of offsets)
+        typedef float F4 __attribute__((ext_vector_type(4)));
+        typedef int I4 __attribute__((ext_vector_type(4)));
+        float c[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const F4 x = *reinterpret_cast<const F4*>(&sh.xs[r][64 * i + 4 * gl]);
+          const I4 y = *reinterpret_cast<const I4*>(&sh.xo[r][64 * i + 4 * gl]);
+          c[i] = (ldexpf(x[0], y[0] - oi) + ldexpf(x[1], y[1] - oi)) +
+                 (ldexpf(x[2], y[2] - oi) + ldexpf(x[3], y[3] - oi));
+        }
+        const float s = row16_sum((c[0] + c[1]) + (c[2] + c[3]));
         if (gl == 0 && gi <= q.n) {
-          const float o = m != -INFINITY ? m * A.c : -INFINITY;
           sh.o[bf][gi] = o;
           sh.no[bf][gi] = -exp_offset(o);
+          publish_row<true, NEED_ARG>(A, q, gi, tag, m, s, idx, RM);
         }
-      }
-      __syncthreads();
-      thread_sums<DT, D>(A, q, raw, sh, bf, t);
-      __syncthreads();
-      if (rows) {
-        float v[16];
-        group_read(&sh.xt[min(gi, q.n)][0], gl, v);
-        const float s = row16_sum(sum16(v));
-        if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, s, idx, RM);
       }
       __builtin_amdgcn_s_setprio(0);
     };
@@ -847,7 +906,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (rows) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
         if (gl == 0 && gi <= q.n) {
-          const float o = m != -INFINITY ? m * A.c : -INFINITY;
+          const float o = ceilf(m * A.c);  // -inf for a slice without a finite logit
           sh.o[0][gi] = o;
           sh.no[0][gi] = -exp_offset(o);
         }
