@@ -408,7 +408,7 @@ __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// ---- 1''. per-thread statistics of every row of item q in one pass (several items per
+// ---- 1-3. per-thread statistics of every row of item q in one pass (several items per
 // workgroup): the max, the thread's own offset o_t = ceil(m_t c) (0 when its logits are all
 // -inf), and the exp2 sum against it; max keys, sums and offsets to LDS. The offsets are
 // integers, so the group's rescaling of the sums to the slice offset is exact ----
@@ -485,33 +485,6 @@ __device__ __forceinline__ void group_max(const L& sh, int n, int gi, int gl, fl
   }
 }
 
-// ---- 3. exp2 sums against the slice offsets o (buffer bf): exp2(z_v c - o) summed per
-// thread, to LDS ----
-template <int DT, int D, typename L>
-__device__ __forceinline__ void thread_sums(const TeamArgs& A, const ItemPos& q,
-                                            typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
-                                            int bf, int t) {
-  constexpr int E = Vec<DT>::kElems;
-#pragma unroll
-  for (int r = 0; r <= D; ++r) {
-    if (r > q.n) continue;
-    launder(raw[r]);
-    float z[E];
-    Vec<DT>::unpack(raw[r], z);
-    const float no = sh.no[bf][r];
-    float v[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, no));
-    float a0 = v[0], a1 = v[1];
-#pragma unroll
-    for (int e = 2; e < E; ++e) {
-      if (e & 1) a1 += v[e];
-      else a0 += v[e];
-    }
-    sh.xt[r][t] = a0 + a1;
-  }
-}
-
 // Slice statistics of row r as tagged words.
 template <bool NEED_SUM, bool NEED_ARG>
 __device__ __forceinline__ void publish_row(const TeamArgs& A, const ItemPos& q, int r,
@@ -559,7 +532,7 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// ---- 3'. exponentials kept in registers (workgroups with a single item): e_v = exp2(z_v c - o)
+// ---- 3. exponentials kept in registers (workgroups with a single item): e_v = exp2(z_v c - o)
 // against the slice offsets (buffer 0) into x, per-thread sums to LDS ----
 template <int DT, int D, typename L>
 __device__ __forceinline__ void thread_exps_kept(const TeamArgs& A, const ItemPos& q,
@@ -943,6 +916,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
     stats(q0, R0, 0);
+    // the first item's group reductions read every column of the LDS rows that the next
+    // item's per-thread statistics overwrite, and nothing else in the first iteration waits
+    // for the whole workgroup before those writes (later items are kept apart by the
+    // barriers around the min-sums)
+    __syncthreads();
 
     uint32_t pset = nsets;  // the team's previous item, whose alpha is still to be folded
     // iteration j: rc holds item j (statistics published), rn item j + 1 (loaded), rp receives
