@@ -346,6 +346,24 @@ def test_deterministic_rerun_bitwise():
         assert torch.equal(first, again)
 
 
+def test_deterministic_rerun_bitwise_many_items_per_workgroup():
+    # batched_serving holds more row sets than the grid holds teams, so each workgroup runs
+    # the multi-item loop with claimed items: every item's arithmetic is fixed whichever team
+    # takes it, and no item may see LDS values left by the one before it
+    w = WL["batched_serving"]
+    note("determinism, batched_serving full size: sampling and greedy, 6 reruns each")
+    xd = dev_logits(w, synth.generate(w))
+    ws = hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, "cuda")
+    for mode in (hs.SAMPLE, hs.GREEDY):
+        kw = dict(temperature=w.temperature, mode=mode, want_agree=True, want_argmax=True,
+                  workspace=ws)
+        first = {k: v.clone() for k, v in hs.eval_alpha(xd, **kw).items()}
+        for _ in range(6):
+            again = hs.eval_alpha(xd, **kw)
+            for k, v in first.items():
+                assert torch.equal(v, again[k]), (mode, k)
+
+
 def test_softmax_stats_entry():
     note("hs_softmax_stats vs oracle")
     for w in (WL["tiny_chain"], synth.variant(WL["qwen3_8b_single"], K=2)):
