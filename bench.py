@@ -114,6 +114,8 @@ def parse():
     ap.add_argument("--bookkeeping", action="store_true",
                     help="time one round of drafter play (argmax of NormalHedge's p) and regret "
                          "bookkeeping (hs_play + hs_regret_update) on the workload's B, N")
+    ap.add_argument("--softmax-stats", action="store_true",
+                    help="time hs_softmax_stats over every row of the workload instead")
     ap.add_argument("--delayed", action="store_true",
                     help="time hs_delayed_update (token-level delayed feedback) on the workload's "
                          "B, N, K instead, K new tokens per query per round")
@@ -228,6 +230,71 @@ def bench_bookkeeping(args, w, hs, torch, dev):
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                          "kernel": "hs_play_kernel + hs_regret_kernel (one wave per query each)",
+                         "bytes_per_call": nbytes}}
+    print(json.dumps(line), flush=True)
+
+
+def bench_softmax_stats(args, w, hs, torch, dev, synth):
+    """hs_softmax_stats over every row of the workload (target and drafters, all queries and
+    positions) on distinct rounds resident in HBM (>= 512 MB, rotated), in a HIP graph. The
+    roofline prices a call at each logit read once plus the three outputs per row."""
+    copies = max(1, math.ceil(ROTATE_BYTES / w.input_bytes))
+    if w.input_bytes * copies > 64e9:
+        copies = max(1, int(64e9 // w.input_bytes))
+    bufs = []
+    for r in range(copies):
+        x = synth.generate(w, round=r)
+        t = torch.from_numpy(x.reshape(-1, x.shape[-1]))
+        if w.dtype == synth.BF16:
+            t = t.view(torch.bfloat16)
+        bufs.append(t.to(dev))
+        del x, t
+    rows = bufs[0].shape[0]
+    out = (torch.empty(rows, dtype=torch.float32, device=dev),
+           torch.empty(rows, dtype=torch.float32, device=dev),
+           torch.empty(rows, dtype=torch.int32, device=dev))
+    stream = torch.cuda.Stream()
+
+    def call(i):
+        hs.softmax_stats(bufs[i % copies], V=w.V, temperature=w.temperature, out=out,
+                         stream=torch.cuda.current_stream())
+
+    with torch.cuda.stream(stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // copies)
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup // copies)):
+            g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+    eb = 2 if w.dtype == synth.BF16 else 4
+    nbytes = rows * w.V * eb + rows * 12
+    achieved = nbytes / (us * 1e-6) / 1e9
+    line = {"metric": "softmax row statistics: rows per second + achieved HBM GB/s",
+            "value": rows / (us * 1e-6), "unit": "rows/s", "n_gpus": 1,
+            "steps": reps * copies, "warmup": max(1, args.warmup // copies) * copies,
+            "us_per_call": us, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": w.name, "rows": rows, "V": w.V,
+                       "logits": "bf16" if w.dtype == synth.BF16 else "f32",
+                       "temperature": w.temperature, "rotation_copies": copies,
+                       "hip_graph": True},
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                         "kernel": "hs_softmax_stats (one workgroup per row)",
                          "bytes_per_call": nbytes}}
     print(json.dumps(line), flush=True)
 
@@ -359,6 +426,9 @@ def main():
         return
     if args.bookkeeping:
         bench_bookkeeping(args, w, hs, torch, dev)
+        return
+    if args.softmax_stats:
+        bench_softmax_stats(args, w, hs, torch, dev, synth)
         return
 
     # ---- inputs: distinct rounds, resident in HBM -----------------------------------------

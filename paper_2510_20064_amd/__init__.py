@@ -131,16 +131,23 @@ def _view(t: torch.Tensor) -> hs_view:
 # --------------------------------------------------------------------------------------------
 
 def softmax_stats(x: torch.Tensor, V: Optional[int] = None, temperature: float = 1.0,
-                  stream=None):
-    """hs_softmax_stats on a [rows][ld] tensor: returns (row_max f32, row_lse f32, row_argmax i32)."""
+                  stream=None, out=None):
+    """hs_softmax_stats on a [rows][ld] tensor: returns (row_max f32, row_lse f32, row_argmax i32),
+    written into `out` (the same three tensors) when it is given."""
     lib = load_library()
     rows, ld = x.shape
     V = ld if V is None else V
     if x.stride(1) != 1:
         raise ValueError("rows must be contiguous")
-    mx = torch.empty(rows, dtype=torch.float32, device=x.device)
-    lse = torch.empty(rows, dtype=torch.float32, device=x.device)
-    am = torch.empty(rows, dtype=torch.int32, device=x.device)
+    if out is None:
+        mx = torch.empty(rows, dtype=torch.float32, device=x.device)
+        lse = torch.empty(rows, dtype=torch.float32, device=x.device)
+        am = torch.empty(rows, dtype=torch.int32, device=x.device)
+    else:
+        mx, lse, am = out
+        for o, dt in ((mx, torch.float32), (lse, torch.float32), (am, torch.int32)):
+            if o.dtype != dt or o.numel() != rows or not o.is_contiguous() or o.device != x.device:
+                raise ValueError("out: three contiguous [rows] tensors (f32, f32, i32) on x's device")
     _check(lib.hs_softmax_stats(_ptr(x), _dtype_code(x), rows, V, x.stride(0), temperature,
                                 _ptr(mx), _ptr(lse), _ptr(am), _stream(stream)))
     return mx, lse, am

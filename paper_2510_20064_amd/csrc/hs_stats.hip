@@ -1,30 +1,74 @@
 // hs_softmax_stats: max, lowest-index argmax and natural-log normaliser of `rows` temperature
-// softmaxes. One workgroup per row, looping over the row's slices.
+// softmaxes. One workgroup per row.
 #include "hs_rowstats.h"
 
 namespace hs {
 
+// Each thread walks its vectors of the row (stride kThreads, U per chunk) keeping a running max,
+// lowest argmax and an exp2 sum against its own integer offset o = ceil(m c): a larger max
+// rescales the sum by 2^(o_old - o_new) exactly, and the next chunk's loads are in flight
+// while the current one is reduced. One block reduction per row at the end.
 template <int DT>
 __global__ __launch_bounds__(kThreads) void hs_softmax_stats_kernel(const char* x, int64_t ld,
                                                                     int64_t V, int64_t nvec,
-                                                                    int64_t vps, int S, float c,
-                                                                    float* rmax, float* rlse,
+                                                                    float c, float* rmax,
+                                                                    float* rlse,
                                                                     int32_t* ramax) {
+  using Vt = Vec<DT>;
+  using Raw = typename Vt::Raw;
+  constexpr int E = Vt::kElems, U = Vt::kU;
+  constexpr int64_t kStep = (int64_t)U * kThreads;  // vectors per chunk of the workgroup
+  const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
-  const char* rowp = x + row * ld * Vec<DT>::kBytes;
+  const char* rowp = x + row * ld * Vt::kBytes;
+  auto fetch = [&](int64_t v0, Raw (&r)[U]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int64_t vi = v0 + (int64_t)j * kThreads + t;
+      r[j] = vi < nvec ? Vt::load_raw(rowp, vi, V) : Vt::neg_raw();
+    }
+  };
   float m = -INFINITY, o = -INFINITY, s = 0.0f;
   int idx = INT_MAX;
-  for (int j = 0; j < S; ++j) {
-    const int64_t v0 = (int64_t)j * vps;
-    const int64_t v1 = v0 + vps < nvec ? v0 + vps : nvec;
-    const SliceStat st = row_slice_stats<DT, true, true>(rowp, v0, v1, V, c);
-    argmax_combine(m, idx, st.m, st.idx);
-    lse2_combine(o, s, st.o, st.s);
+  Raw cur[U], nxt[U];
+  fetch(0, cur);
+  for (int64_t v0 = 0; v0 < nvec; v0 += kStep) {
+    if (v0 + kStep < nvec) fetch(v0 + kStep, nxt);
+    float z[U][E];
+#pragma unroll
+    for (int j = 0; j < U; ++j) Vt::unpack(cur[j], z[j]);
+    // indices are visited in increasing order, so a strict compare keeps the lowest
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (z[j][e] > m) {
+          m = z[j][e];
+          idx = (int)((v0 + (int64_t)j * kThreads + t) * E + e);
+        }
+    if (m != -INFINITY) {
+      const float on = ceilf(m * c);
+      if (on != o) {
+        s = (o == -INFINITY) ? 0.0f : ldexpf(s, (int)fmaxf(o - on, -256.0f));
+        o = on;
+      }
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[j][e], c, -o));
+      s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) cur[j] = nxt[j];
   }
-  if (threadIdx.x == 0) {
-    if (rmax) rmax[row] = m;
-    if (ramax) ramax[row] = idx;
-    if (rlse) rlse[row] = (o == -INFINITY) ? NAN : (o + log2f(s)) * 0.69314718055994530942f;
+  // a thread whose logits are all -inf still owns its lowest valid index
+  if (idx == INT_MAX && t < nvec) idx = t * E;
+  const SliceStat r = block_reduce_stat<true, true>(m, idx, o, s);
+  if (t == 0) {
+    if (rmax) rmax[row] = r.m;
+    if (ramax) ramax[row] = r.idx;
+    if (rlse) rlse[row] = (r.o == -INFINITY) ? NAN : (r.o + log2f(r.s)) * 0.69314718055994530942f;
   }
 }
 
@@ -33,16 +77,13 @@ int launch_softmax_stats(const void* x, int dtype, int64_t rows, int64_t V, int6
                          hipStream_t stream) {
   const int E = dtype == HS_F32 ? Vec<HS_F32>::kElems : Vec<HS_BF16>::kElems;
   const int64_t nvec = (V + E - 1) / E;
-  const int64_t per = kSliceElems / E;
-  const int S = (int)((nvec + per - 1) / per);
-  const int64_t vps = (nvec + S - 1) / S;
   const char* xp = reinterpret_cast<const char*>(x);
   if (dtype == HS_F32)
     hs_softmax_stats_kernel<HS_F32><<<(unsigned)rows, kThreads, 0, stream>>>(
-        xp, ld, V, nvec, vps, S, c, row_max, row_lse, row_argmax);
+        xp, ld, V, nvec, c, row_max, row_lse, row_argmax);
   else
     hs_softmax_stats_kernel<HS_BF16><<<(unsigned)rows, kThreads, 0, stream>>>(
-        xp, ld, V, nvec, vps, S, c, row_max, row_lse, row_argmax);
+        xp, ld, V, nvec, c, row_max, row_lse, row_argmax);
   return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
 }
 

@@ -376,6 +376,12 @@ def test_softmax_stats_entry():
             assert np.array_equal(am.cpu().numpy(), ra)
             assert np.array_equal(mx.cpu().numpy().astype(np.float64), rm)
             assert np.allclose(lse.cpu().numpy(), rl, rtol=2e-6, atol=1e-5)
+            # caller-provided outputs (as the bench passes them): the same bits
+            out = tuple(torch.full_like(v, -7) for v in (mx, lse, am))
+            got = hs.softmax_stats(xd, temperature=T, out=out)
+            torch.cuda.synchronize()
+            assert all(g is o for g, o in zip(got, out))
+            assert all(torch.equal(a, b) for a, b in zip(got, (mx, lse, am)))
 
 
 def test_accept_len_loss_kinds_chain():
