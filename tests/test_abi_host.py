@@ -127,6 +127,19 @@ def test_softmax_stats_validation_codes():
     assert lib.hs_softmax_stats(FAKE, 0, 4, 100, 100, 0.0, FAKE, None, None, None) == 5
 
 
+def test_softmax_stats_binding_rejects_mismatched_outputs():
+    # checked before the library is called, so host tensors do
+    import torch
+
+    x = torch.zeros((3, 64), dtype=torch.float32)
+    bad = [(torch.empty(3), torch.empty(3), torch.empty(3)),                         # argmax f32
+           (torch.empty(4), torch.empty(3), torch.empty(3, dtype=torch.int32)),      # wrong length
+           (torch.empty(6)[::2], torch.empty(3), torch.empty(3, dtype=torch.int32))]  # strided
+    for out in bad:
+        with pytest.raises(ValueError):
+            hs.softmax_stats(x, out=out)
+
+
 def test_round_validation_codes():
     lib = hs.load_library()
     d = _views(8)
