@@ -384,6 +384,37 @@ def test_softmax_stats_entry():
             assert all(torch.equal(a, b) for a, b in zip(got, (mx, lse, am)))
 
 
+def test_softmax_stats_growing_maxima():
+    # rows whose running max grows chunk after chunk, so every thread rescales its sum many
+    # times: an increasing ramp, the max on the last logit, and a jump of 200 (early sums
+    # rescaled below fp32's range); bf16 and fp32, V with a ragged tail
+    rng = np.random.default_rng(31)
+    V = 100003
+    z = rng.normal(0, 1, (5, V)).astype(np.float32)
+    z[0] = np.linspace(-30.0, 30.0, V, dtype=np.float32)
+    z[1, -1] = 40.0
+    z[2, V // 2:] += 200.0
+    z[3] = -np.linspace(-30.0, 30.0, V, dtype=np.float32)   # max first, then only smaller
+    z[4, ::7] = -np.inf
+    u = z.view(np.uint32).astype(np.uint64)
+    zb = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    for x, dt in ((z, synth.F32), (zb, synth.BF16)):
+        note("softmax stats, growing maxima, dtype=%d" % dt)
+        ld = V + (1 if dt == synth.F32 else 5)  # rows on 16-byte boundaries
+        pad = np.zeros((x.shape[0], ld), dtype=x.dtype)
+        pad[:, :V] = x
+        t = torch.from_numpy(pad)
+        if dt == synth.BF16:
+            t = t.view(torch.bfloat16)
+        for T in (1.0, 0.3):
+            mx, lse, am = hs.softmax_stats(t.cuda(), V=V, temperature=T)
+            torch.cuda.synchronize()
+            rm, ra, rl = oracle.softmax_stats(np.ascontiguousarray(pad[:, :V]), T=T)
+            assert np.array_equal(am.cpu().numpy(), ra), T
+            assert np.array_equal(mx.cpu().numpy().astype(np.float64), rm), T
+            assert np.allclose(lse.cpu().numpy(), rl, rtol=2e-6, atol=1e-5), T
+
+
 def test_accept_len_loss_kinds_chain():
     note("hs_accept_len: all three loss kinds on seeded gamma")
     rng = np.random.default_rng(4)
