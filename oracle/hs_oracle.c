@@ -28,12 +28,16 @@
  *   or_play                 : pinned (point masses, empirical frequencies on a uniform grid
  *                             of draws, argmax ties by index, zero rows).
  *   or_regret_update        : pinned (hand-computed stream, always playing one drafter,
- *                             Hedge's expected-regret bound ln N / eta + eta T / 8).
+ *                             chunked updates equal one update, the played EAL sum).
  *   or_window_losses        : pinned (all-accept and all-reject windows, K = 1, constant
  *                             gamma geometric sum, the censoring appendix's worked example).
- *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss)).
+ *   or_hedge                : pinned (closed form w ~ exp(-eta * cumulative loss),
+ *                             Hedge's expected-regret bound ln N / eta + eta T / 8).
  *   or_normalhedge          : pinned (closed-form c for one or m equal positive
- *                             regrets, scale covariance, sum_i p_i dR_i = 0).
+ *                             regrets, scale covariance, sum_i p_i dR_i = 0, and
+ *                             the weights equal the normalised gradient in R of the
+ *                             scale equation's left side at the solved c, taken by
+ *                             finite differences, with several distinct regrets).
  */
 #include <math.h>
 #include <stdint.h>

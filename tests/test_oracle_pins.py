@@ -387,6 +387,61 @@ def test_normalhedge_scale_covariance_and_permutation():
     assert np.allclose(p3, p1[:, perm], atol=1e-13)
 
 
+@pytest.mark.parametrize("seed", [21, 22, 23])
+def test_normalhedge_weights_are_the_gradient_of_the_scale_equation(seed):
+    # NormalHedge's weight on drafter i is the partial derivative, in R_i, of the potential
+    # whose level set e fixes c: p_i is proportional to d/dR_i (1/N) sum_j exp([R_j]_+^2 / 2c)
+    # at the solved c. The derivative is taken here by central differences of that left
+    # side (a route independent of the oracle's weight formula), with several distinct
+    # positive regrets, so a wrong exponent or a wrong prefactor in the weights fails.
+    rng = np.random.default_rng(seed)
+    N = 9
+    R0 = rng.normal(0.2, 1.0, (1, N))
+    R0[0, :3] = [1.3, 0.4, 2.1]  # at least three distinct positive regrets
+    R0[0, 3] = -0.5
+    zero = np.zeros((1, 1, N))  # a zero loss leaves R unchanged and re-solves c
+    R, p, c = oracle.normalhedge(R0, np.full((1, N), 1 / N), zero)
+    assert np.array_equal(R, R0) and c[0] > 0
+
+    def lhs(r):
+        rp = np.maximum(r, 0.0)
+        return np.mean(np.exp(rp * rp / (2.0 * c[0])))
+
+    h = 1e-6
+    grad = np.zeros(N)
+    for i in range(N):
+        e = np.zeros(N)
+        e[i] = h
+        grad[i] = (lhs(R0[0] + e) - lhs(R0[0] - e)) / (2 * h)
+    grad[R0[0] <= 0] = 0.0  # [R]_+ has no slope there (the one-sided kink at 0 is not hit)
+    want = grad / grad.sum()
+    assert np.allclose(p[0], want, rtol=1e-7, atol=1e-9)
+    # and the solved c really is the root: the level set is e
+    assert abs(lhs(R0[0]) - math.e) < 1e-12
+
+
+def test_hedge_expected_regret_within_the_hedge_bound():
+    # Hedge on losses in [0, 1]: sum_t <w_t, l_t> - min_i sum_t l_t,i <= ln N / eta + eta T / 8
+    # (the standard bound, Hoeffding's lemma per round), for any loss sequence; a sign slip in
+    # the update (weights growing with loss) breaks it on an adversarial stream.
+    rng = np.random.default_rng(12)
+    B, N, T = 4, 8, 400
+    eta = math.sqrt(8 * math.log(N) / T)
+    w = np.full((B, N), 1 / N)
+    mix = np.zeros(B)
+    cum = np.zeros((B, N))
+    for t in range(T):
+        # adversarial-ish: the drafter that currently has the most weight loses
+        loss = rng.random((B, N)) * 0.3
+        loss[np.arange(B), np.argmax(w, axis=1)] = 1.0
+        loss[:, 0] = np.minimum(loss[:, 0], 0.25)  # drafter 0 stays the best in hindsight
+        mix += (w * loss).sum(axis=1)
+        cum += loss
+        w = oracle.hedge(w, loss[None], eta)
+    regret = mix - cum.min(axis=1)
+    assert np.all(regret <= math.log(N) / eta + eta * T / 8 + 1e-9)
+
+
 def test_normalhedge_equal_losses_leave_regrets_exactly_unchanged():
     # l_A = sum_i p_i l = l when every loss is equal: regrets must not move at all,
     # whatever p is (no spurious positive regret from rounding)
