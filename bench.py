@@ -7,17 +7,20 @@ Theorem 3's expected acceptance length, the length loss, and the Hedge and Norma
 updates (hs_round: one launch of the evaluation kernel, which folds the slice sums into alpha
 and runs each query's learner step once its alpha is complete).
 
-Workload: the Qwen3-8B-shaped single query (B=1 query, N=8 drafters, K=8 positions,
-V=151936, bf16 logits, T=1). Inputs are resident in HBM before timing starts; successive
-steps rotate through >= 512 MB of distinct rounds so that the 256 MB Infinity Cache cannot
-serve them. Steps are captured in a HIP graph (the path is launch-bound at this size).
+Default workload: the large drafter pool (B=32 queries, N=64 drafters, K=8 positions,
+V=151936, bf16 logits, T=1, Hedge with eta = sqrt(8 ln N / 1000) and NormalHedge), the largest
+configuration, 5.06 GB of logits per round. Inputs are resident in HBM before timing starts;
+successive steps rotate through distinct rounds (at least two, and >= 512 MB in all) so that
+the 256 MB Infinity Cache cannot serve a repeated input. Steps run as HIP graph replays; every
+graph is captured before the timed region.
 
-Prints one JSON line (rank 0). `value` = drafter-positions evaluated per second (B*N*K per
-step). `roofline` prices one hs_eval_alpha call (one launch of the team kernel, timed with
-HIP events on the stream it runs on) against HBM bandwidth with
+Prints one JSON line. `value` = drafter-positions evaluated per second (B*N*K per step).
+`roofline` prices one hs_eval_alpha call (one launch of the team kernel, timed with HIP events
+on the stream it runs on, over calls replayed back to back) against HBM bandwidth with
 algorithmic bytes (every logit read once); `traffic` is the counter-measured HBM bytes of that
-call from the committed FETCH_SIZE / WRITE_SIZE summary, null if the kernel sources changed
-since it was taken. `cpu_baseline` times the float64 oracle on the host.
+call from the committed FETCH_SIZE / WRITE_SIZE summary of the workload, null if there is
+none or the kernel sources changed since it was taken. `cpu_baseline` times the float64 oracle
+on the host, on all cores and on one thread.
 """
 from __future__ import annotations
 
@@ -35,10 +38,9 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 ROTATE_BYTES = 512 * 1024 * 1024
 METRIC = "drafter-positions evaluated/sec + achieved HBM GB/s (% of peak), 1 MI355X"
-# Sources of the evaluation kernels; the counter summary below is valid only for these bytes.
+# Sources of the evaluation kernels; a counter summary is valid only for these bytes.
 KERNEL_SOURCES = ["paper_2510_20064_amd/csrc/hs_team.hip", "paper_2510_20064_amd/csrc/hs_wave.h",
                   "paper_2510_20064_amd/csrc/hs_internal.h", "paper_2510_20064_amd/csrc/hs_learner.h"]
-PMC_SUMMARY = "profiles/hs_eval_alpha_qwen3_8b_single_pmc.md"
 
 
 def kernel_source_digest() -> str:
@@ -51,11 +53,15 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per hs_eval_alpha call from the committed FETCH_SIZE / WRITE_SIZE summary,
-    or None when there is none for this workload or the kernel sources changed since."""
-    path = os.path.join(ROOT, PMC_SUMMARY)
-    if workload != "qwen3_8b_single" or not os.path.exists(path):
+def pmc_summary_path(name: str) -> str:
+    return os.path.join(ROOT, "profiles", "hs_eval_alpha_%s_pmc.md" % name)
+
+
+def measured_traffic(name: str):
+    """HBM bytes per hs_eval_alpha call from the committed FETCH_SIZE / WRITE_SIZE summary of
+    this workload, or None when there is none or the kernel sources changed since."""
+    path = pmc_summary_path(name)
+    if not os.path.exists(path):
         return None
     rec = None
     with open(path) as f:
@@ -96,16 +102,23 @@ def measured_topl_traffic(workload: str):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=4800)
-    ap.add_argument("--warmup", type=int, default=480)
-    ap.add_argument("--workload", default="qwen3_8b_single")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="large_pool_stream")
+    ap.add_argument("--stack", type=int, default=1, metavar="R",
+                    help="R independent instances of the workload per step (R times the "
+                         "queries, each with its own logits; for the latency-bound small shapes)")
+    ap.add_argument("--cpu-seconds", type=float, default=18.0,
+                    help="approximate CPU time budget of the oracle baseline, two thirds on all "
+                         "cores and one third on one thread (0 = skip)")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--greedy", action="store_true",
                     help="evaluate in greedy argmax-agreement mode (the workload's second run)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--read-calibration", action="store_true",
+                    help="also time a plain streaming read of the resident inputs (a library "
+                         "reduction over every input byte): this box's achievable read rate")
     ap.add_argument("--topl", type=int, default=0, metavar="L",
                     help="time hs_eval_topl (EAGLE's top-L acceptance mass, Theorem 2) with L "
                          "children per node on the workload instead")
@@ -416,6 +429,8 @@ def main():
     w = synth.workloads()[args.workload]
     if args.greedy:
         w = synth.variant(w, mode=synth.GREEDY)
+    if args.stack > 1:  # R independent instances: R times the queries, each its own logits
+        w = synth.variant(w, B=w.B * args.stack)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.delayed:
@@ -432,7 +447,7 @@ def main():
         return
 
     # ---- inputs: distinct rounds, resident in HBM -----------------------------------------
-    copies = max(1, math.ceil(ROTATE_BYTES / w.input_bytes))
+    copies = max(2, math.ceil(ROTATE_BYTES / w.input_bytes))
     if w.input_bytes * copies > 64e9:
         copies = max(1, int(64e9 // w.input_bytes))
     bufs = []
@@ -442,6 +457,7 @@ def main():
         if w.dtype == synth.BF16:
             t = t.view(torch.bfloat16)
         bufs.append(t.to(dev))
+        del x, t
     parent = w.parent()
     path_end = w.path_end()
     pe_dev = None if path_end is None else torch.from_numpy(path_end).to(dev)
@@ -455,91 +471,79 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.Stream()
+    greedy = w.mode == hs.GREEDY
+    use_graph = not args.no_graph
 
     def step_fn(i):
         rounds[i % copies].run(stream=torch.cuda.current_stream())
 
-    # ---- graphs of the per-copy steps -----------------------------------------------------
-    use_graph = not args.no_graph
+    ev_ws = hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, dev)
+    ev_out = ({"agree": torch.empty((w.B, w.N, w.K), dtype=torch.uint8, device=dev)} if greedy
+              else {"alpha": torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=dev)})
+
+    def eval_fn(i):
+        hs.eval_alpha(bufs[i % copies], V=w.V, temperature=w.temperature, mode=w.mode,
+                      workspace=ev_ws, out=ev_out, stream=torch.cuda.current_stream())
+
+    # ---- every graph the timed regions replay, captured up front ----------------------------
     graphs = {}
 
-    def graph_for(n):
-        if n not in graphs:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.stream(stream):
-                for i in range(n):  # eager pass before capture
-                    step_fn(i)
-            torch.cuda.synchronize()
-            with torch.cuda.graph(g, stream=stream):
-                for i in range(n):
-                    step_fn(i)
-            torch.cuda.synchronize()
-            graphs[n] = g
-        return graphs[n]
+    def capture(fn, n):
+        key = (fn.__name__, n)
+        if n == 0 or key in graphs:
+            return
+        with torch.cuda.stream(stream):
+            for i in range(n):  # one eager pass before capture
+                fn(i)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(n):
+                fn(i)
+        torch.cuda.synchronize()
+        graphs[key] = g
 
-    def run_steps(n):
+    def run(fn, n):
+        """n calls of fn (in rounds of `copies`), replaying graphs captured beforehand."""
         if not use_graph:
             with torch.cuda.stream(stream):
                 for i in range(n):
-                    step_fn(i)
+                    fn(i)
             return
         full, rem = divmod(n, copies)
-        if full:
-            g = graph_for(copies)
-            with torch.cuda.stream(stream):
-                for _ in range(full):
-                    g.replay()
-        if rem:
-            g = graph_for(rem)
-            with torch.cuda.stream(stream):
-                g.replay()
+        with torch.cuda.stream(stream):
+            for _ in range(full):
+                graphs[(fn.__name__, copies)].replay()
+            if rem:
+                graphs[(fn.__name__, rem)].replay()
 
-    # ---- warmup + timed region ------------------------------------------------------------
-    run_steps(args.warmup)
+    n_eval = copies * max(1, args.steps // copies)
+    if use_graph:
+        for n in {copies, args.steps % copies, args.warmup % copies}:
+            capture(step_fn, n)
+        capture(eval_fn, copies)
+
+    # ---- warmup + timed region: the hs_round steps ------------------------------------------
+    run(step_fn, args.warmup)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
-    run_steps(args.steps)
+    run(step_fn, args.steps)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = e0.elapsed_time(e1) / args.steps
     value = w.positions / (ms_step * 1e-3)
 
-    # ---- evaluation kernel alone, live, on the same stream --------------------------------
-    ev_ws = [hs.alloc_workspace(w.B, w.N, w.K, w.V, w.dtype, dev)]
-    greedy = w.mode == hs.GREEDY
-    outs = [{"agree": torch.empty((w.B, w.N, w.K), dtype=torch.uint8, device=dev)} if greedy else
-            {"alpha": torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=dev)}]
-
-    def eval_fn(i):
-        hs.eval_alpha(bufs[i % copies], V=w.V, temperature=w.temperature, mode=w.mode,
-                      workspace=ev_ws[0], out=outs[0], stream=torch.cuda.current_stream())
-
-    n_eval = copies * max(1, args.steps // (4 * copies))
-    with torch.cuda.stream(stream):
-        for i in range(copies):
-            eval_fn(i)
+    # ---- the evaluation kernel alone (hs_eval_alpha), live, on the same stream -------------
+    run(eval_fn, copies)
     torch.cuda.synchronize()
-    if use_graph:
-        ge = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(ge, stream=stream):
-            for i in range(copies):
-                eval_fn(i)
-        torch.cuda.synchronize()
     e2 = torch.cuda.Event(enable_timing=True)
     e3 = torch.cuda.Event(enable_timing=True)
     e2.record(stream)
-    with torch.cuda.stream(stream):
-        for _ in range(n_eval // copies):
-            if use_graph:
-                ge.replay()
-            else:
-                for i in range(copies):
-                    eval_fn(i)
+    run(eval_fn, n_eval)
     e3.record(stream)
     torch.cuda.synchronize()
     eval_us = e2.elapsed_time(e3) * 1e3 / n_eval
@@ -551,37 +555,32 @@ def main():
         for _ in range(5):
             b.copy_(a)
         torch.cuda.synchronize()
+        del a, b
 
-    # ---- float64 oracle on the host (bounded sample of the same workload) -----------------
-    cpu = None
-    if args.cpu_seconds > 0:
-        import oracle
+    read_cal = None
+    if args.read_calibration:
+        # sums of the inputs as int32 words: every byte read once, nothing written but a scalar
+        words = [b.view(-1).view(torch.int32) for b in bufs]
+        for t in words:
+            t.sum(dtype=torch.int64)
+        torch.cuda.synchronize()
+        e4 = torch.cuda.Event(enable_timing=True)
+        e5 = torch.cuda.Event(enable_timing=True)
+        reps = max(2, n_eval // copies)
+        with torch.cuda.stream(stream):
+            e4.record(stream)
+            for _ in range(reps):
+                for t in words:
+                    t.sum(dtype=torch.int64)
+            e5.record(stream)
+        torch.cuda.synchronize()
+        rd_us = e4.elapsed_time(e5) * 1e3 / (reps * copies)
+        read_cal = {"GBps": w.input_bytes / (rd_us * 1e-6) / 1e9, "us_per_pass": rd_us,
+                    "kernel": "torch int32 sum over the %d-byte input of one step" % w.input_bytes}
 
-        xs = [synth.generate(w, round=r) for r in range(min(copies, 4))]
-        par = parent
-        wo = np.full((w.B, w.N), 1.0 / w.N)
-        Ro = np.zeros((w.B, w.N))
-        po = np.full((w.B, w.N), 1.0 / w.N)
-        t1 = time.perf_counter()
-        n_done = 0
-        while True:
-            x = xs[n_done % len(xs)]
-            ref = oracle.evaluate(x, V=w.V, T=w.temperature, want_alpha=not greedy)
-            gam = (ref["agree"].astype(np.float64) if greedy else ref["alpha"]).transpose(0, 2, 1)
-            acc = oracle.accept_len(gam, parent=par, path_end=path_end, loss_kind=w.loss)
-            wo = oracle.hedge(wo, acc["loss"], w.eta)
-            Ro, po, _ = oracle.normalhedge(Ro, po, acc["loss"])
-            n_done += 1
-            el = time.perf_counter() - t1
-            if el >= args.cpu_seconds:
-                break
-        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        threads = min(threads, os.cpu_count() or threads)
-        cpu = {"value": w.positions * n_done / el, "unit": "drafter-positions/s",
-               "cores": threads, "kind": "oracle",
-               "sample": "%d full rounds of the same workload (all %d positions each), "
-                         "float64 C oracle with OpenMP over rows, %.1f s" % (n_done, w.positions, el)}
+    cpu = cpu_baseline(args, w, np, synth, greedy) if args.cpu_seconds > 0 else None
 
+    name = w.name if args.stack == 1 else "%s_x%d" % (w.name, args.stack)
     line = {
         "metric": METRIC, "value": value, "unit": "drafter-positions/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
@@ -591,16 +590,76 @@ def main():
                    "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
                    "temperature": w.temperature, "mode": "greedy" if greedy else "sample",
                    "loss": ("length", "accept_token", "accept_chunk")[w.loss],
-                   "learners": "hedge+normalhedge", "rotation_copies": copies,
+                   "learners": "hedge+normalhedge", "tree": bool(w.tree),
+                   "stacked_instances": args.stack, "rotation_copies": copies,
                    "input_bytes_per_step": w.input_bytes, "hip_graph": use_graph,
                    "wall_s": round(wall, 4)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w.name),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(name),
                      "kernel": "hs_eval_alpha = hs_team_kernel (one launch)",
-                     "kernel_us": eval_us, "algorithmic_bytes_per_launch": w.input_bytes},
+                     "kernel_us": eval_us, "kernel_calls_timed": n_eval,
+                     "algorithmic_bytes_per_launch": w.input_bytes,
+                     "step_us": ms_step * 1e3},
         "cpu_baseline": cpu,
     }
+    if read_cal is not None:
+        line["read_calibration"] = read_cal
     print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(args, w, np, synth, greedy):
+    """The float64 oracle (alpha or agreement, EAL, loss, Hedge, NormalHedge) on the host, on a
+    bounded sample of the same workload: whole queries of round 0 (all N drafters and K
+    positions each), first on every core for two thirds of the budget, then on one thread."""
+    import oracle
+
+    nq = min(w.B, 4)
+    x = synth.generate(synth.variant(w, B=nq), round=0)  # the first nq queries of round 0
+    units = [np.ascontiguousarray(x[:, b:b + 1]) for b in range(nq)]
+    del x
+    par = w.parent()
+    pe = w.path_end()
+
+    def one(i):
+        b = i % nq
+        ref = oracle.evaluate(units[b], V=w.V, T=w.temperature, want_alpha=not greedy)
+        gam = (ref["agree"].astype(np.float64) if greedy else ref["alpha"]).transpose(0, 2, 1)
+        acc = oracle.accept_len(gam, parent=par, path_end=None if pe is None else pe[b:b + 1],
+                                loss_kind=w.loss)
+        wo = oracle.hedge(np.full((1, w.N), 1.0 / w.N), acc["loss"], w.eta)
+        oracle.normalhedge(np.zeros((1, w.N)), np.full((1, w.N), 1.0 / w.N), acc["loss"])
+        return wo
+
+    def timed(budget, min_units=1):
+        t1 = time.perf_counter()
+        n = 0
+        while True:
+            one(n)
+            n += 1
+            el = time.perf_counter() - t1
+            if el >= budget and n >= min_units:
+                return n, el
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = min(threads, os.cpu_count() or threads)
+    oracle.set_threads(threads)
+    n_all, el_all = timed(args.cpu_seconds * 2.0 / 3.0)
+    oracle.set_threads(1)
+    n_one, el_one = timed(args.cpu_seconds / 3.0)
+    oracle.set_threads(threads)
+    per_unit = w.N * w.K
+    unit_bytes = w.R * w.K * w.V * w.elem_bytes
+    return {"value": per_unit * n_all / el_all, "unit": "drafter-positions/s", "cores": threads,
+            "kind": "oracle",
+            "input_GBps": unit_bytes * n_all / el_all / 1e9,
+            "single_thread": {"value": per_unit * n_one / el_one, "unit": "drafter-positions/s",
+                              "cores": 1, "input_GBps": unit_bytes * n_one / el_one / 1e9,
+                              "queries": n_one, "seconds": round(el_one, 2)},
+            "sample": "%d whole queries (all %d drafters x %d positions each, %.1f MB of logits "
+                      "each) of round 0 of the same workload: float64 C oracle (softmax "
+                      "statistics, alpha or agreement, EAL, loss, Hedge, NormalHedge), OpenMP "
+                      "over rows on %d threads, %.1f s; then %d queries on 1 thread, %.1f s"
+                      % (n_all, w.N, w.K, unit_bytes / 1e6, threads, el_all, n_one, el_one)}
 
 
 if __name__ == "__main__":

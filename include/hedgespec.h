@@ -120,14 +120,25 @@ size_t hs_eval_alpha_workspace_size(int B, int N, int K, int64_t V, int dtype);
  *                non-NULL output is filled as well.
  * K            : positions per query (chain) or tree nodes M; 1 <= K <= 64.
  * workspace    : at least hs_eval_alpha_workspace_size() bytes of device memory,
- *                256-byte aligned, ZERO-FILLED before its first use (e.g. hipMemset).
- *                The library keeps a call counter in it and tags every word it
- *                exchanges between workgroups with it, so the workspace is reused for
- *                any shape without clearing. After a device fault or an HS_ERR_HIP
- *                return, zero it again. Waits inside the kernel are bounded: a
- *                workspace that was not zero-filled, or a device too busy with other
- *                work to hold a whole team of workgroups at once, gives NaN alpha and
- *                -2 argmax values instead of a hang.
+ *                256-byte aligned, ZERO-FILLED before its first use (e.g. hipMemset),
+ *                and afterwards written only by these calls. The library keeps a call
+ *                counter in it (the epoch, uint32 at byte 0) and tags every word it
+ *                exchanges between workgroups with a 31-bit tag derived from it, so the
+ *                workspace is reused for any shape without clearing; its counters (bytes
+ *                16 and 24) carry the tag too, so a stale count of an earlier call is
+ *                never taken for the current one. Memory that other code wrote may hold
+ *                words that look current: such a workspace gives undefined results (but
+ *                never a hang). After a device fault or an HS_ERR_HIP return, zero it again.
+ * Waits      : every wait of one workgroup for another's words is bounded (about 0.5 s,
+ *                see hs_set_wait_limit). A wait that gives up (a device too busy with
+ *                other work to hold a whole team of workgroups at once) makes the call
+ *                mark every output invalid: alpha NaN, agree 0, argmax -2.
+ * Logit range  : fp32 accuracy for finite logits z with |z| log2(e) / T <= 2^28 (for
+ *                example |z| <= 1.8e8 at T = 1). A logit far below its row's maximum
+ *                contributes its exact probability, which underflows to 0, however large
+ *                its magnitude: masks such as -1e9 or the storage type's most negative
+ *                finite value are fine next to ordinary logits. A row whose largest
+ *                logit is outside the range is treated as having no distribution (NaN).
  * Each logit is read from HBM once per call, in one launch. Results are
  * deterministic (fixed reduction order) for a given shape.
  */
@@ -307,9 +318,14 @@ int hs_regret_update(const double* loss, int L, int B, int N, const int32_t* pla
  * updates with that loss (same workspace contract as hs_eval_alpha). In sample mode
  * the learner step runs inside the evaluation launch when its LDS (gamma, losses and
  * scratch of one query) fits in the evaluation kernel's: one launch. Otherwise, and
- * in greedy mode, it is a second launch, one wave per query. Arguments mean what they mean in the calls above. Learner
- * state pointers may be NULL to skip that learner (logw and w together; R, p
- * and c together). eal is required; alpha/agree as hs_eval_alpha requires them for `mode`.
+ * in greedy mode, it is a second launch, one wave per query. Arguments mean what they
+ * mean in the calls above. Learner state pointers may be NULL to skip that learner (logw
+ * and w together; R, p and c together). eal is required; alpha/agree as hs_eval_alpha
+ * requires them for `mode`.
+ * A round whose evaluation lost a word (a wait gave up, see hs_eval_alpha) never feeds it
+ * to a learner: each query whose gamma depends on a lost word (with the second launch:
+ * every query) keeps its learner state unchanged and gets NaN eal, prefix and loss; the
+ * call still returns HS_OK (the failure happens on the device, after the call returned).
  */
 typedef struct hs_round_args {
   hs_view target;
@@ -345,6 +361,16 @@ int hs_round(const hs_round_args* args, void* stream);
 const char* hs_status_string(int status);
 const char* hs_last_error(void);
 int hs_version(void);
+
+/*
+ * hs_set_wait_limit - polls (about 2 us apart) before a wait of one evaluation workgroup
+ * for another's words gives up, for every hs_eval_alpha / hs_round launched after this call
+ * in the process. Negative restores the default (2^18, about 0.5 s). 0 makes every such wait
+ * give up at once, whatever the words hold: every call then takes its failure path (outputs
+ * marked invalid, learner state unchanged) while every kernel still ends normally, which is
+ * how that path is tested. Not synchronised with calls in flight on other threads.
+ */
+void hs_set_wait_limit(int polls);
 
 #ifdef __cplusplus
 }

@@ -82,6 +82,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_normalhedge_update.argtypes = [P, P, P, P, I, I, I, P]
     lib.hs_round.argtypes = [ctypes.POINTER(hs_round_args), P]
     lib.hs_delayed_update.argtypes = [P, P, I, I, I, I, P, I64, P, P, P, P, D, P, P, P, P, P, P]
+    lib.hs_set_wait_limit.argtypes = [I]
+    lib.hs_set_wait_limit.restype = None
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
@@ -151,6 +153,12 @@ def softmax_stats(x: torch.Tensor, V: Optional[int] = None, temperature: float =
     _check(lib.hs_softmax_stats(_ptr(x), _dtype_code(x), rows, V, x.stride(0), temperature,
                                 _ptr(mx), _ptr(lse), _ptr(am), _stream(stream)))
     return mx, lse, am
+
+
+def set_wait_limit(polls: int) -> None:
+    """hs_set_wait_limit: polls before a wait inside the evaluation kernel gives up (negative:
+    the default; 0: every wait gives up at once, to exercise the failure path)."""
+    load_library().hs_set_wait_limit(int(polls))
 
 
 def eval_workspace_size(B: int, N: int, K: int, V: int, dtype: int) -> int:

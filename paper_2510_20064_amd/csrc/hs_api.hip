@@ -198,6 +198,8 @@ HS_API const char* hs_last_error(void) { return g_err; }
 
 HS_API int hs_version(void) { return 100; }
 
+HS_API void hs_set_wait_limit(int polls) { hs::set_wait_polls(polls); }
+
 HS_API int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t V, int64_t ld,
                             float temperature, float* row_max, float* row_lse,
                             int32_t* row_argmax, void* stream) {

@@ -182,8 +182,8 @@ struct SliceStat {
 // current ones and nothing has to be cleared.
 struct TeamWs {
   size_t epoch;  // control block: uint32 call counter at +0, the call's fail flag (word) at
-                 // +8, the row-set counter (uint32) at +20, the count of teams that have
-                 // finished (uint32) at +24, then a ring of 4 mailbox words per team at +64
+                 // +8, the row-set count (tagged word) at +16, the count of teams that have
+                 // finished (tagged word) at +24, then a ring of 4 mailbox words per team at +64
   size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
   size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
   size_t part;   // [G][N][S] words: per-slice sums of min(p, q_i)
@@ -192,6 +192,10 @@ struct TeamWs {
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Tag of the evaluation call with epoch e: 31 bits (bit 31 of a word's tag half is its taint
+// mark), never 0, the content of a zero-filled workspace.
+__host__ __device__ inline uint32_t tag_of_epoch(uint32_t e) { return (e % 0x7FFFFFFFu) + 1u; }
 
 inline TeamWs team_ws(const TeamGeom& g) {
   TeamWs L;
@@ -227,11 +231,26 @@ __device__ inline void argmax_combine(float& m, int& idx, float m2, int idx2) {
   }
 }
 
+// The offset that the exp2 sums of a part of a row are taken against, m the part's largest
+// logit: an integer-valued float at or above the exact product m c. fl(m c) can lie below it
+// by half an ulp, which for |m c| >= 2^31 would put the largest exponent z c - offset (one
+// fma, exactly rounded) above 128; the nudge by a factor 1 +- 2^-22 (at least 1.5 ulp)
+// keeps every exponent <= 0, so no exp2 and no sum of them overflows, whatever the logits.
+// The largest exponent is then >= -(1 + |m c| 2^-22): exact to fp32 accuracy while
+// |m c| <= 2^28; beyond that a part's sum underflows towards 0 (such a part contributes
+// as a masked one). -inf when m c is -inf: the part has no logit whose scaled value is finite.
+__device__ inline float exp_offset_of(float m, float c) {
+  const float mc = m * c;
+  return ceilf(mc * (mc > 0.0f ? 1.0f + 0x1p-22f : 1.0f - 0x1p-22f));
+}
+
 // Combine two (offset, sum) pairs of exp2 sums: sum_a 2^(o_a - o) + sum_b 2^(o_b - o).
+// A pair whose offset is -inf has no finite logit: its sum is 0, or NaN when it saw a NaN
+// logit, and it is carried as s * 0 so that the NaN survives.
 __device__ inline void lse2_combine(float& o, float& s, float o2, float s2) {
   float on = fmaxf(o, o2);
-  float a = (o == -INFINITY) ? 0.0f : s * __builtin_amdgcn_exp2f(o - on);
-  float b = (o2 == -INFINITY) ? 0.0f : s2 * __builtin_amdgcn_exp2f(o2 - on);
+  float a = (o == -INFINITY) ? s * 0.0f : s * __builtin_amdgcn_exp2f(o - on);
+  float b = (o2 == -INFINITY) ? s2 * 0.0f : s2 * __builtin_amdgcn_exp2f(o2 - on);
   o = on;
   s = a + b;
 }
@@ -263,9 +282,10 @@ struct TailArgs {
   double* R;
   double* p;
   double* c;
-#ifdef HS_TRACE
-  uint64_t* trace;  // per query: 16 phase timestamps of lane 0
-#endif
+  // set when this step follows an evaluation launch of its own: that launch's workspace
+  // epoch (advanced once by it) and fail word; a failed evaluation skips the step
+  const uint32_t* round_epoch;
+  const uint64_t* round_fail;
 };
 int launch_tail(const TailArgs& a, hipStream_t stream);
 
@@ -310,4 +330,7 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
 // Workgroups of the team kernel that one device holds at once for this shape and mode (0 if
 // unknown); the launch needs at least S of them.
 int team_capacity(const TeamGeom& g, bool need_sum, bool need_arg);
+// Polls before a wait inside the team kernel gives up, for launches after this call (negative:
+// the default; 0: every wait gives up at once).
+void set_wait_polls(int polls);
 }  // namespace hs

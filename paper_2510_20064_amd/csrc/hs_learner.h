@@ -18,12 +18,6 @@
 
 namespace hs {
 
-#ifdef HS_TRACE
-#define HS_TSTAMP(k) \
-  if ((threadIdx.x & 63) == 0 && a.trace) a.trace[(size_t)b * 16 + (k)] = __builtin_amdgcn_s_memrealtime()
-#else
-#define HS_TSTAMP(k)
-#endif
 
 // Wave64 reductions of doubles on the DPP network (no LDS crossbar round trip): pairs and
 // quads by quad_perm, 8- and 16-lane groups by the half-row and row mirrors, then the four
@@ -196,6 +190,22 @@ __device__ __forceinline__ void learner_update(double* logw, double* w, double e
   }
 }
 
+// Outputs of query b when its step is skipped because its gamma depends on a word the
+// evaluation lost: EAL, prefix products and losses NaN; the learner state is not touched.
+// Run by all 64 lanes of one wave.
+__device__ inline void mark_query_failed(const TailArgs& a, int b) {
+  const int i = threadIdx.x & 63;
+  if (i >= a.N || a.gamma_src == 0) return;
+  const int64_t qi = (int64_t)b * a.N + i;
+  a.eal[qi] = NAN;
+  if (a.prefix)
+    for (int n = 0; n < a.M; ++n) a.prefix[qi * a.M + n] = NAN;
+  if (a.loss_out) {
+    const int L = a.loss_kind == HS_LOSS_ACCEPT_TOKEN ? a.M : 1;
+    for (int l = 0; l < L; ++l) a.loss_out[((int64_t)l * a.B + b) * a.N + i] = NAN;
+  }
+}
+
 // Learner step for query b, executed by all 64 lanes of one wave (uniform control flow).
 // gamma_lds (optional): the query's gamma as [N][M] floats in LDS, instead of a.alpha / a.agree.
 // pre (optional): the state, already loaded by load_learner_in.
@@ -277,7 +287,6 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
       for (int l = 0; l < L; ++l) a.loss_out[((int64_t)l * a.B + b) * N + i] = lossv[l * N + i];
   }
 
-  HS_TSTAMP(3);
   auto loss_at = [&](int l) -> double {
     if (!act) return 0.0;
     if (a.gamma_src != 0) return lossv[l * N + i];
@@ -285,7 +294,6 @@ __device__ __forceinline__ void tail_query(const TailArgs& a, int b, double* lds
   };
   learner_update(a.logw, a.w, a.eta, a.R, a.p, a.c, b, N, L, in,
                  lds + tail_lds_doubles(a) - kLearnScratch, loss_at);
-  HS_TSTAMP(5);
 }
 
 }  // namespace hs

@@ -5,9 +5,10 @@
 namespace hs {
 
 // Each thread walks its vectors of the row (stride kThreads, U per chunk) keeping a running max,
-// lowest argmax and an exp2 sum against its own integer offset o = ceil(m c): a larger max
-// rescales the sum by 2^(o_old - o_new) exactly, and the next chunk's loads are in flight
-// while the current one is reduced. One block reduction per row at the end.
+// lowest argmax and an exp2 sum against its own integer-valued offset o = exp_offset_of(m, c)
+// (at or above m c, so no exponent is positive): a larger max rescales the sum by
+// 2^(o_old - o_new) exactly, and the next chunk's loads are in flight while the current one is
+// reduced. One block reduction per row at the end.
 template <int DT>
 __global__ __launch_bounds__(kThreads) void hs_softmax_stats_kernel(const char* x, int64_t ld,
                                                                     int64_t V, int64_t nvec,
@@ -46,19 +47,22 @@ __global__ __launch_bounds__(kThreads) void hs_softmax_stats_kernel(const char* 
           m = z[j][e];
           idx = (int)((v0 + (int64_t)j * kThreads + t) * E + e);
         }
-    if (m != -INFINITY) {
-      const float on = ceilf(m * c);
-      if (on != o) {
-        s = (o == -INFINITY) ? 0.0f : ldexpf(s, (int)fmaxf(o - on, -256.0f));
-        o = on;
-      }
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < U; ++j)
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[j][e], c, -o));
-      s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    // o = -inf until the running max scaled by c is finite; until then the sum is taken
+    // against offset 0, where every logit seen so far gives exp2(-inf) = 0 (a -inf logit, or a
+    // finite one whose product with c is below the fp32 range) or NaN (a NaN logit), so the
+    // sum is 0 or NaN and is carried into the first finite offset as s * 0
+    const float on = exp_offset_of(m, c);
+    if (on != o) {
+      s = (o == -INFINITY) ? s * 0.0f : ldexpf(s, (int)fmaxf(o - on, -256.0f));
+      o = on;
     }
+    const float off = o != -INFINITY ? o : 0.0f;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[j][e], c, -off));
+    s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
 #pragma unroll
     for (int j = 0; j < U; ++j) cur[j] = nxt[j];
   }

@@ -9,7 +9,8 @@
 // 256-thread workgroup (thread t owns vector t of every row). The S items of a row set form
 // a team that is resident at the same time:
 //   1. every item reduces its rows (max, lowest argmax, exp2 sum against the slice offset
-//      o = ceil(m c), c = log2(e) / T, an integer) and publishes them as tagged words;
+//      o, an integer-valued float at or above m c, c = log2(e) / T) and publishes them as
+//      tagged words;
 //   2. item s folds the S slice statistics of row s (rows s, s + S, ... when S is smaller
 //      than the row count) into the row's log2 normaliser L = hi + lo and publishes it;
 //   3. every item reads the normalisers and forms its slice's part of sum_v min(p_v, q_v)
@@ -26,7 +27,9 @@
 // The grid holds as many teams as the device keeps resident at once, so all members of a
 // team run together and waiting on one cannot deadlock. Words crossing workgroups carry the
 // call's tag; the last team to finish advances the epoch the tag derives from. Every wait is
-// bounded: a word that never arrives yields NaN (argmax -2), no hang.
+// bounded: a word that never arrives yields NaN (argmax -2), no hang, and everything computed
+// from it carries a taint mark, so the learner step of such a round leaves the learner state
+// unchanged.
 #include <algorithm>
 #include <atomic>
 #include <cstdio>
@@ -36,14 +39,8 @@
 
 namespace hs {
 
-constexpr uint32_t kSpinLimit = 1u << 18;  // polls before a wait gives up (~0.5 s)
-#ifndef HS_POLL_SLEEP
-#define HS_POLL_SLEEP 2
-#endif
-constexpr int kPollSleep = HS_POLL_SLEEP;  // s_sleep units (64 clocks) between polls
-#ifndef HS_CRIT_PRIO
-#define HS_CRIT_PRIO 2
-#endif
+constexpr int kPollSleep = 2;  // s_sleep units (64 clocks) between polls
+constexpr int kCritPrio = 2;   // wave priority of the exchange-critical stages (s_setprio)
 
 struct TeamArgs {
   // What every workgroup reads before its first loads comes first: the first 128 bytes of the
@@ -66,8 +63,9 @@ struct TeamArgs {
   float c;
   FastDiv divNsub;     // by nsub
   uint64_t* fail;      // set, with the call's tag, by the first wait that gives up
-  uint32_t* next_set;  // row sets claimed beyond each team's fixed ones
-  uint32_t* finished;  // teams of this launch that have finished
+  uint32_t polls;      // polls before a wait gives up (0: every wait gives up at once)
+  uint64_t* next_set;  // row sets claimed beyond each team's fixed ones (a tagged count)
+  uint64_t* finished;  // teams of this launch that have finished (a tagged count)
   uint64_t* mbox;      // [teams][4]: the row set of each team's coming items
   uint64_t* stat;  // [sets][D + 1][S][3]
   uint64_t* norm;  // [sets][D + 1][3]
@@ -82,49 +80,52 @@ struct TeamArgs {
   int learn;
   uint64_t* gw;
   TailArgs tail;
-#ifdef HS_TRACE
-  uint64_t* trace;  // [items][8] phase timestamps of workgroup thread 0
-#endif
   RowTable rows;
 };
 
-#ifdef HS_TRACE
-uint64_t* g_trace = nullptr;
-extern "C" __attribute__((visibility("default"))) void hs_debug_set_trace(void* p) {
-  g_trace = reinterpret_cast<uint64_t*>(p);
-}
-#define HS_STAMP(i) \
-  if (t == 0 && A.trace) A.trace[(size_t)(set * S + slot) * 8 + (i)] = __builtin_amdgcn_s_memrealtime()
-// per workgroup, after the item slots: kernel entry and first loads issued
-#define HS_STAMP_WG(i)                                                                  \
-  if (t == 0 && A.trace)                                                                \
-  A.trace[(size_t)A.items * 8 + (size_t)blockIdx.x * 2 + (i)] = __builtin_amdgcn_s_memrealtime()
-#else
-#define HS_STAMP(i)
-#define HS_STAMP_WG(i)
-#endif
 
-// Tag of this call's words: never 0, the content of a zero-filled workspace.
 // (a vector load: a scalar one would hold up the kernel-argument loads waited on with it)
 __device__ inline uint32_t call_tag(const uint32_t* epoch) {
   const uint32_t e =
       __hip_atomic_load(const_cast<uint32_t*>(epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return (uint32_t)__builtin_amdgcn_readfirstlane((int)((e % 0xFFFFFFFFu) + 1u));
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)tag_of_epoch(e));
 }
 
-// The word at w once it carries tag. Bounded: after kSpinLimit polls, or as soon as another
-// wait of this call has given up, the value is 0xFFFFFFFE (a NaN as float, -2 as int); the
-// first wait to give up raises the call's fail flag, so one lost word costs one time-out,
-// not one per wait.
-__device__ inline uint64_t await_word(const uint64_t* w, uint32_t tag, uint64_t* fail) {
-  constexpr uint64_t kLost = 0xFFFFFFFEull << 32;
+// Adds 1 to the count that the word w keeps for the call with this tag and returns the
+// count before (0 for the first add of a call): the word holds (count << 32) | tag, and a
+// word with another tag, from an earlier call or never written, counts as 0. So nothing has
+// to be reset between calls, and whatever a word held before cannot skew this call's count.
+__device__ inline uint32_t tagged_add(uint64_t* w, uint32_t tag) {
+  uint64_t cur = get_word(w);
+  for (;;) {  // each failed exchange means another add succeeded: this ends
+    const uint32_t n = (uint32_t)cur == tag ? (uint32_t)(cur >> 32) : 0u;
+    uint64_t expect = cur;
+    if (__hip_atomic_compare_exchange_strong(w, &expect, ((uint64_t)(n + 1u) << 32) | tag,
+                                             __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      return n;
+    cur = expect;
+  }
+}
+
+// The word at w once it carries tag (its taint mark, if any, kept). Bounded: after `polls`
+// polls, or as soon as another wait of this call has given up, the value is 0xFFFFFFFE (a NaN
+// as float, -2 as int), tainted; the first wait to give up raises the call's fail flag, so one
+// lost word costs one time-out, not one per wait. polls = 0 (set from the host, to test the
+// failure path) makes every wait give up at once.
+__device__ inline uint64_t await_word(const uint64_t* w, uint32_t tag, const TeamArgs& A) {
+  constexpr uint64_t kLost = (0xFFFFFFFEull << 32) | kTaint;
+  if (A.polls == 0) {
+    put_word(A.fail, word_of(1, tag));
+    return kLost | tag;
+  }
   uint64_t v = get_word(w);
-  for (uint32_t n = 1; (uint32_t)v != tag; ++n) {
-    if (n == kSpinLimit) {
-      put_word(fail, word_of(1, tag));
+  for (uint32_t n = 1; tag_of(v) != tag; ++n) {
+    if (n >= A.polls) {
+      put_word(A.fail, word_of(1, tag));
       return kLost | tag;
     }
-    if ((n & 255) == 0 && (uint32_t)get_word(fail) == tag) return kLost | tag;
+    if ((n & 255) == 0 && (uint32_t)get_word(A.fail) == tag) return kLost | tag;
     __builtin_amdgcn_s_sleep(kPollSleep);
     v = get_word(w);
   }
@@ -137,16 +138,21 @@ __device__ inline uint64_t await_word(const uint64_t* w, uint32_t tag, uint64_t*
 __device__ inline uint64_t mbox_word(uint32_t set, int j, uint32_t tag) {
   return ((uint64_t)((set << 6) | ((uint32_t)j & 63u)) << 32) | tag;
 }
-// The row set posted for item j (bounded: `none` after a time-out, raising the fail flag).
-__device__ inline uint32_t await_mbox(const uint64_t* w, int j, uint32_t tag, uint64_t* fail,
+// The row set posted for item j (bounded as await_word: `none` after a time-out, raising the
+// fail flag).
+__device__ inline uint32_t await_mbox(const uint64_t* w, int j, uint32_t tag, const TeamArgs& A,
                                       uint32_t none) {
   auto ok = [&](uint64_t v) {
     return (uint32_t)v == tag && ((uint32_t)(v >> 32) & 63u) == ((uint32_t)j & 63u);
   };
+  if (A.polls == 0) {
+    put_word(A.fail, word_of(1, tag));
+    return none;
+  }
   uint64_t v = get_word(w);
   for (uint32_t n = 1; !ok(v); ++n) {
-    if (n == kSpinLimit || ((n & 255) == 0 && (uint32_t)get_word(fail) == tag)) {
-      put_word(fail, word_of(1, tag));
+    if (n >= A.polls || ((n & 255) == 0 && (uint32_t)get_word(A.fail) == tag)) {
+      put_word(A.fail, word_of(1, tag));
       return none;
     }
     __builtin_amdgcn_s_sleep(kPollSleep);
@@ -157,7 +163,8 @@ __device__ inline uint32_t await_mbox(const uint64_t* w, int j, uint32_t tag, ui
 
 // Fold of row rr of row set `set`: the S slice statistics, two slices per lane per pass
 // (lane j takes slices j, j + 64, ... in order), then the wave. Publishes the row's log2
-// normaliser as hi + lo and its argmax; writes the argmax and agreement outputs.
+// normaliser as hi + lo and its argmax; writes the argmax and agreement outputs. The
+// published words are tainted when any slice word was lost.
 template <int D, bool NEED_SUM, bool NEED_ARG>
 __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int b, int k, int sub,
                                 uint32_t tag, int lane) {
@@ -166,6 +173,7 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
   const uint64_t* base = A.stat + ((int64_t)set * RM + rr) * S * 3;
   float m = -INFINITY, o = -INFINITY, sum = 0.0f;
   int idx = INT_MAX;
+  bool lost = false;
   for (int j0 = 0; j0 < S; j0 += 128) {
     uint64_t w[2][3];
 #pragma unroll
@@ -181,23 +189,27 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
     for (int h = 0; h < 2; ++h) {
       const int j = j0 + lane + 64 * h;
       if (j < S) {
-        if ((uint32_t)w[h][0] != tag) w[h][0] = await_word(base + 3 * j, tag, A.fail);
+        if (tag_of(w[h][0]) != tag) w[h][0] = await_word(base + 3 * j, tag, A);
+        lost |= tainted(w[h][0]);
         const float ms = word_f(w[h][0]);
         if (NEED_ARG) {
-          if ((uint32_t)w[h][2] != tag) w[h][2] = await_word(base + 3 * j + 2, tag, A.fail);
+          if (tag_of(w[h][2]) != tag) w[h][2] = await_word(base + 3 * j + 2, tag, A);
+          lost |= tainted(w[h][2]);
           argmax_combine(m, idx, ms, word_i(w[h][2]));
         } else {
           m = fmaxf(m, ms);
         }
         if (NEED_SUM) {
-          if ((uint32_t)w[h][1] != tag) w[h][1] = await_word(base + 3 * j + 1, tag, A.fail);
-          lse2_combine(o, sum, ceilf(ms * A.c), word_f(w[h][1]));
+          if (tag_of(w[h][1]) != tag) w[h][1] = await_word(base + 3 * j + 1, tag, A);
+          lost |= tainted(w[h][1]);
+          lse2_combine(o, sum, exp_offset_of(ms, A.c), word_f(w[h][1]));
         }
       }
     }
   }
   wave_max<NEED_ARG>(m, idx);
   if (NEED_SUM) wave_lse(o, sum);
+  const uint32_t tt = tag | taint_bits(__ballot(lost) != 0);
   if (lane != 0) return;
   uint64_t* nw = A.norm + ((int64_t)set * RM + rr) * 3;
   if (NEED_SUM) {
@@ -206,21 +218,22 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
     const float hi = o + l2;
     const float bb = hi - o;
     const float lo = (o - (hi - bb)) + (l2 - bb);
-    put_word(nw, word_of(hi, tag));
-    put_word(nw + 1, word_of(lo, tag));
+    put_word(nw, word_of(hi, tt));
+    put_word(nw + 1, word_of(lo, tt));
   }
   if (NEED_ARG) {
-    put_word(nw + 2, word_of(idx, tag));
+    put_word(nw + 2, word_of(idx, tt));
     if (rr == 0) {
       if (sub == 0 && A.argmax_t) A.argmax_t[(int64_t)b * A.K + k] = idx;
     } else {
       const int64_t oi = ((int64_t)b * A.N + sub * D + rr - 1) * A.K + k;
       if (A.argmax_d) A.argmax_d[oi] = idx;
       if (A.agree) {
-        const int it = word_i(await_word(A.norm + (int64_t)set * RM * 3 + 2, tag, A.fail));
+        const uint64_t tw = await_word(A.norm + (int64_t)set * RM * 3 + 2, tag, A);
+        const int it = word_i(tw);
         const bool ag = idx == it && it >= 0;
         A.agree[oi] = (uint8_t)ag;
-        if (A.learn == 2) put_word(A.gw + oi, word_of(ag ? 1.0f : 0.0f, tag));
+        if (A.learn == 2) put_word(A.gw + oi, word_of(ag ? 1.0f : 0.0f, tt | ((uint32_t)tw & kTaint)));
       }
     }
   }
@@ -259,14 +272,17 @@ struct TeamLds {
   float xt[D + 1][kThreads];                  // per-thread max keys / maxima, then exp2 sums
   int xi[NEED_ARG ? D + 1 : 1][kThreads];     // per-thread argmax
   float xs[PT ? D + 1 : 1][kThreads];         // per-thread exp2 sums against the thread's offset
-  int xo[PT ? D + 1 : 1][kThreads];           // that offset (an integer)
+  float xo[PT ? D + 1 : 1][kThreads];         // that offset (an integer-valued float)
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
-  float o[2][D + 1];                          // slice offsets ceil(m c)
+  float o[2][D + 1];                          // slice offsets exp_offset_of(m, c)
   float no[2][D + 1];                         // -exp_offset(o): the addend of the exponents
   float nw[D];     // from the logits: -exp_offset(o_d) - (a_t - a_d), a_x = (o_x - hi_x) - lo_x
+  float dl[D];     // from the logits: a_t - a_d
+  uint32_t wide;   // from the logits: some drafter's |offset| is too large for nw to be exact
   float G[D];      // kept e_v: 2^(a_t - a_d)
   float F[D];      // factor of drafter d's group sum: 2^(a_d) (kept e_v), else 2^(a_t)
   uint32_t next;  // a row set of the team's coming items, posted by thread 0
+  uint32_t taint;  // the item's normalisers include a lost word: its partials are tainted
   // the row table, copied from the kernel arguments once (lane-parallel loads instead of a
   // chain of dependent scalar loads per item)
   const char* ptr[kMaxRows];
@@ -349,9 +365,9 @@ __device__ __forceinline__ void mask_tail(const TeamArgs& A, const ItemPos& q,
   }
 }
 
-// The offset a slice is exponentiated against: ceil(m c) for a slice whose max m is finite (an
-// integer, so that sums against different offsets rescale exactly), 0 for a slice with no
-// finite logit (every e_v is then exp2(-inf) = 0).
+// The offset a slice is exponentiated against: exp_offset_of(m, c) when that is finite (an
+// integer-valued float, so that sums against different offsets rescale exactly), 0 for a slice
+// with no logit whose scaled value is finite (every e_v is then exp2(-inf) = 0).
 __device__ inline float exp_offset(float o) { return o != -INFINITY ? o : 0.0f; }
 
 // min of two values that are >= 0 or +NaN (0 * inf): the unsigned order of the bits is their
@@ -409,9 +425,12 @@ __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
 }
 
 // ---- 1-3. per-thread statistics of every row of item q in one pass (several items per
-// workgroup): the max, the thread's own offset o_t = ceil(m_t c) (0 when its logits are all
-// -inf), and the exp2 sum against it; max keys, sums and offsets to LDS. The offsets are
-// integers, so the group's rescaling of the sums to the slice offset is exact ----
+// workgroup): the max, the thread's own offset o_t (exp_offset_of: integer-valued, at or
+// above m_t c) and the exp2 sum against it; max keys, sums and offsets to LDS. The offsets
+// are integer-valued, so the group's rescaling of the sums to the slice offset is exact. A
+// thread whose m_t c is -inf (logits all -inf, or finite ones whose product with c is below
+// the fp32 range) takes offset 0: each of its logits then gives exp2(-inf) = 0, or NaN for a
+// NaN logit ----
 template <int DT, int D, bool NEED_ARG, typename L>
 __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos& q,
                                                 typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
@@ -436,7 +455,8 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
         m = fmaxf(m, z[e]);
       }
     }
-    const float of = m != -INFINITY ? ceilf(m * A.c) : 0.0f;
+    const float ot = exp_offset_of(m, A.c);
+    const float of = ot != -INFINITY ? ot : 0.0f;
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -of));
@@ -454,7 +474,7 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
       sh.xt[r][t] = __int_as_float(fkey(m));
     }
     sh.xs[r][t] = a0 + a1;
-    sh.xo[r][t] = (int)of;
+    sh.xo[r][t] = of;
   }
 }
 
@@ -513,13 +533,20 @@ template <int D, bool KEPT, typename L>
 __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q, uint32_t tag,
                                             L& sh, int bf, int lane) {
   float h = 0.0f;
-  if (lane < 2 * (q.n + 1))
-    h = word_f(await_word(A.norm + ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1),
-                          tag, A.fail));
+  bool lost = false;
+  if (lane < 2 * (q.n + 1)) {
+    const uint64_t w =
+        await_word(A.norm + ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1), tag, A);
+    h = word_f(w);
+    lost = tainted(w);
+  }
+  const bool any_lost = __ballot(lost) != 0;
+  if (lane == 0) sh.taint = taint_bits(any_lost);
   const float lo = dpp_f<0xB1>(h);  // lane 2r: the lo of row r, from lane 2r + 1
   const float a = (sh.o[bf][min(lane >> 1, D)] - h) - lo;
   const float at = lane_f(a, 0);
-  if (!(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1)) {
+  const bool drafter = !(lane & 1) && lane >= 2 && lane < 2 * (q.n + 1);
+  if (drafter) {
     const int d = (lane >> 1) - 1;
     const bool undefined = at != at || a != a;
     if (KEPT) {
@@ -527,8 +554,16 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
       sh.F[d] = undefined ? NAN : __builtin_amdgcn_exp2f(a);
     } else {
       sh.nw[d] = sh.no[bf][d + 1] - (at - a);
+      sh.dl[d] = at - a;
       sh.F[d] = undefined ? NAN : __builtin_amdgcn_exp2f(at);
     }
+  }
+  if (!KEPT) {
+    // nw_d holds the offset and the small difference a_t - a_d in one float: exact enough
+    // (error <= 2^-17) while |offset| <= 128, the case of ordinary logits; beyond that the
+    // min-sums subtract the difference in a second operation
+    const bool wide = __ballot(drafter && fabsf(sh.no[bf][min(lane >> 1, D)]) > 128.0f) != 0;
+    if (lane == 0) sh.wide = wide;
   }
 }
 
@@ -599,20 +634,29 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
   const float nt = sh.no[bf][0];
 #pragma unroll
   for (int e = 0; e < E; ++e) u[e] = fmaf(u[e], A.c, nt);
+  const bool wide = sh.wide != 0;
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     if (d >= q.n) continue;
     float w[E];
     launder(raw[d + 1]);
     Vec<DT>::unpack(raw[d + 1], w);
-    const float nw = sh.nw[d];
     float y[E];
+    if (!wide) {
+      const float nw = sh.nw[d];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      // both operands are results of arithmetic, so fminf needs no canonicalising. A slice
-      // with no finite logit has every u_v (target) or w_v (drafter) at -inf; nw_d is then
-      // infinite or NaN, and where the other operand becomes NaN it loses to the -inf
-      y[e] = __builtin_amdgcn_exp2f(fminf(u[e], fmaf(w[e], A.c, nw)));
+      for (int e = 0; e < E; ++e) {
+        // both operands are results of arithmetic, so fminf needs no canonicalising. A slice
+        // with no finite logit has every u_v (target) or w_v (drafter) at -inf; nw_d is then
+        // infinite or NaN, and where the other operand becomes NaN it loses to the -inf
+        y[e] = __builtin_amdgcn_exp2f(fminf(u[e], fmaf(w[e], A.c, nw)));
+      }
+    } else {
+      // a large offset: the exact residual z c - o_d first, then the difference
+      const float no = sh.no[bf][d + 1], dl = sh.dl[d];
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        y[e] = __builtin_amdgcn_exp2f(fminf(u[e], fmaf(w[e], A.c, no) - dl));
     }
     // two interleaved sums, started from the first terms (no additions of zero)
     float a0 = y[0], a1 = y[1];
@@ -635,6 +679,7 @@ __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, 
   for (int d = q.s + ((wv + 3) & 3) * S; d < q.n; d += kWaves * S) {
     const uint64_t* src = A.part + ((int64_t)q.g * A.N + q.sub * D + d) * S;
     float v = 0.0f;
+    bool lost = false;
     for (int j0 = 0; j0 < S; j0 += 128) {
       uint64_t w[2];
 #pragma unroll
@@ -644,18 +689,20 @@ __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, 
       for (int h = 0; h < 2; ++h) {
         const int j = j0 + lane + 64 * h;
         if (j < S) {
-          if ((uint32_t)w[h] != tag) w[h] = await_word(src + j, tag, A.fail);
+          if (tag_of(w[h]) != tag) w[h] = await_word(src + j, tag, A);
+          lost |= tainted(w[h]);
           v += word_f(w[h]);
         }
       }
     }
     v = wave_sum_f(v);
-    // clamped to [0, 1]; a NaN (a lost word upstream) stays NaN
+    const uint32_t tt = tag | taint_bits(__ballot(lost) != 0);
+    // clamped to [0, 1]; a NaN (a row without a distribution, or a lost word) stays NaN
     if (lane == 0) {
       const int64_t o = ((int64_t)q.b * A.N + q.sub * D + d) * A.K + q.k;
       const float al = v != v ? v : fminf(fmaxf(v, 0.0f), 1.0f);
       A.alpha[o] = al;
-      if (A.learn == 1) put_word(A.gw + o, word_of(al, tag));
+      if (A.learn == 1) put_word(A.gw + o, word_of(al, tt));
     }
   }
 }
@@ -663,6 +710,8 @@ __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, 
 // ---- 9. learner step of query b, once this workgroup has finished its items: the query's
 // N * K gamma words are gathered into LDS (the team buffers are free by now), then wave 0 runs
 // the step; the learner's state is loaded before the gather, so those loads fly meanwhile.
+// When any gamma word is tainted (computed from a lost word) the step is skipped: the
+// learner state stays as it was and the query's EAL, prefix and loss outputs are NaN.
 // The host only asks for it when the learner's LDS fits in the team's. ----
 template <typename L>
 __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int b, L& sh,
@@ -674,16 +723,25 @@ __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int
   LearnerIn pre{};
   if (t < 64) pre = load_learner_in(A.tail, b);
   __syncthreads();  // the team buffers are no longer read
-  for (int o = t; o < nk; o += kThreads) gam[o] = word_f(await_word(src + o, tag, A.fail));
-  __syncthreads();
-  if (t < 64) tail_query(A.tail, b, lds, gam, &pre);
+  bool lost = false;
+  for (int o = t; o < nk; o += kThreads) {
+    const uint64_t w = await_word(src + o, tag, A);
+    lost |= tainted(w);
+    gam[o] = word_f(w);
+  }
+  const bool skip = __syncthreads_or(lost) != 0;
+  if (t < 64) {
+    if (skip) mark_query_failed(A.tail, b);
+    else tail_query(A.tail, b, lds, gam, &pre);
+  }
   __syncthreads();
 }
 
 // ---- 8. end of a workgroup ----
 // A team's leader finishes after it has folded row 0 of the team's last item, so every member
 // has by then read the call's tag and no claim of the team is outstanding; the last leader to
-// finish advances the epoch and resets the counters (one atomic per team, not per workgroup).
+// finish advances the epoch (one count per team, not per workgroup). The counts are tagged
+// with the call, so none has to be reset.
 // When a wait of this call gave up, every workgroup that sees the fail flag marks every output
 // (alpha NaN, argmax -2, agreement 0): a wave that took a lost word has seen the flag, so each
 // value computed from one is overwritten by the same workgroup, and outputs of row sets that
@@ -694,13 +752,8 @@ __device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool lea
   if (t == 0) {
     const uint64_t fw = get_word(A.fail);
     uint32_t flags = ((uint32_t)fw == tag && (fw >> 32) != 0) ? 2u : 0u;
-    if (leader &&
-        __hip_atomic_fetch_add(A.finished, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-            (uint32_t)teams - 1u) {
-      *A.finished = 0u;  // every team has finished: nothing reads these any more
-      *A.next_set = 0u;
-      *A.epoch = *A.epoch + 1u;
-    }
+    if (leader && tagged_add(A.finished, tag) == (uint32_t)teams - 1u)
+      *A.epoch = *A.epoch + 1u;  // every team has finished: the next call takes a new tag
     sh.next = flags;
   }
   __syncthreads();
@@ -733,7 +786,6 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   __shared__ TeamLds<D, NEED_ARG, NEED_SUM && !SINGLE> sh;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int gi = t >> 4, gl = t & 15;  // 16-lane group gi reduces row gi; gl: lane in it
-  HS_STAMP_WG(0);
   const int S = A.S;
   // every scalar the first loads depend on, requested in one round at entry (otherwise each
   // is loaded just before its first use, one scalar-cache round trip apiece)
@@ -765,15 +817,13 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   // has none every later claim has none either)
   auto claim = [&](int j) __attribute__((always_inline)) {
     if (!dynamic || !leader || t != 0) return;
-    const uint32_t v = (uint32_t)(kStatic * teams) +
-                       __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t v = (uint32_t)(kStatic * teams) + tagged_add(A.next_set, tag);
     put_word(mbox + (j & 3), mbox_word(min(v, nsets), j, tag));
   };
   // thread 0: the row set of the team's item j >= kStatic (nsets: none left) into LDS, so that
   // all waves of the workgroup take the same one after the next barrier
   auto post_set = [&](int j) __attribute__((always_inline)) {
-    if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A.fail, nsets) : nsets;
+    if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A, nsets) : nsets;
   };
 
   if constexpr (!NEED_SUM) {
@@ -781,18 +831,15 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     Raw nxt[RM];
     uint32_t set = (uint32_t)T, next = fixed_set(1);
     fetch_item<DT, D>(A, item_pos(A, set, slot, D), true, sh, nxt);
-    HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
     for (int j = 0; set < nsets; ++j) {
       const ItemPos q = item_pos(A, set, slot, D);
-      HS_STAMP(0);
-      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      __builtin_amdgcn_s_setprio(kCritPrio);
       mask_tail<DT, D>(A, q, nxt);
       thread_max<DT, D, NEED_ARG>(A, q, nxt, sh, t);
       if (j >= 1) post_set(j + 1);
       claim(j + 2);
       __syncthreads();
-      HS_STAMP(1);
       if (j >= 1) next = sh.next;
       if (next < nsets) fetch_item<DT, D>(A, item_pos(A, next, slot, D), true, sh, nxt);
       if (wv * 4 <= q.n) {
@@ -801,18 +848,16 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
         if (gl == 0 && gi <= q.n) publish_row<false, NEED_ARG>(A, q, gi, tag, m, 0.0f, idx, RM);
       }
-      HS_STAMP(3);
       fold_item<D, false, NEED_ARG>(A, q, tag, lane, wv);
       __builtin_amdgcn_s_setprio(0);
       __syncthreads();  // the LDS rows are free for the next item
-      HS_STAMP(7);
       set = next;
     }
     finish(A, tag, leader, teams, sh, t);
   } else {
     // statistics of item q from raw (bf: its offset buffer), published
     auto stats = [&](const ItemPos& q, Raw (&raw)[RM], int bf) __attribute__((always_inline)) {
-      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      __builtin_amdgcn_s_setprio(kCritPrio);
       mask_tail<DT, D>(A, q, raw);
       thread_stats_pt<DT, D, NEED_ARG>(A, q, raw, sh, t);
       __syncthreads();
@@ -821,19 +866,24 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         int idx;
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
         const int r = min(gi, q.n);
-        const float o = ceilf(m * A.c);  // -inf for a slice without a finite logit
-        const int oi = m != -INFINITY ? (int)o : 0;
+        // -inf for a slice without a logit whose product with c is in range
+        const float o = exp_offset_of(m, A.c);
+        const float os = exp_offset(o);
         // the 16 sums of this lane rescaled to the slice offset (exact: powers of two) and
-        // added in sum16's order, four at a time (one 16-byte read of sums and of offsets)
+        // added in sum16's order, four at a time (one 16-byte read of sums and of offsets).
+        // A thread's offset is at most the slice's, unless the thread took offset 0 for a sum
+        // that is 0 or NaN; the shift is kept in [-256, 0], where 2^-256 scales any fp32 sum
+        // to 0, so that huge offset differences neither overflow nor wrap
         typedef float F4 __attribute__((ext_vector_type(4)));
-        typedef int I4 __attribute__((ext_vector_type(4)));
         float c[4];
+        auto sh2 = [&](float x, float y) __attribute__((always_inline)) {
+          return ldexpf(x, (int)fminf(fmaxf(y - os, -256.0f), 0.0f));
+        };
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const F4 x = *reinterpret_cast<const F4*>(&sh.xs[r][64 * i + 4 * gl]);
-          const I4 y = *reinterpret_cast<const I4*>(&sh.xo[r][64 * i + 4 * gl]);
-          c[i] = (ldexpf(x[0], y[0] - oi) + ldexpf(x[1], y[1] - oi)) +
-                 (ldexpf(x[2], y[2] - oi) + ldexpf(x[3], y[3] - oi));
+          const F4 y = *reinterpret_cast<const F4*>(&sh.xo[r][64 * i + 4 * gl]);
+          c[i] = (sh2(x[0], y[0]) + sh2(x[1], y[1])) + (sh2(x[2], y[2]) + sh2(x[3], y[3]));
         }
         const float s = row16_sum((c[0] + c[1]) + (c[2] + c[3]));
         if (gl == 0 && gi <= q.n) {
@@ -854,7 +904,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         const float y = row16_sum(sum16(v));
         if (gl == 0 && gi < q.n)
           put_word(A.part + ((int64_t)q.g * A.N + q.sub * D + gi) * S + q.s,
-                   word_of(y * sh.F[gi], tag));
+                   word_of(y * sh.F[gi], tag | sh.taint));
       }
     };
 
@@ -864,12 +914,10 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     fetch_item<DT, D, SINGLE>(A, q0, true, sh, R0);
     if constexpr (SINGLE) {
       // one item per workgroup: nothing to overlap, so its e_v stay in registers
-      HS_STAMP_WG(1);
       tag = call_tag(A.epoch);  // first needed once the first loads are in flight
       const ItemPos& q = q0;
       float x[RM][Vec<DT>::kElems];
-      HS_STAMP(0);
-      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+      __builtin_amdgcn_s_setprio(kCritPrio);
       mask_tail<DT, D>(A, q, R0);
       thread_max<DT, D, NEED_ARG>(A, q, R0, sh, t);
       __syncthreads();
@@ -879,7 +927,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (rows) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
         if (gl == 0 && gi <= q.n) {
-          const float o = ceilf(m * A.c);  // -inf for a slice without a finite logit
+          const float o = exp_offset_of(m, A.c);  // -inf: no finite logit in the slice
           sh.o[0][gi] = o;
           sh.no[0][gi] = -exp_offset(o);
         }
@@ -893,18 +941,13 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         const float sm = row16_sum(sum16(v));
         if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, sm, idx, RM);
       }
-      HS_STAMP(1);
       fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
       __builtin_amdgcn_s_setprio(0);
-      HS_STAMP(2);
       if (wv == 0) await_norms<D, true>(A, q, tag, sh, 0, lane);
       __syncthreads();
-      HS_STAMP(3);
       thread_minsums_kept<DT, D>(q, x, sh, t);
       __syncthreads();
-      HS_STAMP(4);
       store_partials(q);
-      HS_STAMP(7);
       fold_alpha<D>(A, q, tag, lane, wv);
       if (A.learn)
         for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
@@ -913,7 +956,6 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     }
     fetch_item<DT, D>(A, item_pos(A, min(set1, nsets - 1), slot, D), set1 < nsets, sh,
                       R1);
-    HS_STAMP_WG(1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
     stats(q0, R0, 0);
     // the first item's group reductions read every column of the LDS rows that the next
@@ -929,35 +971,29 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
                     __attribute__((always_inline)) -> bool {
       const int bf = j & 1;
       const ItemPos q = item_pos(A, set, slot, D);
-      HS_STAMP(0);
       // the leader's claim of item j + 3 goes out before the fold and is posted after it, so
       // waiting for its result waits for nothing else
       const bool claiming = dynamic && leader && t == 0 && set2 < nsets;
       uint32_t cv = 0;
       if (claiming)
-        cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __builtin_amdgcn_s_setprio(HS_CRIT_PRIO);
+        cv = tagged_add(A.next_set, tag);
+      __builtin_amdgcn_s_setprio(kCritPrio);
       fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
       __builtin_amdgcn_s_setprio(0);
       if (claiming)
         put_word(mbox + ((j + 3) & 3),
                  mbox_word(min((uint32_t)(kStatic * teams) + cv, nsets), j + 3, tag));
-      HS_STAMP(1);
       fetch_item<DT, D>(A, item_pos(A, min(set2, nsets - 1), slot, D), set2 < nsets, sh,
                         rp);
       if (set1 < nsets) stats(item_pos(A, set1, slot, D), rn, bf ^ 1);
-      HS_STAMP(2);
       // alpha of the previous item, whose partials were stored an iteration ago
       if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv);
       if (set2 < nsets) post_set(j + 3);
       if (wv == 0) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
-      HS_STAMP(3);
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
       __syncthreads();
-      HS_STAMP(4);
       store_partials(q);
-      HS_STAMP(7);
       if (set1 >= nsets) return false;
       pset = set;
       set = set1;
@@ -981,6 +1017,13 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
 // ---- host side -------------------------------------------------------------------------------
 
 namespace {
+
+// Polls before a wait inside the team kernel gives up (about 0.5 s at the default); 0 makes
+// every wait give up at once, which tests of the failure path set from the host.
+constexpr uint32_t kDefaultPolls = 1u << 18;
+std::atomic<uint32_t> g_wait_polls{kDefaultPolls};
+
+uint32_t wait_polls() { return g_wait_polls.load(std::memory_order_relaxed); }
 
 // Workgroups of the team kernel the current device holds at once.
 template <int DT, int D, bool NS, bool NA, bool SG>
@@ -1023,9 +1066,6 @@ int launch_t(TeamArgs A, const TeamGeom& g, hipStream_t stream, bool* learned) {
   A.teams = (int)teams;
   if (single) hs_team_kernel<DT, D, NS, NA, NS><<<(unsigned)P, kThreads, 0, stream>>>(A);
   else hs_team_kernel<DT, D, NS, NA, false><<<(unsigned)P, kThreads, 0, stream>>>(A);
-#ifdef HS_TRACE
-  fprintf(stderr, "team grid %lld S %d items %lld\n", (long long)P, g.S, (long long)g.items);
-#endif
   return HS_OK;
 }
 
@@ -1065,6 +1105,10 @@ struct Launch {
 };
 
 }  // namespace
+
+void set_wait_polls(int polls) {
+  g_wait_polls.store(polls < 0 ? kDefaultPolls : (uint32_t)polls, std::memory_order_relaxed);
+}
 
 int team_capacity(const TeamGeom& g, bool need_sum, bool need_arg) {
   return dispatch<Capacity>(g, need_sum, need_arg);
@@ -1106,8 +1150,9 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.c = c;
   A.epoch = reinterpret_cast<uint32_t*>(ws + L.epoch);
   A.fail = reinterpret_cast<uint64_t*>(ws + L.epoch + 8);
-  A.next_set = reinterpret_cast<uint32_t*>(ws + L.epoch + 20);
-  A.finished = reinterpret_cast<uint32_t*>(ws + L.epoch + 24);
+  A.polls = wait_polls();
+  A.next_set = reinterpret_cast<uint64_t*>(ws + L.epoch + 16);
+  A.finished = reinterpret_cast<uint64_t*>(ws + L.epoch + 24);
   A.mbox = reinterpret_cast<uint64_t*>(ws + L.epoch + 64);
   A.stat = reinterpret_cast<uint64_t*>(ws + L.stat);
   A.norm = reinterpret_cast<uint64_t*>(ws + L.norm);
@@ -1116,22 +1161,20 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.argmax_t = argmax_t;
   A.argmax_d = argmax_d;
   A.agree = agree;
-#ifdef HS_TRACE
-  A.trace = g_trace;
-#endif
   if (tail) {  // the learner step in the same launch, when its LDS fits
     A.learn = tail->gamma_src;
     A.gw = reinterpret_cast<uint64_t*>(ws + L.gw);
     A.tail = *tail;
-#ifdef HS_TRACE
-    A.tail.trace = g_trace ? g_trace + (size_t)g.items * 8 + 2 * kMaxTeams : nullptr;
-#endif
   }
   bool learned = false;
   int rc = dispatch<Launch>(g, need_sum, need_arg, A, g, stream, &learned);
   if (rc) return rc;
   if (hipGetLastError() != hipSuccess) return HS_ERR_HIP;
-  if (tail && !learned) return launch_tail(A.tail, stream);  // a launch of its own
+  if (tail && !learned) {  // a launch of its own, told where to see whether this one failed
+    A.tail.round_epoch = A.epoch;
+    A.tail.round_fail = A.fail;
+    return launch_tail(A.tail, stream);
+  }
   return HS_OK;
 }
 

@@ -40,20 +40,9 @@ struct TopArgs {
   float* gamma;    // [B][N][K]
   uint8_t* hit;    // [B][N][K]
   int32_t* idx;    // [B][N][K][L]
-#ifdef HS_TRACE
-  uint64_t* trace;  // per workgroup of each launch: 16 phase timestamps of wave 0, lane 0
-#endif
   RowTable rows;  // last: the scalars above sit in the first scalar-cache lines
 };
 
-#ifdef HS_TRACE
-uint64_t* g_topl_trace = nullptr;
-#define HS_TSTAMP(base, i)                                                       \
-  if (threadIdx.x == 0 && A.trace)                                               \
-  A.trace[((size_t)(base) + blockIdx.x) * 16 + (i)] = __builtin_amdgcn_s_memrealtime()
-#else
-#define HS_TSTAMP(base, i)
-#endif
 
 constexpr int64_t kNone64 = INT64_MIN;
 constexpr uint64_t kFlip64 = 0x8000000000000000ull;
@@ -303,7 +292,7 @@ __device__ inline void load_unit(const TopArgs& A, const Unit& q, int lane,
 }
 
 // The target's slice statistics: max, lowest argmax (when the greedy hit is wanted), exp2
-// offset fl(max c) and the sum of exp2(z c - offset).
+// offset (exp_offset_of) and the sum of exp2(z c - offset).
 template <int DT>
 __device__ inline void target_unit(const TopArgs& A, const Unit& q, const typename Vec<DT>::Raw (&x)[4],
                                    int lane) {
@@ -330,16 +319,21 @@ __device__ inline void target_unit(const TopArgs& A, const Unit& q, const typena
       }
     }
   }
+  // offset o = exp_offset_of(m, c), at or above m c; a lane whose max scaled by c is -inf (no
+  // finite logit, or only ones below the fp32 range after scaling) sums against 0 instead,
+  // where each of its logits gives exp2(-inf) = 0 or, for a NaN logit, NaN; the combine
+  // carries such a sum as s * 0
   float o = -INFINITY, sum = 0.0f;
-  if (A.want_sum && m != -INFINITY) {
-    o = m * A.c;
+  if (A.want_sum) {
+    o = exp_offset_of(m, A.c);
+    const float off = o != -INFINITY ? o : 0.0f;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t e0 = (q.v0 + i * 64 + lane) * VE;
 #pragma unroll
       for (int e = 0; e < VE; ++e)
-        if (e0 + e < A.V) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[i * VE + e], A.c, -o));
+        if (e0 + e < A.V) acc[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[i * VE + e], A.c, -off));
     }
     sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   }
@@ -477,13 +471,11 @@ __global__ __launch_bounds__(kThreads) void hs_topl_slice_kernel(TopArgs A) {
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform over the wave
   const uint32_t u = blockIdx.x * kWaves + wv;
   if (u >= A.units) return;  // wave-uniform; the waves share no barrier
-  HS_TSTAMP(0, 0);
   typename Vt::Raw x[4];
   const Unit q = decode_unit<DT>(A, u);
   load_unit<DT>(A, q, lane, x);
   if (q.row == 0) target_unit<DT>(A, q, x, lane);
   else drafter_unit<DT>(A, q, x, lane, s_cand[wv], s_lmax[wv]);
-  HS_TSTAMP(0, 1);
 }
 
 // ---- launch 2: global Top_L and the mass ----------------------------------------------------
@@ -508,7 +500,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
   const int L = A.L;
   const int nc = A.S * L;
   const int64_t* ck = A.ckey + r * nc;
-  HS_TSTAMP(A.units, 0);
 
   // loads up front: the target's statistics records, then the candidates (unconditional
   // loads at a clamped index, then a select: no branch between the loads)
@@ -549,7 +540,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
   }
   wave_max<true>(m, am);
   if (A.gamma) wave_lse(o, sm);
-  HS_TSTAMP(A.units, 1);
 
   // theta: the L-th largest lane maximum, by rank counting. The lanes holding a real
   // candidate are distinct and at least L (slice 0 lists L real tokens in L consecutive
@@ -559,7 +549,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
   wave_lds_sync();
   const uint64_t sel = __ballot(mk != kNone64 && rank_in(lm, 64, mk) == L - 1);
   const int64_t theta = sel ? bcast(mk, __builtin_ctzll(sel)) : kNone64 + 1;
-  HS_TSTAMP(A.units, 2);
 
   // the candidates >= theta (at most L lanes hold any), compacted to LDS
   int64_t* key = s_key[wv];
@@ -585,7 +574,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
   }
   if (C <= kMergeCap && lane < 16) key[C + lane] = kNone64;  // padding for the rank counts
   wave_lds_sync();
-  HS_TSTAMP(A.units, 3);
 
   // exact Top_L: per lane a winner flag, its key and its rank
   bool win;
@@ -652,7 +640,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
     wkey = win ? wk[lane] : kNone64;
     rank = rank_in(wk, W, wkey);
   }
-  HS_TSTAMP(A.units, 4);
 
   // the target logits of the winners, gathered from the target row
   const int gidx = (int)(0xFFFFFFFFu - (uint32_t)(uint64_t)wkey);
@@ -675,7 +662,6 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
     if (lane == 0) A.hit[r] = h ? 1 : 0;
   }
   if (A.idx && win) A.idx[r * L + rank] = gidx;
-  HS_TSTAMP(A.units, 5);
 }
 
 // One wave per unit. (A resident grid looping over the units with the next unit's logits in
@@ -690,11 +676,6 @@ void launch_t(const TopArgs& A, int64_t nrows, hipStream_t st) {
 
 }  // namespace
 
-#ifdef HS_TRACE
-extern "C" __attribute__((visibility("default"))) void hs_debug_set_topl_trace(void* p) {
-  g_topl_trace = reinterpret_cast<uint64_t*>(p);
-}
-#endif
 
 size_t topl_ws_bytes(const TeamGeom& g, int L) {
   const size_t rows = (size_t)g.B * g.N * g.K;
@@ -731,9 +712,6 @@ int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool wa
   A.gamma = gamma;
   A.hit = hit;
   A.idx = idx;
-#ifdef HS_TRACE
-  A.trace = g_topl_trace;
-#endif
   if (g.dtype == HS_BF16) launch_t<HS_BF16>(A, (int64_t)nrows, stream);
   else launch_t<HS_F32>(A, (int64_t)nrows, stream);
   return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;

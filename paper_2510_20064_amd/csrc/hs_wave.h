@@ -27,6 +27,13 @@ __device__ inline uint64_t word_of(int x, uint32_t tag) {
 }
 __device__ inline float word_f(uint64_t w) { return __uint_as_float((uint32_t)(w >> 32)); }
 __device__ inline int word_i(uint64_t w) { return (int)(uint32_t)(w >> 32); }
+// Tags are 31-bit. Bit 31 of a word's tag half marks a value computed from a word that was
+// lost (a wait that gave up): the mark travels with the data, so whoever consumes the value,
+// directly or through later words, knows it without any ordering between different words.
+constexpr uint32_t kTaint = 0x80000000u;
+__device__ inline uint32_t tag_of(uint64_t w) { return (uint32_t)w & ~kTaint; }
+__device__ inline bool tainted(uint64_t w) { return ((uint32_t)w & kTaint) != 0; }
+__device__ inline uint32_t taint_bits(bool t) { return t ? kTaint : 0u; }
 
 // ---- wave reductions on the DPP network ----------------------------------------------------
 // Pairs and quads by quad_perm, 8- and 16-lane groups by the half-row and row mirrors, then

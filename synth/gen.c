@@ -89,6 +89,11 @@ static inline double store_one(double x, int dtype, void* out, int64_t idx) {
   return (double)bf16_to_f32(h);
 }
 
+static int cmp_i64(const void* a, const void* b) {
+  const int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+  return (x > y) - (x < y);
+}
+
 /* nboost distinct indices in [0, V), drawn by hashing with rejection of repeats. */
 int synth_boost_indices(uint64_t seed, int64_t round, int64_t b, int64_t k, int64_t V, int nboost,
                         int64_t* idx) {
@@ -118,41 +123,56 @@ int synth_fill(int dtype, int64_t V, int64_t ld, int B, int K, int N, uint64_t s
   if (dtype != SYN_F32 && dtype != SYN_BF16) return -1;
   if (V < 1 || ld < V || B < 1 || K < 1 || N < 1 || nboost < 0 || nboost > V) return -2;
   int64_t nitems = (bk ? nbk : (int64_t)B * K);
-  int64_t total = nitems * nrows;
+  int fail = 0;
+  /* one (b, k) item per task: its target row once (fp64 before rounding), then every
+     requested row of the item from it */
 #pragma omp parallel for schedule(dynamic, 1)
-  for (int64_t it = 0; it < total; ++it) {
-    int64_t ri = it / nitems, p = it % nitems;
-    int row = rows[ri];
+  for (int64_t p = 0; p < nitems; ++p) {
     int64_t b = bk ? bk[2 * p] : p / K;
     int64_t k = bk ? bk[2 * p + 1] : p % K;
-    int64_t base = (ri * nitems + p) * ld;
     uint64_t tkey = synth_row_key(seed, round, 0, b, k);
-    int64_t bidx[64];
+    double* tv = (double*)malloc(sizeof(double) * (size_t)V);
+    if (!tv) {
+#pragma omp atomic write
+      fail = 1;
+      continue;
+    }
+    int64_t bidx[65];
     int nb = nboost < 64 ? nboost : 64;
     if (nb > 0) synth_boost_indices(seed, round, b, k, V, nb, bidx);
-    if (row == 0) {
-      for (int64_t v = 0; v < V; ++v) {
-        double t = sigma_t * normal_at(tkey, v);
-        for (int j = 0; j < nb; ++j)
-          if (bidx[j] == v) t = t + boost;
-        store_one(t, dtype, out, base + v);
+    /* the indices are distinct: walk them in increasing order beside v */
+    qsort(bidx, (size_t)nb, sizeof(int64_t), cmp_i64);
+    bidx[nb] = V;
+    int nxt = 0;
+    for (int64_t v = 0; v < V; ++v) {
+      double t = sigma_t * normal_at(tkey, v);
+      if (bidx[nxt] == v) {
+        t = t + boost;
+        ++nxt;
       }
-    } else {
-      double s = scale[b * N + (row - 1)];
-      uint64_t dkey = synth_row_key(seed, round, row, b, k);
-      float tmpf;
-      uint16_t tmph;
-      for (int64_t v = 0; v < V; ++v) {
-        double t = sigma_t * normal_at(tkey, v);
-        for (int j = 0; j < nb; ++j)
-          if (bidx[j] == v) t = t + boost;
-        double ts = (dtype == SYN_F32) ? store_one(t, dtype, &tmpf, 0) : store_one(t, dtype, &tmph, 0);
-        double d = ts + s * normal_at(dkey, v);
-        store_one(d, dtype, out, base + v);
+      tv[v] = t;
+    }
+    for (int ri = 0; ri < nrows; ++ri) {
+      int row = rows[ri];
+      int64_t base = ((int64_t)ri * nitems + p) * ld;
+      if (row == 0) {
+        for (int64_t v = 0; v < V; ++v) store_one(tv[v], dtype, out, base + v);
+      } else {
+        double s = scale[b * N + (row - 1)];
+        uint64_t dkey = synth_row_key(seed, round, row, b, k);
+        float tmpf;
+        uint16_t tmph;
+        for (int64_t v = 0; v < V; ++v) {
+          double ts = (dtype == SYN_F32) ? store_one(tv[v], dtype, &tmpf, 0)
+                                         : store_one(tv[v], dtype, &tmph, 0);
+          double d = ts + s * normal_at(dkey, v);
+          store_one(d, dtype, out, base + v);
+        }
       }
     }
+    free(tv);
   }
-  return 0;
+  return fail ? -3 : 0;
 }
 
 /* Seeded Fisher-Yates shuffle of 0..n-1 keyed by (seed, tag, b). */

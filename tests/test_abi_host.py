@@ -253,3 +253,19 @@ def test_binding_constants_match_the_header():
              "HS_PLAY_ARGMAX": hs.PLAY_ARGMAX, "HS_PLAY_SAMPLE": hs.PLAY_SAMPLE}
     for name, value in pairs.items():
         assert defs[name] == value, name
+
+
+def test_workspace_control_block_layout(tmp_path):
+    # the header's statement of the control block (epoch at 0, tagged counters at 16 and 24,
+    # mailboxes from 64, aligned disjoint regions) against the library's own layout code,
+    # compiled for the host and run on the CPU
+    import subprocess
+
+    exe = tmp_path / "ws_layout_check"
+    src = os.path.join(ROOT, "tests", "ws_layout_check.cpp")
+    subprocess.check_call(["/opt/rocm/bin/hipcc", "-std=c++17", "-O1", "-I",
+                           os.path.join(ROOT, "include"), "-I",
+                           os.path.join(ROOT, "paper_2510_20064_amd", "csrc"), src, "-o", str(exe)])
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0, out.stdout + out.stderr
+    assert "layout check: ok" in out.stdout

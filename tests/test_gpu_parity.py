@@ -165,27 +165,14 @@ def test_batched_serving_full_size(run):
     run_round_and_check(w, x, mode=mode)
 
 
-def test_draft_tree_full_size_sampled_queries():
+def test_draft_tree_full_size_every_group():
+    # config 4 at its full shape through hs_round with parent pointers: alpha of all 16 queries x
+    # 64 nodes x 16 drafters, the prefix products over the tree and the EAL along each query's
+    # sampled path, all compared with the oracle (Theorem 1, Theorem 3)
     w = WL["draft_tree"]
-    note("draft_tree B16 N16 M64 V151936 bf16 (sampled queries, tree EAL)")
+    note("draft_tree B16 N16 M64 V151936 bf16: hs_round with parent pointers, every group")
     x = synth.generate(w)
-    par = w.parent()
-    pe = w.path_end()
-    got, _ = check_eval(w, x, groups=[(b, k) for b in (0, 7, 15) for k in range(0, 64, 9)])
-    # tree acceptance length on the GPU's alpha for sampled queries: oracle alpha for those queries
-    xd = dev_logits(w, x)
-    out = hs.eval_alpha(xd, temperature=1.0)
-    pe_dev = torch.from_numpy(pe).cuda()
-    acc = hs.accept_len(out["alpha"], parent=par, path_end=pe_dev, want_prefix=True)
-    torch.cuda.synchronize()
-    for b in (3, 12):
-        sub = x[:, b]  # [R][M][V]
-        ref = oracle.evaluate(sub, T=1.0)
-        gam = ref["alpha"].T[None]  # [1][N][M]
-        ra = oracle.accept_len(gam, parent=par, path_end=pe[b:b + 1], want_prefix=True)
-        eal = acc["eal"][b].cpu().numpy()
-        assert np.all(np.abs(eal - ra["eal"][0]) <= EAL_RTOL * ra["eal"][0])
-        assert np.allclose(acc["prefix"][b].cpu().numpy(), ra["prefix"][0], rtol=1e-4, atol=1e-6)
+    run_round_and_check(w, x, parent=w.parent(), path_end=w.path_end())
 
 
 def test_draft_tree_reduced_vocab_full_round():
@@ -194,13 +181,19 @@ def test_draft_tree_reduced_vocab_full_round():
     run_round_and_check(w, synth.generate(w), parent=w.parent(), path_end=w.path_end())
 
 
-def test_large_pool_full_size_sampled_queries():
+def test_large_pool_full_size_stream_across_the_regime_switch():
+    # config 5 at its full shape for 22 consecutive rounds, 490 .. 511, across the regime
+    # switch at 500: every (query, drafter, position) alpha, every EAL, and the learners both
+    # on the oracle's own losses (same input: the weight bar 1e-5 every round) and end to end
+    # from the GPU's own losses. End to end, NormalHedge amplifies fp32-level differences in
+    # alpha: on the oracle alone, alpha perturbed by 2e-7 relative noise moves p by about 1e-5
+    # over 22 rounds from a uniform start (3e-4 over the whole 1000-round stream), so the
+    # end-to-end bound here is 1e-4; Hedge's w stays within 1e-5
     w = WL["large_pool_stream"]
-    note("large_pool_stream B32 N64 K8 V151936 bf16, round 0 and 600 (sampled queries)")
-    for r in (0, 600):
-        x = synth.generate(w, round=r)
-        check_eval(w, x, groups=[(b, k) for b in (0, 31) for k in range(8)] + [(13, 5)])
-        del x
+    r0, n = 490, 22
+    note("large_pool_stream B32 N64 K8 V151936 bf16: rounds %d..%d, every group" % (r0, r0 + n - 1))
+    run_round_and_check(w, synth.generate(w, round=r0), rounds=n,
+                        gen=lambda r: synth.generate(w, round=r0 + r), p_drift_tol=1e-4)
 
 
 def test_large_pool_stream_reduced_vocab_1000_rounds():

@@ -73,6 +73,10 @@ def test_play_and_regret_across_a_regime_switch():
         if r:
             rnd.set_logits(torch.from_numpy(synth.generate(w, round=r)).view(torch.bfloat16).cuda())
         choice = hs.play(rnd.state.p, hs.PLAY_ARGMAX)  # before this round's update
+        # the choice equals the oracle's on the same weights, bit for bit
+        torch.cuda.synchronize()
+        assert np.array_equal(choice.cpu().numpy(),
+                              oracle.play(rnd.state.p.cpu().numpy(), 0).astype(np.int32)), r
         rnd.run()
         reg.update(rnd.loss, choice.view(1, -1), rnd.eal)
         torch.cuda.synchronize()
