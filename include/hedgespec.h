@@ -147,6 +147,25 @@ int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, int N, in
                   int32_t* argmax_t, int32_t* argmax_d, void* workspace, size_t workspace_bytes,
                   void* stream);
 
+/*
+ * hs_eval_alpha_noalloc - hs_eval_alpha for callers that cannot allocate device memory or
+ * pass a workspace: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Arguments, outputs, results and errors are those of hs_eval_alpha (same kernels)
+ * without the workspace: the exchange words live in a fixed array of
+ * hs_eval_alpha_noalloc_max_workspace() bytes (64 MiB) that the library's code object holds
+ * on every device it runs on until the process ends (zero when loaded, and never in need of
+ * clearing: its words are tagged per call). A shape whose workspace
+ * (hs_eval_alpha_workspace_size) is larger gets HS_ERR_WORKSPACE before anything is enqueued.
+ * The first call on a device looks up that device's copy (hipGetSymbolAddress); no call
+ * allocates. Calls on one device share the array: calls that overlap in time on one device
+ * (different streams, or threads without ordering) race and give undefined results; calls
+ * ordered on one stream are safe.
+ */
+int hs_eval_alpha_noalloc(const hs_view* target, const hs_view* drafters_host, int N, int B,
+                          int K, int64_t V, int dtype, float temperature, int mode, float* alpha,
+                          uint8_t* agree, int32_t* argmax_t, int32_t* argmax_d, void* stream);
+size_t hs_eval_alpha_noalloc_max_workspace(void);
+
 /* Bytes of device workspace hs_eval_topl needs for this shape (0 on invalid shapes). */
 size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dtype);
 

@@ -72,6 +72,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_eval_alpha_workspace_size.argtypes = [I, I, I, I64, I]
     lib.hs_eval_alpha_workspace_size.restype = SZ
     lib.hs_eval_alpha.argtypes = [VP, VP, I, I, I, I64, I, F, I, P, P, P, P, P, SZ, P]
+    lib.hs_eval_alpha_noalloc.argtypes = [VP, VP, I, I, I, I64, I, F, I, P, P, P, P, P]
+    lib.hs_eval_alpha_noalloc_max_workspace.argtypes = []
+    lib.hs_eval_alpha_noalloc_max_workspace.restype = SZ
     lib.hs_eval_topl_workspace_size.argtypes = [I, I, I, I64, I, I]
     lib.hs_eval_topl_workspace_size.restype = SZ
     lib.hs_eval_topl.argtypes = [VP, VP, I, I, I, I64, I, I, F, I, P, P, P, P, SZ, P]
@@ -87,7 +90,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
-    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_eval_topl", "hs_play", "hs_regret_update",
+    for name in ["hs_softmax_stats", "hs_eval_alpha", "hs_eval_alpha_noalloc", "hs_eval_topl", "hs_play", "hs_regret_update",
                  "hs_accept_len", "hs_hedge_update",
                  "hs_normalhedge_update", "hs_round", "hs_delayed_update", "hs_version"]:
         getattr(lib, name).restype = I
@@ -213,6 +216,31 @@ def eval_alpha(target: torch.Tensor, drafters=None, V: Optional[int] = None,
                              _ptr(o.get("alpha")), _ptr(o.get("agree")), _ptr(o.get("argmax_t")),
                              _ptr(o.get("argmax_d")), _ptr(workspace), workspace.numel(),
                              _stream(stream)))
+    return o
+
+
+def eval_alpha_noalloc(target: torch.Tensor, drafters=None, V: Optional[int] = None,
+                       temperature: float = 1.0, mode: int = SAMPLE, out: Optional[dict] = None,
+                       stream=None):
+    """hs_eval_alpha_noalloc: hs_eval_alpha with the library's fixed workspace array instead of
+    a caller's workspace. `out` holds preallocated outputs (alpha, agree, argmax_t, argmax_d;
+    those present are filled); nothing is allocated when it covers what the mode requires."""
+    lib = load_library()
+    t, ds = _split_logits(target, drafters)
+    B, K, ld = t.shape
+    N = len(ds)
+    V = ld if V is None else V
+    o = {} if out is None else out
+    if mode == SAMPLE and "alpha" not in o:
+        o["alpha"] = torch.empty((B, N, K), dtype=torch.float32, device=t.device)
+    if mode == GREEDY and "agree" not in o:
+        o["agree"] = torch.empty((B, N, K), dtype=torch.uint8, device=t.device)
+    tv = _view(t)
+    dv = (hs_view * N)(*[_view(d) for d in ds])
+    _check(lib.hs_eval_alpha_noalloc(ctypes.byref(tv), dv, N, B, K, V, _dtype_code(t),
+                                     temperature, mode, _ptr(o.get("alpha")), _ptr(o.get("agree")),
+                                     _ptr(o.get("argmax_t")), _ptr(o.get("argmax_d")),
+                                     _stream(stream)))
     return o
 
 

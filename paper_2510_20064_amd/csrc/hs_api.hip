@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "hs_internal.h"
 
 #define HS_API extern "C" __attribute__((visibility("default")))
@@ -236,6 +238,74 @@ HS_API int hs_eval_alpha(const hs_view* target, const hs_view* drafters_host, in
   hs::RowTable rows;
   int rc = validate_eval(q, &g, &rows);
   if (rc) return rc;
+  if ((rc = check_capacity(q, g))) return rc;
+  rc = run_eval(q, g, rows, nullptr, (hipStream_t)stream);
+  return rc ? rc : ok();
+}
+
+namespace {
+
+// ---- the evaluation workspace of hs_eval_alpha_noalloc ----------------------------------------
+// A file-scope device array, zero-initialised when the code object is loaded; every device the
+// library runs on holds its own copy for the life of the process. In host code its name is only
+// a stand-in: the device address of each device's copy comes from hipGetSymbolAddress, looked
+// up once per device (with that device current) and kept here.
+constexpr size_t kStaticWsBytes = (size_t)64 << 20;
+__device__ __align__(256) unsigned char scratch[kStaticWsBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];  // per device ordinal; nullptr until looked up
+
+// This device's copy of `scratch` (nullptr with an error message if it cannot be found).
+void* static_workspace() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    fail(HS_ERR_HIP, "hs_eval_alpha_noalloc: no current HIP device");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t rc = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (rc != hipSuccess || !p) {
+      fail(HS_ERR_HIP, "hs_eval_alpha_noalloc: hipGetSymbolAddress failed on device %d: %s", dev,
+           hipGetErrorString(rc));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+HS_API size_t hs_eval_alpha_noalloc_max_workspace(void) { return kStaticWsBytes; }
+
+HS_API int hs_eval_alpha_noalloc(const hs_view* target, const hs_view* drafters_host, int N,
+                                 int B, int K, int64_t V, int dtype, float temperature, int mode,
+                                 float* alpha, uint8_t* agree, int32_t* argmax_t,
+                                 int32_t* argmax_d, void* stream) {
+  // the shape's workspace must fit in the fixed array: checked before any HIP call
+  hs::TeamGeom g;
+  if (!hs::team_geom(B, N, K, V, dtype, &g)) {
+    EvalReq probe{target, drafters_host, N, B, K, V, dtype, temperature, mode, alpha, agree,
+                  argmax_t, argmax_d, reinterpret_cast<void*>(256), kStaticWsBytes};
+    hs::RowTable rows;
+    return validate_eval(probe, &g, &rows);  // the shape's own error code and message
+  }
+  const size_t need = hs::team_ws(g).total;
+  if (need > kStaticWsBytes)
+    return fail(HS_ERR_WORKSPACE,
+                "hs_eval_alpha_noalloc: this shape needs %zu bytes of workspace, more than the "
+                "fixed %zu (use hs_eval_alpha with a workspace of its own)",
+                need, kStaticWsBytes);
+  EvalReq q{target, drafters_host, N, B, K, V, dtype, temperature, mode, alpha, agree, argmax_t,
+            argmax_d, reinterpret_cast<void*>(256), kStaticWsBytes};
+  hs::RowTable rows;
+  int rc = validate_eval(q, &g, &rows);  // every host-side check, before the first HIP call
+  if (rc) return rc;
+  q.ws = static_workspace();
+  if (!q.ws) return HS_ERR_HIP;
   if ((rc = check_capacity(q, g))) return rc;
   rc = run_eval(q, g, rows, nullptr, (hipStream_t)stream);
   return rc ? rc : ok();

@@ -269,3 +269,25 @@ def test_workspace_control_block_layout(tmp_path):
     out = subprocess.run([str(exe)], capture_output=True, text=True)
     assert out.returncode == 0, out.stdout + out.stderr
     assert "layout check: ok" in out.stdout
+
+
+def test_noalloc_workspace_limit_and_validation():
+    # hs_eval_alpha_noalloc: its fixed workspace size, a shape that needs more is refused with
+    # HS_ERR_WORKSPACE, and an invalid shape gets hs_eval_alpha's own error, all on the host
+    # before any HIP call (the pointers are fakes, never dereferenced)
+    lib = hs.load_library()
+    cap = int(lib.hs_eval_alpha_noalloc_max_workspace())
+    assert cap == 64 << 20
+    assert lib.hs_eval_alpha_workspace_size(32, 64, 8, 151936, 1) <= cap  # the large pool fits
+    assert lib.hs_eval_alpha_workspace_size(64, 64, 8, 151936, 1) > cap
+
+    def call(B, N, K, V, T=1.0):
+        tv = hs.hs_view(FAKE, K * 151936, 151936)
+        return lib.hs_eval_alpha_noalloc(ctypes.byref(tv), _views(N, sb=K * 151936), N, B, K, V, 1,
+                                         T, 0, FAKE, None, None, None, None)
+
+    assert call(64, 64, 8, 151936) == 7  # HS_ERR_WORKSPACE
+    assert b"hs_eval_alpha_noalloc" in lib.hs_last_error()
+    assert call(0, 8, 8, 151936) == 2  # HS_ERR_SHAPE
+    assert call(1, 65, 8, 151936) == 8  # HS_ERR_LIMIT
+    assert call(1, 8, 8, 151936, T=0.0) == 5  # HS_ERR_TEMPERATURE
