@@ -241,7 +241,15 @@ __device__ inline void argmax_combine(float& m, int& idx, float m2, int idx2) {
 // as a masked one). -inf when m c is -inf: the part has no logit whose scaled value is finite.
 __device__ inline float exp_offset_of(float m, float c) {
   const float mc = m * c;
-  return ceilf(mc * (mc > 0.0f ? 1.0f + 0x1p-22f : 1.0f - 0x1p-22f));
+  return mc > -INFINITY ? ceilf(fmaf(fabsf(mc), 0x1p-22f, mc)) : -INFINITY;
+}
+
+// fp32 -> int32 with the hardware's saturation (out-of-range values clamp to INT_MIN or
+// INT_MAX, NaN gives 0), which the C++ conversion does not promise.
+__device__ inline int cvt_i32_sat(float x) {
+  int r;
+  asm("v_cvt_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
 }
 
 // Combine two (offset, sum) pairs of exp2 sums: sum_a 2^(o_a - o) + sum_b 2^(o_b - o).

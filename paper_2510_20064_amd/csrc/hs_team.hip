@@ -64,7 +64,7 @@ struct TeamArgs {
   FastDiv divNsub;     // by nsub
   uint64_t* fail;      // set, with the call's tag, by the first wait that gives up
   uint32_t polls;      // polls before a wait gives up (0: every wait gives up at once)
-  uint64_t* next_set;  // row sets claimed beyond each team's fixed ones (a tagged count)
+  uint32_t* next_set;  // row sets claimed beyond each team's fixed ones
   uint64_t* finished;  // teams of this launch that have finished (a tagged count)
   uint64_t* mbox;      // [teams][4]: the row set of each team's coming items
   uint64_t* stat;  // [sets][D + 1][S][3]
@@ -272,7 +272,7 @@ struct TeamLds {
   float xt[D + 1][kThreads];                  // per-thread max keys / maxima, then exp2 sums
   int xi[NEED_ARG ? D + 1 : 1][kThreads];     // per-thread argmax
   float xs[PT ? D + 1 : 1][kThreads];         // per-thread exp2 sums against the thread's offset
-  float xo[PT ? D + 1 : 1][kThreads];         // that offset (an integer-valued float)
+  int xo[PT ? D + 1 : 1][kThreads];           // that offset (saturated to int32)
   float xp[D][kThreads];                      // per-thread min-sums of each drafter
   float o[2][D + 1];                          // slice offsets exp_offset_of(m, c)
   float no[2][D + 1];                         // -exp_offset(o): the addend of the exponents
@@ -456,7 +456,7 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
       }
     }
     const float ot = exp_offset_of(m, A.c);
-    const float of = ot != -INFINITY ? ot : 0.0f;
+    const float of = ot != -INFINITY ? ot : 0.0f;  // NaN-free: m is never NaN
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -of));
@@ -474,7 +474,7 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
       sh.xt[r][t] = __int_as_float(fkey(m));
     }
     sh.xs[r][t] = a0 + a1;
-    sh.xo[r][t] = of;
+    sh.xo[r][t] = cvt_i32_sat(of);
   }
 }
 
@@ -515,11 +515,17 @@ __device__ __forceinline__ void publish_row(const TeamArgs& A, const ItemPos& q,
   if (NEED_ARG) put_word(wp + 2, word_of(idx, tag));
 }
 
-// ---- 4. fold duty: rows s, s + S, ... of the row set, spread over the waves ----
+// Slot s's duty index for an item whose duties start at slot rot: duties are numbered from
+// rot on, so that the row and alpha folds move round the team from item to item instead of
+// falling on the same few members every time (the team goes at its slowest member's pace).
+__device__ inline int duty_index(int s, int rot, int S) { return s >= rot ? s - rot : s - rot + S; }
+
+// ---- 4. fold duty: rows i, i + S, ... of the row set (i = the slot's duty index for the
+// item's rotation rot), spread over the waves ----
 template <int D, bool NEED_SUM, bool NEED_ARG>
 __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                          int lane, int wv) {
-  for (int rr = q.s + wv * A.S; rr <= q.n; rr += kWaves * A.S)
+                                          int lane, int wv, int rot = 0) {
+  for (int rr = duty_index(q.s, rot, A.S) + wv * A.S; rr <= q.n; rr += kWaves * A.S)
     fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
 }
 
@@ -623,10 +629,10 @@ __device__ __forceinline__ void thread_minsums_kept(const ItemPos& q,
 // z_d,v c + nw_d; one fma, one min, one exp2 and one add per drafter logit. The factor 2^(a_t)
 // is applied to the group sum. Identical rows give nw_d = -o_t, so both operands agree
 // bitwise ----
-template <int DT, int D, typename L>
-__device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos& q,
-                                               typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
-                                               int bf, int t) {
+template <int DT, int D, bool WIDE, typename L>
+__device__ __forceinline__ void thread_minsums_form(const TeamArgs& A, const ItemPos& q,
+                                                    typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                                    int bf, int t) {
   constexpr int E = Vec<DT>::kElems;
   float u[E];
   launder(raw[0]);
@@ -634,7 +640,6 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
   const float nt = sh.no[bf][0];
 #pragma unroll
   for (int e = 0; e < E; ++e) u[e] = fmaf(u[e], A.c, nt);
-  const bool wide = sh.wide != 0;
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     if (d >= q.n) continue;
@@ -642,7 +647,7 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
     launder(raw[d + 1]);
     Vec<DT>::unpack(raw[d + 1], w);
     float y[E];
-    if (!wide) {
+    if (!WIDE) {
       const float nw = sh.nw[d];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
@@ -668,15 +673,24 @@ __device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos&
     sh.xp[d][t] = a0 + a1;
   }
 }
+// The form is chosen once per item (uniform), so that each copy of the loop is straight-line
+// over all drafters and the compiler can interleave them.
+template <int DT, int D, typename L>
+__device__ __forceinline__ void thread_minsums(const TeamArgs& A, const ItemPos& q,
+                                               typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
+                                               int bf, int t) {
+  if (sh.wide == 0) thread_minsums_form<DT, D, false>(A, q, raw, sh, bf, t);
+  else thread_minsums_form<DT, D, true>(A, q, raw, sh, bf, t);
+}
 
 // ---- 7. alpha of the set's drafters from the slice partials: output d is summed by slot
 // d mod S (wave 1 for the first), lane l taking slices l, l + 64, ... in order, then across the
 // wave ----
 template <int D>
 __device__ __forceinline__ void fold_alpha(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                           int lane, int wv) {
+                                           int lane, int wv, int rot = 0) {
   const int S = A.S;
-  for (int d = q.s + ((wv + 3) & 3) * S; d < q.n; d += kWaves * S) {
+  for (int d = duty_index(q.s, rot, S) + ((wv + 3) & 3) * S; d < q.n; d += kWaves * S) {
     const uint64_t* src = A.part + ((int64_t)q.g * A.N + q.sub * D + d) * S;
     float v = 0.0f;
     bool lost = false;
@@ -740,8 +754,8 @@ __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int
 // ---- 8. end of a workgroup ----
 // A team's leader finishes after it has folded row 0 of the team's last item, so every member
 // has by then read the call's tag and no claim of the team is outstanding; the last leader to
-// finish advances the epoch (one count per team, not per workgroup). The counts are tagged
-// with the call, so none has to be reset.
+// finish advances the epoch and resets the row-set counter (one count per team, not per
+// workgroup; the count of finished teams is tagged with the call, so it needs no reset).
 // When a wait of this call gave up, every workgroup that sees the fail flag marks every output
 // (alpha NaN, argmax -2, agreement 0): a wave that took a lost word has seen the flag, so each
 // value computed from one is overwritten by the same workgroup, and outputs of row sets that
@@ -752,8 +766,10 @@ __device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool lea
   if (t == 0) {
     const uint64_t fw = get_word(A.fail);
     uint32_t flags = ((uint32_t)fw == tag && (fw >> 32) != 0) ? 2u : 0u;
-    if (leader && tagged_add(A.finished, tag) == (uint32_t)teams - 1u)
-      *A.epoch = *A.epoch + 1u;  // every team has finished: the next call takes a new tag
+    if (leader && tagged_add(A.finished, tag) == (uint32_t)teams - 1u) {
+      *A.next_set = 0u;           // every team has finished: nothing claims any more
+      *A.epoch = *A.epoch + 1u;   // the next call takes a new tag
+    }
     sh.next = flags;
   }
   __syncthreads();
@@ -794,6 +810,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
                "s"(A.divK.s1), "s"(A.divK.s2), "s"(A.V), "s"(A.dd), "s"(A.base0), "s"(A.base1),
                "s"(A.sb0), "s"(A.sk0), "s"(A.sb1), "s"(A.sk1), "s"(A.epoch));
   const int teams = A.teams;
+  // consecutive workgroups form a team; the workgroups that share a CU (w, w + CUs, ...)
+  // then belong to different teams, so that one team's waits leave the CU to the others
   const int T = (int)fdiv(blockIdx.x, A.divS), slot = blockIdx.x - T * S;
   const uint32_t nsets = fdiv((uint32_t)A.items, A.divS);
   constexpr int kStatic = NEED_SUM ? 3 : 2;  // items per team with a fixed row set
@@ -817,13 +835,24 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
   // has none every later claim has none either)
   auto claim = [&](int j) __attribute__((always_inline)) {
     if (!dynamic || !leader || t != 0) return;
-    const uint32_t v = (uint32_t)(kStatic * teams) + tagged_add(A.next_set, tag);
+    const uint32_t v = (uint32_t)(kStatic * teams) +
+                       __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
     put_word(mbox + (j & 3), mbox_word(min(v, nsets), j, tag));
   };
   // thread 0: the row set of the team's item j >= kStatic (nsets: none left) into LDS, so that
   // all waves of the workgroup take the same one after the next barrier
   auto post_set = [&](int j) __attribute__((always_inline)) {
     if (t == 0) sh.next = dynamic ? await_mbox(mbox + (j & 3), j, tag, A, nsets) : nsets;
+  };
+  // first slot of the row or alpha fold duties of row set `set` (several items per workgroup):
+  // (set (D + 1) + extra) mod S, so consecutive items use different members, and the alpha
+  // folds of an item start where its row folds end. (The argmax-only kernel keeps row 0 on
+  // the leader, which bounds how far the leader's claims run ahead of its team; in the alpha
+  // kernels every member waits for the normalisers of each item, which bounds it there.)
+  auto rotation = [&](uint32_t s, int extra) __attribute__((always_inline)) -> int {
+    const uint32_t x = s * (uint32_t)RM + (uint32_t)extra;
+    return (int)(x - fdiv(x, A.divS) * (uint32_t)S);
   };
 
   if constexpr (!NEED_SUM) {
@@ -868,22 +897,23 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         const int r = min(gi, q.n);
         // -inf for a slice without a logit whose product with c is in range
         const float o = exp_offset_of(m, A.c);
-        const float os = exp_offset(o);
+        const int os = cvt_i32_sat(exp_offset(o));
         // the 16 sums of this lane rescaled to the slice offset (exact: powers of two) and
         // added in sum16's order, four at a time (one 16-byte read of sums and of offsets).
         // A thread's offset is at most the slice's, unless the thread took offset 0 for a sum
-        // that is 0 or NaN; the shift is kept in [-256, 0], where 2^-256 scales any fp32 sum
-        // to 0, so that huge offset differences neither overflow nor wrap
+        // that is 0 or NaN. Offsets beyond the int32 range saturate, and a difference that
+        // wraps needs |offset| >= 2^30, where the thread's exponents are all <= -256 and its
+        // sum is exactly 0 (or NaN): ldexp of 0 or NaN is 0 or NaN whatever the shift
         typedef float F4 __attribute__((ext_vector_type(4)));
+        typedef int I4 __attribute__((ext_vector_type(4)));
         float c[4];
-        auto sh2 = [&](float x, float y) __attribute__((always_inline)) {
-          return ldexpf(x, (int)fminf(fmaxf(y - os, -256.0f), 0.0f));
-        };
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const F4 x = *reinterpret_cast<const F4*>(&sh.xs[r][64 * i + 4 * gl]);
-          const F4 y = *reinterpret_cast<const F4*>(&sh.xo[r][64 * i + 4 * gl]);
-          c[i] = (sh2(x[0], y[0]) + sh2(x[1], y[1])) + (sh2(x[2], y[2]) + sh2(x[3], y[3]));
+          const I4 y = *reinterpret_cast<const I4*>(&sh.xo[r][64 * i + 4 * gl]);
+          auto d = [&](int yi) { return (int)((uint32_t)yi - (uint32_t)os); };  // wraps
+          c[i] = (ldexpf(x[0], d(y[0])) + ldexpf(x[1], d(y[1]))) +
+                 (ldexpf(x[2], d(y[2])) + ldexpf(x[3], d(y[3])));
         }
         const float s = row16_sum((c[0] + c[1]) + (c[2] + c[3]));
         if (gl == 0 && gi <= q.n) {
@@ -961,7 +991,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     // the first item's group reductions read every column of the LDS rows that the next
     // item's per-thread statistics overwrite, and nothing else in the first iteration waits
     // for the whole workgroup before those writes (later items are kept apart by the
-    // barriers around the min-sums)
+    // barriers around the min-sums); after it every wave has published its rows
     __syncthreads();
 
     uint32_t pset = nsets;  // the team's previous item, whose alpha is still to be folded
@@ -976,9 +1006,9 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       const bool claiming = dynamic && leader && t == 0 && set2 < nsets;
       uint32_t cv = 0;
       if (claiming)
-        cv = tagged_add(A.next_set, tag);
+        cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __builtin_amdgcn_s_setprio(kCritPrio);
-      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
+      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, rotation(set, 0));
       __builtin_amdgcn_s_setprio(0);
       if (claiming)
         put_word(mbox + ((j + 3) & 3),
@@ -987,7 +1017,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
                         rp);
       if (set1 < nsets) stats(item_pos(A, set1, slot, D), rn, bf ^ 1);
       // alpha of the previous item, whose partials were stored an iteration ago
-      if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv);
+      if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv, rotation(pset, RM));
       if (set2 < nsets) post_set(j + 3);
       if (wv == 0) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
@@ -1007,7 +1037,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (!iter(j + 1, R1, R2, R0)) break;
       if (!iter(j + 2, R2, R0, R1)) break;
     }
-    fold_alpha<D>(A, item_pos(A, set, slot, D), tag, lane, wv);
+    fold_alpha<D>(A, item_pos(A, set, slot, D), tag, lane, wv, rotation(set, RM));
     if (A.learn)
       for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
     finish(A, tag, leader, teams, sh, t);
@@ -1151,7 +1181,7 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.epoch = reinterpret_cast<uint32_t*>(ws + L.epoch);
   A.fail = reinterpret_cast<uint64_t*>(ws + L.epoch + 8);
   A.polls = wait_polls();
-  A.next_set = reinterpret_cast<uint64_t*>(ws + L.epoch + 16);
+  A.next_set = reinterpret_cast<uint32_t*>(ws + L.epoch + 16);
   A.finished = reinterpret_cast<uint64_t*>(ws + L.epoch + 24);
   A.mbox = reinterpret_cast<uint64_t*>(ws + L.epoch + 64);
   A.stat = reinterpret_cast<uint64_t*>(ws + L.stat);
