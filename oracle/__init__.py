@@ -18,7 +18,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hs_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# HS_ORACLE_LIB: a build of hs_oracle.c to load instead (the sanitizer test's instrumented one)
+_LIB = os.environ.get("HS_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 F32, BF16 = 0, 1
 LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
@@ -38,7 +39,8 @@ def build(force: bool = False) -> str:
 def _load():
     global _lib
     if _lib is None:
-        build()
+        if not os.environ.get("HS_ORACLE_LIB"):
+            build()
         lib = ctypes.CDLL(_LIB)
         P, I, I64, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
         lib.or_row_stats.argtypes = [P, I, I64, D, P, P, P]

@@ -16,7 +16,8 @@ from typing import Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libhedgespec.so")
+# HS_LIBRARY: another build of the library to load (e.g. one with host sanitizers)
+LIB_PATH = os.environ.get("HS_LIBRARY") or os.path.join(_HERE, "libhedgespec.so")
 
 HS_OK = 0
 HS_F32, HS_BF16 = 0, 1
