@@ -391,6 +391,23 @@ int hs_version(void);
  */
 void hs_set_wait_limit(int polls);
 
+/*
+ * hs_stream_read - measurement aid, not a step of the method: reads every 16-byte vector of a
+ * device buffer once and writes, for each wave, the XOR of the 32-bit words it read. Timed
+ * over a buffer far larger than the 256 MB Infinity Cache, it gives the rate at which this
+ * device streams resident data from HBM: the practical ceiling the evaluation kernels'
+ * achieved bandwidth is compared with (they, too, read every logit once).
+ *   x:      device pointer, 16-byte aligned; bytes: its size, a positive multiple of 16.
+ *   grid:   workgroups of 256 threads (1..65536); they stride over the buffer together.
+ *   unroll: 1, 2, 4 or 8 loads of 16 bytes in flight per thread.
+ *   nontemporal: nonzero for loads that tell the caches not to keep the data.
+ *   out:    device pointer to grid * 4 uint32 words (written; the caller owns it).
+ *   stream: hipStream_t or NULL. Asynchronous; errors: HS_ERR_NULL, HS_ERR_ALIGN,
+ *           HS_ERR_SHAPE, HS_ERR_ARG, HS_ERR_HIP.
+ */
+int hs_stream_read(const void* x, size_t bytes, int grid, int unroll, int nontemporal,
+                   uint32_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -88,6 +88,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_delayed_update.argtypes = [P, P, I, I, I, I, P, I64, P, P, P, P, D, P, P, P, P, P, P]
     lib.hs_set_wait_limit.argtypes = [I]
     lib.hs_set_wait_limit.restype = None
+    lib.hs_stream_read.argtypes = [P, SZ, I, I, I, P, P]
     lib.hs_status_string.argtypes = [I]
     lib.hs_status_string.restype = ctypes.c_char_p
     lib.hs_last_error.restype = ctypes.c_char_p
@@ -163,6 +164,21 @@ def set_wait_limit(polls: int) -> None:
     """hs_set_wait_limit: polls before a wait inside the evaluation kernel gives up (negative:
     the default; 0: every wait gives up at once, to exercise the failure path)."""
     load_library().hs_set_wait_limit(int(polls))
+
+
+def stream_read(x: torch.Tensor, grid: int = 2048, unroll: int = 4, nontemporal: bool = False,
+                out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """hs_stream_read: read every byte of the contiguous device tensor x once (a measurement
+    aid: the device's streaming read rate); returns the grid * 4 per-wave XOR words."""
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    if out is None:
+        out = torch.empty(grid * 4, dtype=torch.int32, device=x.device)
+    elif out.numel() < grid * 4 or out.dtype != torch.int32 or out.device != x.device:
+        raise ValueError("out: at least grid * 4 int32 words on x's device")
+    _check(load_library().hs_stream_read(_ptr(x), x.numel() * x.element_size(), grid, unroll,
+                                         int(bool(nontemporal)), _ptr(out), _stream(stream)))
+    return out
 
 
 def eval_workspace_size(B: int, N: int, K: int, V: int, dtype: int) -> int:

@@ -202,6 +202,28 @@ HS_API int hs_version(void) { return 100; }
 
 HS_API void hs_set_wait_limit(int polls) { hs::set_wait_polls(polls); }
 
+namespace hs {
+// Streaming-read probe (hs_probe.hip): `vectors` 16-byte vectors of x read once by `grid`
+// workgroups of 256 threads with `unroll` (1, 2, 4 or 8) loads in flight per thread; one word
+// per wave to out (grid * 4 words).
+int launch_stream_read(const void* x, uint64_t vectors, int grid, int unroll, bool nontemporal,
+                       uint32_t* out, hipStream_t s);
+}  // namespace hs
+
+HS_API int hs_stream_read(const void* x, size_t bytes, int grid, int unroll, int nontemporal,
+                          uint32_t* out, void* stream) {
+  if (!x || !out) return fail(HS_ERR_NULL, "hs_stream_read: NULL buffer");
+  if (((uintptr_t)x & 15) != 0 || (bytes & 15) != 0)
+    return fail(HS_ERR_ALIGN, "hs_stream_read: buffer and size must be multiples of 16 bytes");
+  if (bytes == 0 || grid < 1 || grid > 65536)
+    return fail(HS_ERR_SHAPE, "hs_stream_read: need bytes > 0 and 1 <= grid <= 65536");
+  if (unroll != 1 && unroll != 2 && unroll != 4 && unroll != 8)
+    return fail(HS_ERR_ARG, "hs_stream_read: unroll must be 1, 2, 4 or 8 (got %d)", unroll);
+  const int rc = hs::launch_stream_read(x, bytes / 16, grid, unroll, nontemporal != 0, out,
+                                        (hipStream_t)stream);
+  return rc == HS_OK ? HS_OK : fail(rc, "hs_stream_read: launch failed");
+}
+
 HS_API int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t V, int64_t ld,
                             float temperature, float* row_max, float* row_lse,
                             int32_t* row_argmax, void* stream) {

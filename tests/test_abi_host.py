@@ -127,6 +127,17 @@ def test_softmax_stats_validation_codes():
     assert lib.hs_softmax_stats(FAKE, 0, 4, 100, 100, 0.0, FAKE, None, None, None) == 5
 
 
+def test_stream_read_validation_codes():
+    lib = hs.load_library()
+    assert lib.hs_stream_read(None, 1024, 64, 4, 0, FAKE, None) == 1
+    assert lib.hs_stream_read(FAKE, 1024, 64, 4, 0, None, None) == 1
+    assert lib.hs_stream_read(FAKE + 8, 1024, 64, 4, 0, FAKE, None) == 4
+    assert lib.hs_stream_read(FAKE, 1000, 64, 4, 0, FAKE, None) == 4
+    assert lib.hs_stream_read(FAKE, 0, 64, 4, 0, FAKE, None) == 2
+    assert lib.hs_stream_read(FAKE, 1024, 0, 4, 0, FAKE, None) == 2
+    assert lib.hs_stream_read(FAKE, 1024, 64, 3, 0, FAKE, None) == 10
+
+
 def test_softmax_stats_binding_rejects_mismatched_outputs():
     # checked before the library is called, so host tensors do
     import torch
