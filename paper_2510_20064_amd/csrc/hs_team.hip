@@ -429,8 +429,8 @@ __device__ __forceinline__ void thread_max(const TeamArgs& A, const ItemPos& q,
 // above m_t c) and the exp2 sum against it; max keys, sums and offsets to LDS. The offsets
 // are integer-valued, so the group's rescaling of the sums to the slice offset is exact. A
 // thread whose m_t c is -inf (logits all -inf, or finite ones whose product with c is below
-// the fp32 range) takes offset 0: each of its logits then gives exp2(-inf) = 0, or NaN for a
-// NaN logit ----
+// the fp32 range) takes offset -2^126: each of its logits then gives 0, or NaN for a NaN
+// logit ----
 template <int DT, int D, bool NEED_ARG, typename L>
 __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos& q,
                                                 typename Vec<DT>::Raw (&raw)[D + 1], L& sh,
@@ -455,8 +455,9 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
         m = fmaxf(m, z[e]);
       }
     }
-    const float ot = exp_offset_of(m, A.c);
-    const float of = ot != -INFINITY ? ot : 0.0f;  // NaN-free: m is never NaN
+    // ot = -inf (no logit whose scaled value is finite) becomes -2^126: every z c - of is then
+    // -inf or far below -2^125, so each e_v is 0 (NaN for a NaN logit); m is never NaN
+    const float of = fmaxf(exp_offset_of(m, A.c), -0x1p126f);
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -of));
@@ -752,24 +753,30 @@ __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int
 }
 
 // ---- 8. end of a workgroup ----
-// A team's leader finishes after it has folded row 0 of the team's last item, so every member
-// has by then read the call's tag and no claim of the team is outstanding; the last leader to
-// finish advances the epoch and resets the row-set counter (one count per team, not per
-// workgroup; the count of finished teams is tagged with the call, so it needs no reset).
-// When a wait of this call gave up, every workgroup that sees the fail flag marks every output
-// (alpha NaN, argmax -2, agreement 0): a wave that took a lost word has seen the flag, so each
-// value computed from one is overwritten by the same workgroup, and outputs of row sets that
-// no team reached are marked too; values written without a lost word are correct either way.
+// A team's leader counts its team once every member has read the call's tag and no claim of
+// the team is outstanding: after folding row 0 of the team's last item (at its end), or, with
+// one item per workgroup and no learner step in the launch, right after folding row 0. The
+// last team counted advances the epoch and resets the row-set counter (one count per team,
+// not per workgroup; the count of finished teams is tagged with the call, so it needs no
+// reset).
+__device__ inline void count_team(const TeamArgs& A, uint32_t tag, int teams) {
+  if (tagged_add(A.finished, tag) == (uint32_t)teams - 1u) {
+    *A.next_set = 0u;           // every team has finished: nothing claims any more
+    *A.epoch = *A.epoch + 1u;   // the next call takes a new tag
+  }
+}
+// When a wait of this call gave up, every workgroup that sees the fail flag at its end marks
+// every output (alpha NaN, argmax -2, agreement 0): a wave that took a lost word has seen the
+// flag, so each value computed from one is overwritten by the same workgroup, and outputs of
+// row sets that no team reached are marked too; values written without a lost word are
+// correct either way.
 template <typename L>
-__device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool leader, int teams,
+__device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool count, int teams,
                                        L& sh, int t) {
   if (t == 0) {
     const uint64_t fw = get_word(A.fail);
-    uint32_t flags = ((uint32_t)fw == tag && (fw >> 32) != 0) ? 2u : 0u;
-    if (leader && tagged_add(A.finished, tag) == (uint32_t)teams - 1u) {
-      *A.next_set = 0u;           // every team has finished: nothing claims any more
-      *A.epoch = *A.epoch + 1u;   // the next call takes a new tag
-    }
+    const uint32_t flags = ((uint32_t)fw == tag && (fw >> 32) != 0) ? 2u : 0u;
+    if (count) count_team(A, tag, teams);
     sh.next = flags;
   }
   __syncthreads();
@@ -900,8 +907,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         const int os = cvt_i32_sat(exp_offset(o));
         // the 16 sums of this lane rescaled to the slice offset (exact: powers of two) and
         // added in sum16's order, four at a time (one 16-byte read of sums and of offsets).
-        // A thread's offset is at most the slice's, unless the thread took offset 0 for a sum
-        // that is 0 or NaN. Offsets beyond the int32 range saturate, and a difference that
+        // A thread's offset is at most the slice's, unless the thread took offset -2^126 for a
+        // sum that is 0 or NaN. Offsets beyond the int32 range saturate, and a difference that
         // wraps needs |offset| >= 2^30, where the thread's exponents are all <= -256 and its
         // sum is exactly 0 (or NaN): ldexp of 0 or NaN is 0 or NaN whatever the shift
         typedef float F4 __attribute__((ext_vector_type(4)));
@@ -973,6 +980,11 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       }
       fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
       __builtin_amdgcn_s_setprio(0);
+      // with one item per workgroup the leader counts its team once it has folded row 0 (every
+      // member has published, so has read the tag), not at its end; in a launch that also runs
+      // the learner step it counts at its end, off the path to the first learner
+      const bool early = leader && !A.learn;
+      if (early && t == 0) count_team(A, tag, teams);
       if (wv == 0) await_norms<D, true>(A, q, tag, sh, 0, lane);
       __syncthreads();
       thread_minsums_kept<DT, D>(q, x, sh, t);
@@ -981,7 +993,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       fold_alpha<D>(A, q, tag, lane, wv);
       if (A.learn)
         for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
-      finish(A, tag, leader, teams, sh, t);
+      finish(A, tag, leader && !early, teams, sh, t);
       return;
     }
     fetch_item<DT, D>(A, item_pos(A, min(set1, nsets - 1), slot, D), set1 < nsets, sh,
