@@ -945,8 +945,32 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       }
     };
 
+    // Several items per workgroup: the row sets of one (query, position) group follow each
+    // other in a team when there are groups enough to keep every team busy, so the target's
+    // slice, the same for all of them, is re-read from this XCD's L2 rather than from HBM. A
+    // team's items come in blocks (a group's nsub row sets, else single row sets): its first
+    // kB blocks are blocks T, T + teams, ... (at least three items, to fill the pipeline), and
+    // later ones are claimed from the device-wide counter three items ahead, by the leader,
+    // and posted in the team's mailbox ring.
+    const bool blocked = !SINGLE && A.nsub > 1 && nsets >= 4u * (uint32_t)teams * (uint32_t)A.nsub;
+    const uint32_t bsz = blocked ? (uint32_t)A.nsub : 1u;
+    const uint32_t nblocks = blocked ? fdiv(nsets, A.divNsub) : nsets;
+    const int kB = blocked ? (int)((3u + bsz - 1u) / bsz) : 3;
+    const bool dyn = kB * teams < (int)nblocks;  // else no team has more than its fixed blocks
+    int nblk = 0;  // blocks given to this team so far (the same count in every member)
+    auto block_first = [&](uint32_t bl) { return bl < nblocks ? bl * bsz : nsets; };
+    // the row set after s (nsets: none), or kClaim when it starts a block that is to be claimed
+    constexpr uint32_t kClaim = 0xFFFFFFFFu;
+    auto successor = [&](uint32_t s) __attribute__((always_inline)) -> uint32_t {
+      if (s >= nsets) return nsets;
+      if (blocked && fdiv(s + 1u, A.divNsub) * bsz != s + 1u) return s + 1u;  // same group
+      if (nblk < kB) return block_first((uint32_t)(T + (nblk++) * teams));
+      return dyn ? kClaim : nsets;
+    };
+
     Raw R0[RM], R1[RM], R2[RM];
-    uint32_t set = (uint32_t)T, set1 = fixed_set(1), set2 = fixed_set(2);
+    uint32_t set = SINGLE ? (uint32_t)T : block_first((uint32_t)T);
+    nblk = 1;
     const ItemPos q0 = item_pos(A, set, slot, D);
     fetch_item<DT, D, SINGLE>(A, q0, true, sh, R0);
     if constexpr (SINGLE) {
@@ -996,6 +1020,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       finish(A, tag, leader && !early, teams, sh, t);
       return;
     }
+    uint32_t set1 = successor(set);
+    uint32_t set2 = successor(set1);  // items 0-2 lie in fixed blocks: never kClaim
     fetch_item<DT, D>(A, item_pos(A, min(set1, nsets - 1), slot, D), set1 < nsets, sh,
                       R1);
     tag = call_tag(A.epoch);  // first needed once the first loads are in flight
@@ -1015,7 +1041,8 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       const ItemPos q = item_pos(A, set, slot, D);
       // the leader's claim of item j + 3 goes out before the fold and is posted after it, so
       // waiting for its result waits for nothing else
-      const bool claiming = dynamic && leader && t == 0 && set2 < nsets;
+      const uint32_t set3 = successor(set2);  // item j + 3, unless it is to be claimed
+      const bool claiming = set3 == kClaim && leader && t == 0;
       uint32_t cv = 0;
       if (claiming)
         cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1024,13 +1051,13 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       __builtin_amdgcn_s_setprio(0);
       if (claiming)
         put_word(mbox + ((j + 3) & 3),
-                 mbox_word(min((uint32_t)(kStatic * teams) + cv, nsets), j + 3, tag));
+                 mbox_word(block_first((uint32_t)(kB * teams) + cv), j + 3, tag));
       fetch_item<DT, D>(A, item_pos(A, min(set2, nsets - 1), slot, D), set2 < nsets, sh,
                         rp);
       if (set1 < nsets) stats(item_pos(A, set1, slot, D), rn, bf ^ 1);
       // alpha of the previous item, whose partials were stored an iteration ago
       if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv, rotation(pset, RM));
-      if (set2 < nsets) post_set(j + 3);
+      if (set3 == kClaim && t == 0) sh.next = await_mbox(mbox + ((j + 3) & 3), j + 3, tag, A, nsets);
       if (wv == 0) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
@@ -1040,7 +1067,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       pset = set;
       set = set1;
       set1 = set2;
-      set2 = set2 < nsets ? sh.next : nsets;
+      set2 = set3 == kClaim ? sh.next : set3;
       return true;
     };
     // unrolled by three so that the register buffers rotate without copies
