@@ -196,6 +196,22 @@ def test_large_pool_full_size_stream_across_the_regime_switch():
                         gen=lambda r: synth.generate(w, round=r0 + r), p_drift_tol=1e-4)
 
 
+@pytest.mark.parametrize("N", [9, 20])
+def test_blocked_row_sets_with_a_ragged_last_set(N):
+    # 128 (query, position) groups of 2 or 3 row sets over teams of 30 workgroups: groups
+    # outnumber the teams four times over, so each team takes a group's row sets one after
+    # another (its target slice then comes from L2), and the last row set of every group holds
+    # fewer drafters (1 of 9, 4 of 20); alpha, agreement and both argmaxes every group, then
+    # hs_round with both learners, at T = 0.7
+    w = synth.variant(WL["qwen3_8b_single"], B=4, N=N, K=32, V=60000, ld=60000,
+                      scales=[0.2 * 20 ** (j / (N - 1)) for j in range(N)], temperature=0.7,
+                      nboost=20)
+    note("blocked row sets: B4 N%d K32 V60000 bf16 T0.7" % N)
+    x = synth.generate(w)
+    check_eval(w, x)
+    run_round_and_check(w, x)
+
+
 def test_large_pool_stream_reduced_vocab_1000_rounds():
     w = synth.variant(WL["large_pool_stream"], V=256)
     note("large_pool_stream B32 N64 K8 at V=256: 1000 rounds, regime switch at 500")
