@@ -54,13 +54,14 @@ def _clang_asan_runtime():
 def test_abi_validation_under_asan_and_ubsan(tmp_path):
     # hs_api.hip rebuilt with the sanitizers on its host code only (each flag after -Xarch_host),
     # linked with the other objects of the regular build
-    objdir = os.path.join(ROOT, "paper_2510_20064_amd", "_build")
-    others = [os.path.join(objdir, f) for f in
-              ["hs_stats.o", "hs_team.o", "hs_tail.o", "hs_delayed.o", "hs_topl.o", "hs_play.o"]]
-    if not all(os.path.exists(o) for o in others):
-        pytest.skip("the library's objects are not built (run the build first)")
     sys.path.insert(0, ROOT)
     from paper_2510_20064_amd import build as B
+
+    objdir = os.path.join(ROOT, "paper_2510_20064_amd", "_build")
+    others = [os.path.join(objdir, f.replace(".hip", ".o")) for f in B.SOURCES
+              if f != "hs_api.hip"]
+    if not all(os.path.exists(o) for o in others):
+        pytest.skip("the library's objects are not built (run the build first)")
 
     san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
