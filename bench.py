@@ -669,11 +669,12 @@ def cpu_baseline(args, w, np, synth, greedy):
             "single_thread": {"value": per_unit * n_one / el_one, "unit": "drafter-positions/s",
                               "cores": 1, "input_GBps": unit_bytes * n_one / el_one / 1e9,
                               "queries": n_one, "seconds": round(el_one, 2)},
-            "sample": "%d whole queries (all %d drafters x %d positions each, %.1f MB of logits "
-                      "each) of round 0 of the same workload: float64 C oracle (softmax "
-                      "statistics, alpha or agreement, EAL, loss, Hedge, NormalHedge), OpenMP "
-                      "over rows on %d threads, %.1f s; then %d queries on 1 thread, %.1f s"
-                      % (n_all, w.N, w.K, unit_bytes / 1e6, threads, el_all, n_one, el_one)}
+            "sample": "%d evaluations of whole queries (all %d drafters x %d positions each, "
+                      "%.1f MB of logits each), cycling over the first %d queries of round 0 of "
+                      "the same workload: float64 C oracle (softmax statistics, alpha or "
+                      "agreement, EAL, loss, Hedge, NormalHedge), OpenMP over rows on %d "
+                      "threads, %.1f s; then %d on 1 thread, %.1f s"
+                      % (n_all, w.N, w.K, unit_bytes / 1e6, nq, threads, el_all, n_one, el_one)}
 
 
 if __name__ == "__main__":
