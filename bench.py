@@ -294,6 +294,13 @@ def bench_softmax_stats(args, w, hs, torch, dev, synth):
     e1.record(stream)
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     eb = 2 if w.dtype == synth.BF16 else 4
     nbytes = rows * w.V * eb + rows * 12
     achieved = nbytes / (us * 1e-6) / 1e9
