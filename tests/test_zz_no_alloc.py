@@ -1,5 +1,5 @@
 """hs_eval_alpha_noalloc (the fixed device workspace) against hs_eval_alpha (a workspace of the
-caller's), through the C ABI: two calls in a row, the second on a smaller input, each compared
+caller's), through the C ABI: calls in a row, each on a smaller input than the last, each compared
 with hs_eval_alpha on the same logits at the parity bars (indices and agreement bit-exact, alpha
 within 2e-5; the two share their kernels, so alpha agrees bit for bit as well)."""
 import numpy as np
@@ -27,8 +27,11 @@ def _outs(B, N, K):
 
 
 @pytest.mark.parametrize("mode", [hs.SAMPLE, hs.GREEDY])
-def test_noalloc_matches_eval_alpha_on_two_calls(mode):
-    shapes = [dict(B=3, N=12, K=5, V=151936), dict(B=1, N=4, K=2, V=40000)]  # second smaller
+def test_noalloc_matches_eval_alpha_on_calls_in_a_row(mode):
+    # each call smaller than the one before; the first has groups enough for the teams to take
+    # a (query, position)'s two row sets in turn
+    shapes = [dict(B=16, N=16, K=8, V=151936), dict(B=3, N=12, K=5, V=151936),
+              dict(B=1, N=4, K=2, V=40000)]
     for i, sh in enumerate(shapes):
         print("\n[case] noalloc call %d mode=%d %s" % (i, mode, sh), flush=True)
         w = synth.variant(BASE, scales=[0.2 + 0.3 * j for j in range(sh["N"])], seed=40 + i,
