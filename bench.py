@@ -544,6 +544,24 @@ def main():
     ms_step = e0.elapsed_time(e1) / args.steps
     value = w.positions / (ms_step * 1e-3)
 
+    # ---- the whole 1000-round stream of the large pool (hs_round per round, the learners
+    # carried through), inputs rotating as above ------------------------------------------------
+    stream_total = None
+    if w.name == "large_pool_stream" and args.stack == 1 and use_graph:
+        rounds_total = 1000
+        capture(step_fn, rounds_total % copies)  # (every other graph exists already)
+        torch.cuda.synchronize()
+        e6 = torch.cuda.Event(enable_timing=True)
+        e7 = torch.cuda.Event(enable_timing=True)
+        e6.record(stream)
+        run(step_fn, rounds_total)
+        e7.record(stream)
+        torch.cuda.synchronize()
+        stream_total = {"rounds": rounds_total, "seconds": e6.elapsed_time(e7) * 1e-3,
+                        "note": "1000 consecutive hs_round steps (HIP graph replays, learner "
+                                "state carried), inputs rotating over %d resident rounds; "
+                                "generation and host-to-device copies excluded" % copies}
+
     # ---- the evaluation kernel alone (hs_eval_alpha), live, on the same stream -------------
     run(eval_fn, copies)
     torch.cuda.synchronize()
@@ -625,6 +643,8 @@ def main():
     }
     if read_cal is not None:
         line["read_calibration"] = read_cal
+    if stream_total is not None:
+        line["stream_total"] = stream_total
     print(json.dumps(line), flush=True)
 
 
