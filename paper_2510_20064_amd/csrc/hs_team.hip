@@ -379,6 +379,16 @@ __device__ inline float min_pos(float a, float b) {
   return __uint_as_float(min(__float_as_uint(a), __float_as_uint(b)));
 }
 
+// fminf of two results of arithmetic (never a signalling NaN): the hardware minimum, which
+// returns the other operand for a quiet NaN as fminf does. Written out because the compiler
+// otherwise re-canonicalises an operand that it cannot prove is a result of arithmetic (the
+// target's exponents, once per item).
+__device__ inline float min_arith(float a, float b) {
+  float r;
+  asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // The raw registers of one row made opaque to the compiler: each stage unpacks the logits
 // afresh (two integer operations per pair) instead of the compiler keeping the unpacked
 // floats of a whole item live from one stage to the next, which would not fit in registers.
@@ -458,9 +468,11 @@ __device__ __forceinline__ void thread_stats_pt(const TeamArgs& A, const ItemPos
         m = fmaxf(m, z[e]);
       }
     }
-    // ot = -inf (no logit whose scaled value is finite) becomes -2^126: every z c - of is then
+    // exp_offset_of(m, c) without its test for m c = -inf (no logit whose scaled value is
+    // finite): the fma then gives NaN, which fmaxf replaces by -2^126; every z c - of is then
     // -inf or far below -2^125, so each e_v is 0 (NaN for a NaN logit); m is never NaN
-    const float of = fmaxf(exp_offset_of(m, A.c), -0x1p126f);
+    const float mc = m * A.c;
+    const float of = fmaxf(ceilf(fmaf(fabsf(mc), 0x1p-22f, mc)), -0x1p126f);
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(z[e], A.c, -of));
@@ -655,10 +667,9 @@ __device__ __forceinline__ void thread_minsums_form(const TeamArgs& A, const Ite
       const float nw = sh.nw[d];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        // both operands are results of arithmetic, so fminf needs no canonicalising. A slice
-        // with no finite logit has every u_v (target) or w_v (drafter) at -inf; nw_d is then
-        // infinite or NaN, and where the other operand becomes NaN it loses to the -inf
-        y[e] = __builtin_amdgcn_exp2f(fminf(u[e], fmaf(w[e], A.c, nw)));
+        // a slice with no finite logit has every u_v (target) or w_v (drafter) at -inf; nw_d
+        // is then infinite or NaN, and where the other operand becomes NaN it loses to the -inf
+        y[e] = __builtin_amdgcn_exp2f(min_arith(u[e], fmaf(w[e], A.c, nw)));
       }
     } else {
       // a large offset: the exact residual z c - o_d first, then the difference
