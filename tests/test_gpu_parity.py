@@ -141,6 +141,16 @@ def test_tiny_chain_full():
     run_round_and_check(w, x)
 
 
+def test_tiny_chain_stacked_instances():
+    # the tiny chain stacked 64 times (64 queries, each with its own logits and learner): fp32
+    # rows, sampled, and more row sets than resident teams, so each team runs several items
+    w = synth.variant(WL["tiny_chain"], B=64)
+    note("tiny_chain x64: B64 N4 K4 V32000 fp32 (full check, several items per workgroup)")
+    x = synth.generate(w)
+    check_eval(w, x)
+    run_round_and_check(w, x)
+
+
 def test_qwen3_8b_single_full():
     w = WL["qwen3_8b_single"]
     note("qwen3_8b_single B1 N8 K8 V151936 bf16 (full check)")
