@@ -421,8 +421,8 @@ def bench_topl(args, w, hs, torch, dev, np, synth):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one MI355X: this build has no multi-GPU path "
-              "(query sharding needs no exchange; see the design notes). Run with --gpus 1.",
+        print("bench.py measures one MI355X: the library has no multi-GPU path "
+              "(queries would shard across GPUs with no exchange between them). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
