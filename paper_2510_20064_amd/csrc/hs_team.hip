@@ -41,6 +41,12 @@ namespace hs {
 
 constexpr int kPollSleep = 2;  // s_sleep units (64 clocks) between polls
 constexpr int kCritPrio = 2;   // wave priority of the exchange-critical stages (s_setprio)
+// The wave that holds no row of the group reductions (16-lane group r reduces row r, so the at
+// most kMaxSetDrafters + 1 rows sit in the other waves) takes a member's first fold duty and
+// the normaliser wait: their load round trips then overlap the other waves' group reductions
+// instead of following them, and wave 0 keeps thread 0's claims and counts.
+constexpr int kDutyWave = kWaves - 1;
+static_assert(kMaxSetDrafters + 1 <= 4 * kDutyWave, "the duty wave must hold no reduction row");
 
 struct TeamArgs {
   // What every workgroup reads before its first loads comes first: the first 128 bytes of the
@@ -95,7 +101,16 @@ __device__ inline uint32_t call_tag(const uint32_t* epoch) {
 // count before (0 for the first add of a call): the word holds (count << 32) | tag, and a
 // word with another tag, from an earlier call or never written, counts as 0. So nothing has
 // to be reset between calls, and whatever a word held before cannot skew this call's count.
+// The call that completes a count leaves the word at (0 << 32) | the next call's tag
+// (count_team), so each add of the next call is a single fetch-and-add, which leaves the tag
+// half alone and costs every adder one round trip however many add at once. An add that
+// finds another tag (the first call on a zeroed workspace) goes on by compare-and-swap: the
+// first exchange replaces the whole word, so its earlier fetch-and-adds on the stale word do
+// not count, and every adder is counted once, by its fetch-and-add or by its exchange.
 __device__ inline uint32_t tagged_add(uint64_t* w, uint32_t tag) {
+  const uint64_t old =
+      __hip_atomic_fetch_add(w, 1ull << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((uint32_t)old == tag) return (uint32_t)(old >> 32);
   uint64_t cur = get_word(w);
   for (;;) {  // each failed exchange means another add succeeded: this ends
     const uint32_t n = (uint32_t)cur == tag ? (uint32_t)(cur >> 32) : 0u;
@@ -537,15 +552,16 @@ __device__ __forceinline__ void publish_row(const TeamArgs& A, const ItemPos& q,
 __device__ inline int duty_index(int s, int rot, int S) { return s >= rot ? s - rot : s - rot + S; }
 
 // ---- 4. fold duty: rows i, i + S, ... of the row set (i = the slot's duty index for the
-// item's rotation rot), spread over the waves ----
+// item's rotation rot), spread over the waves, wave `first` taking the first ----
 template <int D, bool NEED_SUM, bool NEED_ARG>
 __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
-                                          int lane, int wv, int rot = 0) {
-  for (int rr = duty_index(q.s, rot, A.S) + wv * A.S; rr <= q.n; rr += kWaves * A.S)
+                                          int lane, int wv, int first, int rot = 0) {
+  const int order = (wv + kWaves - first) % kWaves;
+  for (int rr = duty_index(q.s, rot, A.S) + order * A.S; rr <= q.n; rr += kWaves * A.S)
     fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
 }
 
-// ---- 5. normalisers (wave 0; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
+// ---- 5. normalisers (the duty wave; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
 // lo; lane 2r forms a_r = (o_r - hi_r) - lo_r and, for a drafter row, the constants of its
 // min-sum to LDS: G and F = 2^(a_r) for kept e_v (6'), else the exponent addend and 2^(a_t) (6).
 // A row with no finite logit folds to hi = -inf, lo = NaN, so its a is NaN: it has no
@@ -769,14 +785,16 @@ __device__ __forceinline__ void learn_query(const TeamArgs& A, uint32_t tag, int
 // ---- 8. end of a workgroup ----
 // A team's leader counts its team once every member has read the call's tag and no claim of
 // the team is outstanding: after folding row 0 of the team's last item (at its end), or, with
-// one item per workgroup and no learner step in the launch, right after folding row 0. The
+// one item per workgroup, right after folding row 0. The
 // last team counted advances the epoch and resets the row-set counter (one count per team,
 // not per workgroup; the count of finished teams is tagged with the call, so it needs no
 // reset).
 __device__ inline void count_team(const TeamArgs& A, uint32_t tag, int teams) {
   if (tagged_add(A.finished, tag) == (uint32_t)teams - 1u) {
-    *A.next_set = 0u;           // every team has finished: nothing claims any more
-    *A.epoch = *A.epoch + 1u;   // the next call takes a new tag
+    const uint32_t e = *A.epoch + 1u;
+    *A.next_set = 0u;  // every team has finished: nothing claims any more
+    put_word(A.finished, (uint64_t)tag_of_epoch(e));  // count 0 for the next call's tag
+    *A.epoch = e;      // the next call takes a new tag
   }
 }
 // When a wait of this call gave up, every workgroup that sees the fail flag at its end marks
@@ -898,7 +916,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         group_max<D, NEED_ARG>(sh, q.n, gi, gl, m, idx);
         if (gl == 0 && gi <= q.n) publish_row<false, NEED_ARG>(A, q, gi, tag, m, 0.0f, idx, RM);
       }
-      fold_item<D, false, NEED_ARG>(A, q, tag, lane, wv);
+      fold_item<D, false, NEED_ARG>(A, q, tag, lane, wv, kDutyWave);
       __builtin_amdgcn_s_setprio(0);
       __syncthreads();  // the LDS rows are free for the next item
       set = next;
@@ -1016,13 +1034,13 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
         const float sm = row16_sum(sum16(v));
         if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, sm, idx, RM);
       }
-      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv);
+      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, 0);
       __builtin_amdgcn_s_setprio(0);
       // with one item per workgroup the leader counts its team once it has folded row 0 (every
-      // member has published, so has read the tag), not at its end; in a launch that also runs
-      // the learner step it counts at its end, off the path to the first learner
-      const bool early = leader && !A.learn;
-      if (early && t == 0) count_team(A, tag, teams);
+      // member has published, so has read the tag), not at its end: the count's round trip
+      // then overlaps the normaliser wait instead of following the learner step or the alpha
+      // folds. (The fold duties start at wave 0, whose thread 0 counts.)
+      if (leader && t == 0) count_team(A, tag, teams);
       if (wv == 0) await_norms<D, true>(A, q, tag, sh, 0, lane);
       __syncthreads();
       thread_minsums_kept<DT, D>(q, x, sh, t);
@@ -1031,7 +1049,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       fold_alpha<D>(A, q, tag, lane, wv);
       if (A.learn)
         for (int b = blockIdx.x; b < A.B; b += gridDim.x) learn_query(A, tag, b, sh, t);
-      finish(A, tag, leader && !early, teams, sh, t);
+      finish(A, tag, false, teams, sh, t);
       return;
     }
     uint32_t set1 = successor(set);
@@ -1061,7 +1079,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (claiming)
         cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __builtin_amdgcn_s_setprio(kCritPrio);
-      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, rotation(set, 0));
+      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, kDutyWave, rotation(set, 0));
       __builtin_amdgcn_s_setprio(0);
       if (claiming)
         put_word(mbox + ((j + 3) & 3),
@@ -1072,7 +1090,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       // alpha of the previous item, whose partials were stored an iteration ago
       if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv, rotation(pset, RM));
       if (set3 == kClaim && t == 0) sh.next = await_mbox(mbox + ((j + 3) & 3), j + 3, tag, A, nsets);
-      if (wv == 0) await_norms<D, false>(A, q, tag, sh, bf, lane);
+      if (wv == kDutyWave) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
       __syncthreads();
