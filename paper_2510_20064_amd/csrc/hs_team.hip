@@ -1072,9 +1072,10 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       const int bf = j & 1;
       const ItemPos q = item_pos(A, set, slot, D);
       // the leader's claim of item j + 3 goes out before the fold and is posted after it, so
-      // waiting for its result waits for nothing else
+      // waiting for its result waits for nothing else; the duty wave, which folds, claims
+      // (the argmax-only kernel, whose folds are short, claims on thread 0)
       const uint32_t set3 = successor(set2);  // item j + 3, unless it is to be claimed
-      const bool claiming = set3 == kClaim && leader && t == 0;
+      const bool claiming = set3 == kClaim && leader && wv == kDutyWave && lane == 0;
       uint32_t cv = 0;
       if (claiming)
         cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
