@@ -12,7 +12,7 @@ namespace hs {
 
 constexpr int kThreads = 256;          // workgroup size of the streaming kernels (4 waves)
 constexpr int kWaves = kThreads / 64;
-constexpr int kSliceElems = 8192;      // logits per workgroup pass in hs_softmax_stats
+constexpr int kSliceElems = 4096;      // logits per workgroup pass in hs_softmax_stats
 constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
 constexpr int kMaxSetDrafters = 8;     // drafters held on chip with the target by one workgroup
 constexpr int kMaxTeamSlices = 512;    // slices per row (one workgroup each) in one team

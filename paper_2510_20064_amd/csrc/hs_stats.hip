@@ -22,11 +22,27 @@ __global__ __launch_bounds__(kThreads) void hs_softmax_stats_kernel(const char* 
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
   const char* rowp = x + row * ld * Vt::kBytes;
+  // branch-free 16-byte loads at an index clamped into the row's complete vectors, nontemporal
+  // for bf16 (every logit is read once: 6% faster than plain loads on both bf16 workloads
+  // measured); the one partial vector at the row end, and vectors past it, are then replaced
+  // in the lanes that hold them
+  const int64_t vfull = V / E;  // complete 16-byte vectors of the row
   auto fetch = [&](int64_t v0, Raw (&r)[U]) __attribute__((always_inline)) {
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    typedef const __attribute__((address_space(1))) u4* gp4;
+    if (vfull > 0) {
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int64_t vi = v0 + (int64_t)j * kThreads + t;
+        const gp4 a = (gp4)(rowp + (vi < vfull ? vi : vfull - 1) * 16);
+        const u4 v = DT == HS_BF16 ? __builtin_nontemporal_load(a) : *a;
+        __builtin_memcpy(&r[j], &v, 16);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < U; ++j) {
       const int64_t vi = v0 + (int64_t)j * kThreads + t;
-      r[j] = vi < nvec ? Vt::load_raw(rowp, vi, V) : Vt::neg_raw();
+      if (vi >= vfull) r[j] = vi < nvec ? Vt::load_raw(rowp, vi, V) : Vt::neg_raw();
     }
   };
   float m = -INFINITY, o = -INFINITY, s = 0.0f;
@@ -38,15 +54,26 @@ __global__ __launch_bounds__(kThreads) void hs_softmax_stats_kernel(const char* 
     float z[U][E];
 #pragma unroll
     for (int j = 0; j < U; ++j) Vt::unpack(cur[j], z[j]);
-    // indices are visited in increasing order, so a strict compare keeps the lowest
+    // the chunk's max first (NaN ignored); only a chunk that raises the running max is searched
+    // for the index, in increasing index order, so the first element equal to the chunk max is
+    // the lowest index attaining it, and the strict compare keeps an earlier chunk's on a tie
+    float cm = z[0][0];
 #pragma unroll
     for (int j = 0; j < U; ++j)
 #pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (z[j][e] > m) {
-          m = z[j][e];
-          idx = (int)((v0 + (int64_t)j * kThreads + t) * E + e);
-        }
+      for (int e = (j == 0 ? 1 : 0); e < E; ++e) cm = fmaxf(cm, z[j][e]);
+    if (cm > m) {
+      bool found = false;
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          if (!found && z[j][e] == cm) {
+            found = true;
+            m = z[j][e];
+            idx = (int)((v0 + (int64_t)j * kThreads + t) * E + e);
+          }
+    }
     // o = -inf until the running max scaled by c is finite; until then the sum is taken
     // against offset 0, where every logit seen so far gives exp2(-inf) = 0 (a -inf logit, or a
     // finite one whose product with c is below the fp32 range) or NaN (a NaN logit), so the
