@@ -403,6 +403,50 @@ def test_softmax_stats_entry():
             assert all(torch.equal(a, b) for a, b in zip(got, (mx, lse, am)))
 
 
+def test_softmax_stats_argmax_ties():
+    # the maximum attained several times: in one 16-byte vector, in one chunk on different
+    # lanes, in later chunks at the same lane, in the partial vector at the row end; a row of
+    # signed zeros, a constant row, a NaN before the maximum and a row of -inf with two ties.
+    # The lowest index must win everywhere (bf16 and fp32, V with a ragged tail)
+    rng = np.random.default_rng(37)
+    V = 100003
+    z = rng.normal(0, 1, (8, V)).astype(np.float32)
+    z[0, [5000, 5001, 70000, 99999]] = 9.0
+    z[1, [12345 + 2 * 2048, 12345, 12345 + 4096]] = 9.0       # same lane, three chunks
+    z[2, [V - 1, V - 2]] = 9.0                                 # the partial vector at the end
+    z[3] = -np.inf
+    z[3, [101, 100]] = 2.0
+    z[4] = 0.0
+    z[4, ::2] = -0.0
+    z[5] = 1.5
+    z[6, 3] = np.nan
+    z[6, [20, 10]] = 9.0
+    z[7, [64 * 8 * 4 + 1, 64 * 8 * 4, 7]] = 9.0                # one vector, then an earlier lane
+    u = z.view(np.uint32).astype(np.uint64)
+    zb = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    zb[6, 3] = 0x7FC0
+    for x, dt in ((z, synth.F32), (zb, synth.BF16)):
+        note("softmax stats, argmax ties, dtype=%d" % dt)
+        ld = V + (1 if dt == synth.F32 else 5)  # rows on 16-byte boundaries
+        pad = np.zeros((x.shape[0], ld), dtype=x.dtype)
+        pad[:, :V] = x
+        t = torch.from_numpy(pad)
+        if dt == synth.BF16:
+            t = t.view(torch.bfloat16)
+        mx, lse, am = hs.softmax_stats(t.cuda(), V=V, temperature=1.0)
+        torch.cuda.synchronize()
+        rm, ra, rl = oracle.softmax_stats(np.ascontiguousarray(pad[:, :V]), T=1.0)
+        assert list(ra[:4]) == [5000, 12345, V - 2, 100], ra
+        assert np.array_equal(am.cpu().numpy(), ra)
+        got_m = mx.cpu().numpy().astype(np.float64)
+        ok = np.isnan(rm)
+        assert np.array_equal(np.isnan(got_m), ok) and np.array_equal(got_m[~ok], rm[~ok])
+        gl = lse.cpu().numpy()
+        fin = np.isfinite(rl)
+        assert np.array_equal(np.isnan(gl), np.isnan(rl))
+        assert np.allclose(gl[fin], rl[fin], rtol=2e-6, atol=1e-5)
+
+
 def test_softmax_stats_growing_maxima():
     # rows whose running max grows chunk after chunk, so every thread rescales its sum many
     # times: an increasing ramp, the max on the last logit, and a jump of 200 (early sums
