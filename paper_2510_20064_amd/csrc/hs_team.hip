@@ -22,7 +22,8 @@
 // per-row value, then one 16-lane group per row reduces the row's 256 values and the result
 // is known to the whole group, so no wave reduces all rows on its own.
 // A workgroup with several items overlaps them: while item j's normalisers are exchanged it
-// runs the statistics of item j + 1, and the loads of item j + 2 are in flight.
+// runs the statistics of item j + 1, and the loads of item j + 2 go out as soon as item j's
+// min-sums have freed its registers.
 //
 // The grid holds as many teams as the device keeps resident at once, so all members of a
 // team run together and waiting on one cannot deadlock. Words crossing workgroups carry the
@@ -829,13 +830,16 @@ __device__ __forceinline__ void finish(const TeamArgs& A, uint32_t tag, bool cou
 // mailbox ring, so teams that run faster (the wave arbiter favours older waves) take more sets
 // and all finish within an item of each other.
 // With alpha two items are in flight per workgroup: iteration j folds item j (published in the
-// previous iteration), issues the loads of item j + 2, takes the statistics of item j + 1 and
-// publishes them, and only then waits for item j's normalisers and takes its min-sums from the
-// logits again. The exchange of one item thus overlaps the statistics of the next.
+// previous iteration), takes the statistics of item j + 1 and publishes them, and only then
+// waits for item j's normalisers and takes its min-sums from the logits again, after which
+// item j's registers receive the loads of item j + 2. The exchange of one item thus overlaps
+// the statistics of the next. Two raw buffers (not three, with the next loads issued before
+// the statistics) keep the kernel within 128 VGPRs, so four workgroups share a CU: 3-4% faster
+// on every large workload than three workgroups with three buffers.
 // SINGLE (alpha kernels only): every team has exactly one item, so nothing is pipelined, the
 // e_v stay in registers and drafters at a constant distance are addressed without the table.
 template <int DT, int D, bool NEED_SUM, bool NEED_ARG, bool SINGLE>
-__global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
+__global__ __launch_bounds__(kThreads, 4) void hs_team_kernel(TeamArgs A) {
   using Raw = typename Vec<DT>::Raw;
   constexpr int RM = D + 1;
   __shared__ TeamLds<D, NEED_ARG, NEED_SUM && !SINGLE> sh;
@@ -1000,7 +1004,7 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       return dyn ? kClaim : nsets;
     };
 
-    Raw R0[RM], R1[RM], R2[RM];
+    Raw R0[RM], R1[RM];
     uint32_t set = SINGLE ? (uint32_t)T : block_first((uint32_t)T);
     nblk = 1;
     const ItemPos q0 = item_pos(A, set, slot, D);
@@ -1065,9 +1069,9 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
     __syncthreads();
 
     uint32_t pset = nsets;  // the team's previous item, whose alpha is still to be folded
-    // iteration j: rc holds item j (statistics published), rn item j + 1 (loaded), rp receives
-    // item j + 2. Returns false once the team has no item j + 1.
-    auto iter = [&](int j, Raw (&rc)[RM], Raw (&rn)[RM], Raw (&rp)[RM])
+    // iteration j: rc holds item j (statistics published) and then receives item j + 2, rn
+    // holds item j + 1 (loaded). Returns false once the team has no item j + 1.
+    auto iter = [&](int j, Raw (&rc)[RM], Raw (&rn)[RM])
                     __attribute__((always_inline)) -> bool {
       const int bf = j & 1;
       const ItemPos q = item_pos(A, set, slot, D);
@@ -1085,17 +1089,17 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       if (claiming)
         put_word(mbox + ((j + 3) & 3),
                  mbox_word(block_first((uint32_t)(kB * teams) + cv), j + 3, tag));
-      fetch_item<DT, D>(A, item_pos(A, min(set2, nsets - 1), slot, D), set2 < nsets, sh,
-                        rp);
       if (set1 < nsets) stats(item_pos(A, set1, slot, D), rn, bf ^ 1);
-      // alpha of the previous item, whose partials were stored an iteration ago
-      if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv, rotation(pset, RM));
       if (set3 == kClaim && t == 0) sh.next = await_mbox(mbox + ((j + 3) & 3), j + 3, tag, A, nsets);
       if (wv == kDutyWave) await_norms<D, false>(A, q, tag, sh, bf, lane);
       __syncthreads();
       thread_minsums<DT, D>(A, q, rc, sh, bf, t);
       __syncthreads();
       store_partials(q);
+      fetch_item<DT, D>(A, item_pos(A, min(set2, nsets - 1), slot, D), set2 < nsets, sh, rc);
+      // alpha of the previous item, whose partials were stored an iteration ago; its polls
+      // overlap the loads just issued (1.4% faster than folding it before the normaliser wait)
+      if (pset < nsets) fold_alpha<D>(A, item_pos(A, pset, slot, D), tag, lane, wv, rotation(pset, RM));
       if (set1 >= nsets) return false;
       pset = set;
       set = set1;
@@ -1103,11 +1107,10 @@ __global__ __launch_bounds__(kThreads, 3) void hs_team_kernel(TeamArgs A) {
       set2 = set3 == kClaim ? sh.next : set3;
       return true;
     };
-    // unrolled by three so that the register buffers rotate without copies
-    for (int j = 0;; j += 3) {
-      if (!iter(j, R0, R1, R2)) break;
-      if (!iter(j + 1, R1, R2, R0)) break;
-      if (!iter(j + 2, R2, R0, R1)) break;
+    // unrolled by two so that the register buffers alternate without copies
+    for (int j = 0;; j += 2) {
+      if (!iter(j, R0, R1)) break;
+      if (!iter(j + 1, R1, R0)) break;
     }
     fold_alpha<D>(A, item_pos(A, set, slot, D), tag, lane, wv, rotation(set, RM));
     if (A.learn)
