@@ -42,6 +42,7 @@ namespace hs {
 
 constexpr int kPollSleep = 2;  // s_sleep units (64 clocks) between polls
 constexpr int kCritPrio = 2;   // wave priority of the exchange-critical stages (s_setprio)
+constexpr int kFoldPrio = 3;   // and of the pipelined kernel's row folds, which gate the team
 // The wave that holds no row of the group reductions (16-lane group r reduces row r, so the at
 // most kMaxSetDrafters + 1 rows sit in the other waves) takes a member's first fold duty and
 // the normaliser wait: their load round trips then overlap the other waves' group reductions
@@ -1087,7 +1088,7 @@ __global__ __launch_bounds__(kThreads, 4) void hs_team_kernel(TeamArgs A) {
       uint32_t cv = 0;
       if (claiming)
         cv = __hip_atomic_fetch_add(A.next_set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __builtin_amdgcn_s_setprio(kCritPrio);
+      __builtin_amdgcn_s_setprio(kFoldPrio);
       fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, kDutyWave, rotation(set, 0));
       __builtin_amdgcn_s_setprio(0);
       if (claiming)
