@@ -67,9 +67,14 @@ __device__ inline double normalhedge_inv_scale(double a, bool act, int N, double
     const double ex = act ? exp(a * s) : 0.0;
     const double E = wsum(ex);
     const double F = wsum(act ? a * ex : 0.0);
-    const double phi = log(E / (double)N) - 1.0;
+    // near the root (mean exp within 1e-4 of e) Newton's step on psi(s) = E / N - e instead:
+    // also convex and increasing, with the same root and sign, and no log to evaluate
+    const double Ne = (double)N * 2.718281828459045;
+    const double d = E - Ne;
+    const bool near = fabs(d) < 1e-4 * Ne;
+    const double phi = near ? d : log(E / (double)N) - 1.0;
     if (phi == 0.0 || !(F > 0.0)) break;
-    double sn = s - phi * E / F;
+    double sn = s - (near ? d / F : phi * E / F);
     if (phi < 0.0) {
       lo = s;
       if (!(sn < hi)) sn = hi;
