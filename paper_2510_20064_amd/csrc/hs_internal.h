@@ -17,6 +17,10 @@ constexpr int kMaxRows = HS_MAX_DRAFTERS + 1;
 constexpr int kMaxSetDrafters = 8;     // drafters held on chip with the target by one workgroup
 constexpr int kMaxTeamSlices = 512;    // slices per row (one workgroup each) in one team
 constexpr int kMaxTeams = 4096;        // teams resident at once (one mailbox ring each)
+// copies of each row's published normaliser (a power of two): with one item per workgroup
+// every member of a team polls its row set's normaliser words at once, so each copy is read
+// by a quarter of them
+constexpr int kNormCopies = 4;
 
 // Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 logits.
 template <int DT>
@@ -186,16 +190,23 @@ struct TeamWs {
                  // finished (tagged word) at +24, then a ring of 4 mailbox words per team at +64
   size_t stat;   // [G * nsub][D + 1][S][3] words: slice max, exp2 sum, argmax
   size_t norm;   // [G * nsub][D + 1][3] words: log2 normaliser hi, lo, argmax
+  size_t norm_copy;  // bytes of one copy of them (kNormCopies - 1 more follow the gamma words)
   size_t part;   // [G][N][S] words: per-slice sums of min(p, q_i)
   size_t gw;     // [B][N][K] words: gamma (alpha or agreement) for a learner in the same launch
   size_t total;
 };
 
-inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Tag of the evaluation call with epoch e: 31 bits (bit 31 of a word's tag half is its taint
 // mark), never 0, the content of a zero-filled workspace.
 __host__ __device__ inline uint32_t tag_of_epoch(uint32_t e) { return (e % 0x7FFFFFFFu) + 1u; }
+
+// Words from one copy of the normaliser words to the next, for `sets` row sets of `rows` rows
+// (the single-item kernel has one row set per team, so it passes its team count).
+__host__ __device__ inline int64_t norm_copy_words(int64_t sets, int rows) {
+  return (int64_t)align256((size_t)(24 * sets * rows)) / 8;
+}
 
 inline TeamWs team_ws(const TeamGeom& g) {
   TeamWs L;
@@ -206,11 +217,13 @@ inline TeamWs team_ws(const TeamGeom& g) {
   L.stat = off;
   off = align256(off + 24 * sets * rows * g.S);
   L.norm = off;
-  off = align256(off + 24 * sets * rows);
+  L.norm_copy = 8 * (size_t)norm_copy_words((int64_t)sets, (int)rows);
+  off += L.norm_copy;
   L.part = off;
   off = align256(off + 8 * (size_t)g.G * g.N * g.S);
   L.gw = off;
   off = align256(off + 8 * (size_t)g.B * g.N * g.K);
+  off += (kNormCopies - 1) * L.norm_copy;  // the normaliser words' other copies
   L.total = off;
   return L;
 }

@@ -76,7 +76,7 @@ struct TeamArgs {
   uint64_t* finished;  // teams of this launch that have finished (a tagged count)
   uint64_t* mbox;      // [teams][4]: the row set of each team's coming items
   uint64_t* stat;  // [sets][D + 1][S][3]
-  uint64_t* norm;  // [sets][D + 1][3]
+  uint64_t* norm;  // [sets][D + 1][3] (the single-item kernel's other copies: norm_copy)
   uint64_t* part;  // [G][N][S]
   float* alpha;
   int32_t* argmax_t;
@@ -178,11 +178,20 @@ __device__ inline uint32_t await_mbox(const uint64_t* w, int j, uint32_t tag, co
   return (uint32_t)(v >> 38);
 }
 
+// Copy c of the normaliser words: the first at A.norm, the others after the gamma words (the
+// single-item kernel only, whose row sets are its teams).
+__device__ inline uint64_t* norm_copy(const TeamArgs& A, int c, int rows) {
+  if (c == 0) return A.norm;
+  const uintptr_t end = reinterpret_cast<uintptr_t>(A.gw + (int64_t)A.B * A.N * A.K);
+  return reinterpret_cast<uint64_t*>((end + 255) & ~(uintptr_t)255) +
+         (c - 1) * norm_copy_words(A.teams, rows);
+}
+
 // Fold of row rr of row set `set`: the S slice statistics, two slices per lane per pass
 // (lane j takes slices j, j + 64, ... in order), then the wave. Publishes the row's log2
-// normaliser as hi + lo and its argmax; writes the argmax and agreement outputs. The
-// published words are tainted when any slice word was lost.
-template <int D, bool NEED_SUM, bool NEED_ARG>
+// normaliser as hi + lo (in NC copies) and its argmax; writes the argmax and agreement
+// outputs. The published words are tainted when any slice word was lost.
+template <int D, bool NEED_SUM, bool NEED_ARG, int NC = 1>
 __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int b, int k, int sub,
                                 uint32_t tag, int lane) {
   constexpr int RM = D + 1;
@@ -227,17 +236,21 @@ __device__ __forceinline__ void fold_row(const TeamArgs& A, int set, int rr, int
   wave_max<NEED_ARG>(m, idx);
   if (NEED_SUM) wave_lse(o, sum);
   const uint32_t tt = tag | taint_bits(__ballot(lost) != 0);
-  if (lane != 0) return;
   uint64_t* nw = A.norm + ((int64_t)set * RM + rr) * 3;
   if (NEED_SUM) {
-    // log2 normaliser o + log2(sum) as an unevaluated sum hi + lo (TwoSum)
+    // log2 normaliser o + log2(sum) as an unevaluated sum hi + lo (TwoSum); lane c writes
+    // copy c
     const float l2 = log2f(sum);
     const float hi = o + l2;
     const float bb = hi - o;
     const float lo = (o - (hi - bb)) + (l2 - bb);
-    put_word(nw, word_of(hi, tt));
-    put_word(nw + 1, word_of(lo, tt));
+    if (lane < NC) {
+      uint64_t* cw = norm_copy(A, lane, RM) + ((int64_t)set * RM + rr) * 3;
+      put_word(cw, word_of(hi, tt));
+      put_word(cw + 1, word_of(lo, tt));
+    }
   }
+  if (lane != 0) return;
   if (NEED_ARG) {
     put_word(nw + 2, word_of(idx, tt));
     if (rr == 0) {
@@ -555,12 +568,12 @@ __device__ inline int duty_index(int s, int rot, int S) { return s >= rot ? s - 
 
 // ---- 4. fold duty: rows i, i + S, ... of the row set (i = the slot's duty index for the
 // item's rotation rot), spread over the waves, wave `first` taking the first ----
-template <int D, bool NEED_SUM, bool NEED_ARG>
+template <int D, bool NEED_SUM, bool NEED_ARG, int NC = 1>
 __device__ __forceinline__ void fold_item(const TeamArgs& A, const ItemPos& q, uint32_t tag,
                                           int lane, int wv, int first, int rot = 0) {
   const int order = (wv + kWaves - first) % kWaves;
   for (int rr = duty_index(q.s, rot, A.S) + order * A.S; rr <= q.n; rr += kWaves * A.S)
-    fold_row<D, NEED_SUM, NEED_ARG>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
+    fold_row<D, NEED_SUM, NEED_ARG, NC>(A, q.set, rr, q.b, q.k, q.sub, tag, lane);
 }
 
 // ---- 5. normalisers (the duty wave; a barrier follows): lanes 2r and 2r + 1 wait for row r's hi and
@@ -575,8 +588,11 @@ __device__ __forceinline__ void await_norms(const TeamArgs& A, const ItemPos& q,
   float h = 0.0f;
   bool lost = false;
   if (lane < 2 * (q.n + 1)) {
+    constexpr int NC = KEPT ? kNormCopies : 1;  // the single-item kernel's fold writes copies
     const uint64_t w =
-        await_word(A.norm + ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1), tag, A);
+        await_word(norm_copy(A, q.s & (NC - 1), D + 1) +
+                       ((int64_t)q.set * (D + 1) + (lane >> 1)) * 3 + (lane & 1),
+                   tag, A);
     h = word_f(w);
     lost = tainted(w);
   }
@@ -1043,7 +1059,7 @@ __global__ __launch_bounds__(kThreads, 4) void hs_team_kernel(TeamArgs A) {
         const float sm = row16_sum(sum16(v));
         if (gl == 0 && gi <= q.n) publish_row<true, NEED_ARG>(A, q, gi, tag, m, sm, idx, RM);
       }
-      fold_item<D, true, NEED_ARG>(A, q, tag, lane, wv, 0);
+      fold_item<D, true, NEED_ARG, kNormCopies>(A, q, tag, lane, wv, 0);
       __builtin_amdgcn_s_setprio(0);
       // with one item per workgroup the leader counts its team once it has folded row 0 (every
       // member has published, so has read the tag), not at its end: the count's round trip
@@ -1271,9 +1287,11 @@ int launch_round(const TeamGeom& g, const RowTable& rows, float c, bool need_sum
   A.argmax_t = argmax_t;
   A.argmax_d = argmax_d;
   A.agree = agree;
+  // the gamma words (the learner step in the same launch); the single-item kernel's extra
+  // normaliser copies follow them
+  A.gw = reinterpret_cast<uint64_t*>(ws + L.gw);
   if (tail) {  // the learner step in the same launch, when its LDS fits
     A.learn = tail->gamma_src;
-    A.gw = reinterpret_cast<uint64_t*>(ws + L.gw);
     A.tail = *tail;
   }
   bool learned = false;

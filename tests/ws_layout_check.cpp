@@ -32,9 +32,13 @@ int main() {
     for (size_t r : regions) CHECK(r % 256 == 0);
     const size_t sets = (size_t)g.G * g.nsub, rows = (size_t)g.D + 1;
     CHECK(L.norm >= L.stat + 24 * sets * rows * g.S);
-    CHECK(L.part >= L.norm + 24 * sets * rows);
+    // the normaliser words, and kNormCopies - 1 more copies after the gamma words (the
+    // single-item kernel's), each 256-byte aligned and large enough
+    CHECK(L.norm_copy % 256 == 0 && L.norm_copy >= 24 * sets * rows);
+    CHECK(L.part >= L.norm + L.norm_copy);
     CHECK(L.gw >= L.part + 8 * (size_t)g.G * g.N * g.S);
-    CHECK(L.total >= L.gw + 8 * (size_t)g.B * g.N * g.K);
+    CHECK(L.total >= hs::align256(L.gw + 8 * (size_t)g.B * g.N * g.K) +
+                         (size_t)(hs::kNormCopies - 1) * L.norm_copy);
     // the tag of every epoch is 31-bit and never 0 (the content of a zeroed workspace)
     const unsigned eps[] = {0u, 1u, 0x7FFFFFFEu, 0x7FFFFFFFu, 0x80000000u, 0xFFFFFFFFu};
     for (unsigned e : eps) {
