@@ -21,7 +21,7 @@ _SRC = os.path.join(_HERE, "hs_oracle.c")
 # HS_ORACLE_LIB: a build of hs_oracle.c to load instead (the sanitizer test's instrumented one)
 _LIB = os.environ.get("HS_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
-F32, BF16 = 0, 1
+F32, BF16, F16 = 0, 1, 2
 LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
 _lib = None
 
@@ -84,7 +84,10 @@ def _dtype_of(x: np.ndarray) -> int:
         return F32
     if x.dtype == np.uint16:
         return BF16
-    raise TypeError("logits must be float32 or uint16 (bf16 bit patterns), got %s" % x.dtype)
+    if x.dtype == np.float16:
+        return F16
+    raise TypeError("logits must be float32, float16 or uint16 (bf16 bit patterns), got %s"
+                    % x.dtype)
 
 
 def set_threads(n: int) -> None:

@@ -12,6 +12,8 @@
  * Built with -O2 -fno-fast-math -ffp-contract=off.
  *
  * Parity status of each routine (pins live in the CPU test suite):
+ *   or_decode               : pinned (every fp16 bit pattern against numpy's binary16 type;
+ *                             fp16 inputs give exactly the fp32 results for the same values).
  *   or_row_stats, or_alpha  : pinned (identities of Theorem 1, closed form for a
  *                             boosted token, brute-force enumeration of the
  *                             speculative-decoding box, disjoint supports).
@@ -46,14 +48,28 @@
 
 #define OR_F32 0
 #define OR_BF16 1
+#define OR_F16 2
 
 #define OR_LOSS_LENGTH 0
 #define OR_LOSS_ACCEPT_TOKEN 1
 #define OR_LOSS_ACCEPT_CHUNK 2
 
-/* Exact decode of one stored logit to fp64: bf16 is the top half of an fp32. */
+/*
+ * Exact decode of one stored logit to fp64: bf16 is the top half of an fp32; fp16 (the
+ * precision the paper's models were served in, Section "Experiment setup and baselines") is
+ * IEEE 754 binary16: 1 sign bit, 5 exponent bits with bias 15, 10 fraction bits; exponent
+ * field 0 holds zero and the subnormals f 2^-24, field 31 infinity (f = 0) and NaN.
+ */
 static double or_decode(const void* base, int dtype, int64_t idx) {
   if (dtype == OR_F32) return (double)((const float*)base)[idx];
+  if (dtype == OR_F16) {
+    const uint16_t h = ((const uint16_t*)base)[idx];
+    const int ex = (h >> 10) & 0x1F, fr = h & 0x3FF;
+    const double sg = (h & 0x8000) ? -1.0 : 1.0;
+    if (ex == 0x1F) return fr ? NAN : sg * INFINITY;
+    if (ex == 0) return sg * ldexp((double)fr, -24);
+    return sg * ldexp(1024.0 + fr, ex - 25);
+  }
   uint32_t u = (uint32_t)((const uint16_t*)base)[idx] << 16;
   float f;
   memcpy(&f, &u, 4);

@@ -26,7 +26,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")
 _LIB = os.path.join(_HERE, "libsynth.so")
 
-F32, BF16 = 0, 1
+F32, BF16, F16 = 0, 1, 2
 _lib = None
 
 
@@ -62,6 +62,8 @@ def _load():
         lib.synth_row_key.restype = ctypes.c_uint64
         lib.synth_row_key.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_int64]
+        lib.synth_round_f16.restype = ctypes.c_uint16
+        lib.synth_round_f16.argtypes = [ctypes.c_double]
         lib.synth_boost_indices.restype = ctypes.c_int
         lib.synth_boost_indices.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
                                             ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
@@ -250,7 +252,7 @@ def generate(w: Workload, round: int = 0, rows: Optional[Sequence[int]] = None,
     """Logits of one round.
 
     Returns an array of shape [len(rows)][B][K][ld] (bk None) or [len(rows)][len(bk)][ld],
-    uint16 (bf16 bit patterns) or float32. Only the first V entries of each row are written
+    uint16 (bf16 bit patterns), float16 or float32. Only the first V entries of each row are written
     (padding beyond V is zero). rows defaults to all N+1 rows (0 = target, 1+i = drafter i).
     """
     lib = _load()
@@ -262,7 +264,7 @@ def generate(w: Workload, round: int = 0, rows: Optional[Sequence[int]] = None,
         bk_a = np.ascontiguousarray(np.asarray(bk, dtype=np.int32).reshape(-1, 2))
         nbk = bk_a.shape[0]
         shape = (len(rows_a), nbk, w.row_ld)
-    dt = np.float32 if w.dtype == F32 else np.uint16
+    dt = {F32: np.float32, BF16: np.uint16, F16: np.float16}[w.dtype]
     if out is None:
         out = np.zeros(shape, dtype=dt)
     else:
@@ -283,6 +285,11 @@ def bf16_bits_to_f64(a: np.ndarray) -> np.ndarray:
 
 def decode(w: Workload, a: np.ndarray) -> np.ndarray:
     return bf16_bits_to_f64(a) if w.dtype == BF16 else a.astype(np.float64)
+
+
+def round_f16(x: float) -> int:
+    """The binary16 bit pattern the generator stores for the fp64 value x (via fp32)."""
+    return int(_load().synth_round_f16(float(x)))
 
 
 def synthetic_losses(seed: int, rounds: int, L: int, B: int, N: int) -> np.ndarray:

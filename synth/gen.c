@@ -20,7 +20,9 @@
  *   drafter i  : d = decode(stored t) + s * Z_i, rounded (the noise is added to
  *                exactly what the kernel reads).
  *   rounding   : fp64 -> fp32 round-to-nearest-even, then (bf16 storage)
- *                fp32 -> bf16 round-to-nearest-even on the bit pattern.
+ *                fp32 -> bf16 round-to-nearest-even on the bit pattern, or (fp16
+ *                storage) fp32 -> IEEE binary16 round-to-nearest-even, with
+ *                gradual underflow and overflow to infinity.
  * Build with -ffp-contract=off so that no multiply-add is fused.
  */
 #include <stdint.h>
@@ -30,6 +32,7 @@
 
 #define SYN_F32 0
 #define SYN_BF16 1
+#define SYN_F16 2
 
 static const uint64_t GOLD = 0x9E3779B97F4A7C15ULL;
 
@@ -77,12 +80,60 @@ static inline float bf16_to_f32(uint16_t h) {
   return f;
 }
 
+/* fp32 -> IEEE 754 binary16 (1 sign, 5 exponent, 10 fraction bits, bias 15), round to
+   nearest, ties to even. */
+static inline uint16_t f32_to_f16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  const uint32_t sign = (u >> 16) & 0x8000u;
+  const uint32_t a = u & 0x7FFFFFFFu;
+  if (a > 0x7F800000u) return (uint16_t)(sign | 0x7E00u); /* NaN: a quiet NaN */
+  if (a >= 0x477FF000u) return (uint16_t)(sign | 0x7C00u); /* >= 65520 rounds to infinity */
+  const int e = (int)(a >> 23) - 127;
+  const uint32_t sig = (a & 0x7FFFFFu) | 0x800000u; /* 24-bit significand (normal inputs) */
+  if (e >= -14) {                                    /* a binary16 normal */
+    uint32_t h = ((uint32_t)(e + 15) << 10) | ((a & 0x7FFFFFu) >> 13);
+    const uint32_t rem = a & 0x1FFFu;
+    if (rem > 0x1000u || (rem == 0x1000u && (h & 1u))) h += 1u; /* a carry moves the exponent */
+    return (uint16_t)(sign | h);
+  }
+  /* a binary16 subnormal m 2^-24: m = sig 2^(e + 1), rounded */
+  const int sh = -(e + 1);
+  if (sh >= 32) return (uint16_t)sign; /* below 2^-32: rounds to zero */
+  uint32_t m = sig >> sh;
+  const uint32_t rem = sig & ((1u << sh) - 1u), half = 1u << (sh - 1);
+  if (rem > half || (rem == half && (m & 1u))) m += 1u; /* 1024 is the smallest normal */
+  return (uint16_t)(sign | m);
+}
+
+static inline float f16_to_f32(uint16_t h) {
+  const uint32_t sign = (uint32_t)(h & 0x8000u) << 16;
+  const uint32_t ex = (h >> 10) & 0x1Fu, m = h & 0x3FFu;
+  float f;
+  if (ex == 0) {
+    f = ldexpf((float)m, -24);
+    if (sign) f = -f;
+    return f;
+  }
+  const uint32_t u = ex == 0x1Fu ? (sign | 0x7F800000u | (m << 13)) : (sign | ((ex + 112u) << 23) | (m << 13));
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+/* The binary16 bit pattern of an fp64 value as the generator stores it (fp32 first). */
+uint16_t synth_round_f16(double x) { return f32_to_f16_rne((float)x); }
+
 /* Round an fp64 value to the storage type; returns the stored value decoded back. */
 static inline double store_one(double x, int dtype, void* out, int64_t idx) {
   float f = (float)x;
   if (dtype == SYN_F32) {
     ((float*)out)[idx] = f;
     return (double)f;
+  }
+  if (dtype == SYN_F16) {
+    uint16_t h = f32_to_f16_rne(f);
+    ((uint16_t*)out)[idx] = h;
+    return (double)f16_to_f32(h);
   }
   uint16_t h = f32_to_bf16_rne(f);
   ((uint16_t*)out)[idx] = h;
@@ -120,7 +171,7 @@ int synth_boost_indices(uint64_t seed, int64_t round, int64_t b, int64_t k, int6
 int synth_fill(int dtype, int64_t V, int64_t ld, int B, int K, int N, uint64_t seed, int64_t round,
                double sigma_t, int nboost, double boost, const double* scale, const int32_t* rows,
                int nrows, const int32_t* bk, int64_t nbk, void* out) {
-  if (dtype != SYN_F32 && dtype != SYN_BF16) return -1;
+  if (dtype != SYN_F32 && dtype != SYN_BF16 && dtype != SYN_F16) return -1;
   if (V < 1 || ld < V || B < 1 || K < 1 || N < 1 || nboost < 0 || nboost > V) return -2;
   int64_t nitems = (bk ? nbk : (int64_t)B * K);
   int fail = 0;
