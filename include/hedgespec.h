@@ -54,13 +54,15 @@ extern "C" {
 #define HS_MAX_POSITIONS 64 /* K (chain positions) or M (tree nodes)                */
 #define HS_MAX_QUERIES 65535
 #define HS_MAX_TOPL 32      /* L: children per draft-tree node in hs_eval_topl           */
-/* V: at most 512 * 256 16-byte vectors per row (1048576 bf16 or 524288 fp32 logits), and
-   the device must hold ceil(V / 2048) (bf16) or ceil(V / 1024) (fp32) evaluation
-   workgroups at once: hs_eval_alpha returns HS_ERR_LIMIT otherwise. */
+/* V: at most 512 * 256 16-byte vectors per row (1048576 bf16 or fp16, or 524288 fp32
+   logits), and the device must hold ceil(V / 2048) (bf16, fp16) or ceil(V / 1024) (fp32)
+   evaluation workgroups at once: hs_eval_alpha returns HS_ERR_LIMIT otherwise. */
 
 /* ---- enumerations ------------------------------------------------------------------------- */
 #define HS_F32 0  /* fp32 logits                            */
 #define HS_BF16 1 /* bf16 logits (upper half of an fp32)    */
+#define HS_F16 2  /* fp16 logits (IEEE 754 binary16), the precision the paper's models were
+                     served in (Section "Experiment setup and baselines") */
 
 #define HS_SAMPLE 0 /* gamma = alpha, speculative sampling at temperature T (Theorem 1)        */
 #define HS_GREEDY 1 /* gamma = argmax agreement, Theorem 1 with one-hot p and q (greedy)       */
@@ -76,7 +78,7 @@ extern "C" {
  * A [B][K][V] logits tensor: element (b, k, v) is at
  * ptr + (b * stride_b + k * stride_k + v) * element_size. V is contiguous.
  * Strides are in elements. ptr and every row start must be 16-byte aligned
- * (strides multiples of 4 for fp32 and of 8 for bf16).
+ * (strides multiples of 4 for fp32 and of 8 for bf16 and fp16).
  */
 typedef struct hs_view {
   const void* ptr;

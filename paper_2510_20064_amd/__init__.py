@@ -20,7 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("HS_LIBRARY") or os.path.join(_HERE, "libhedgespec.so")
 
 HS_OK = 0
-HS_F32, HS_BF16 = 0, 1
+HS_F32, HS_BF16, HS_F16 = 0, 1, 2
 SAMPLE, GREEDY = 0, 1
 LOSS_LENGTH, LOSS_ACCEPT_TOKEN, LOSS_ACCEPT_CHUNK = 0, 1, 2
 MAX_DRAFTERS = 64
@@ -126,7 +126,9 @@ def _dtype_code(t: torch.Tensor) -> int:
         return HS_F32
     if t.dtype in (torch.bfloat16, torch.uint16, torch.int16):
         return HS_BF16
-    raise TypeError("logits must be float32 or bfloat16, got %s" % t.dtype)
+    if t.dtype == torch.float16:
+        return HS_F16
+    raise TypeError("logits must be float32, bfloat16 or float16, got %s" % t.dtype)
 
 
 def _view(t: torch.Tensor) -> hs_view:

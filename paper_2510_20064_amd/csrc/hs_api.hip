@@ -78,7 +78,8 @@ struct EvalReq {
 int validate_eval(const EvalReq& q, hs::TeamGeom* g, hs::RowTable* rows) {
   int rc = check_shape(q.B, q.N, q.K, q.V);
   if (rc) return rc;
-  if (q.dtype != HS_F32 && q.dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
+  if (q.dtype != HS_F32 && q.dtype != HS_BF16 && q.dtype != HS_F16)
+    return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
   if (q.mode != HS_SAMPLE && q.mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", q.mode);
   if (!q.drafters) return fail(HS_ERR_NULL, "drafters_host is NULL");
   if ((rc = check_view(q.target, q.dtype, "target"))) return rc;
@@ -228,7 +229,8 @@ HS_API int hs_softmax_stats(const void* logits, int dtype, int64_t rows, int64_t
                             float temperature, float* row_max, float* row_lse,
                             int32_t* row_argmax, void* stream) {
   if (!logits) return fail(HS_ERR_NULL, "logits is NULL");
-  if (dtype != HS_F32 && dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", dtype);
+  if (dtype != HS_F32 && dtype != HS_BF16 && dtype != HS_F16)
+    return fail(HS_ERR_DTYPE, "unknown dtype %d", dtype);
   if (rows < 1 || V < 1 || ld < V) return fail(HS_ERR_SHAPE, "need rows >= 1, 1 <= V <= ld");
   if (rows > INT32_MAX || V > INT32_MAX) return fail(HS_ERR_LIMIT, "rows and V must be < 2^31");
   if (!(isfinite(temperature) && temperature > 0.0f))
@@ -353,7 +355,8 @@ struct TopReq {
 int validate_topl(const TopReq& q, hs::TeamGeom* g, hs::RowTable* rows) {
   int rc = check_shape(q.B, q.N, q.K, q.V);
   if (rc) return rc;
-  if (q.dtype != HS_F32 && q.dtype != HS_BF16) return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
+  if (q.dtype != HS_F32 && q.dtype != HS_BF16 && q.dtype != HS_F16)
+    return fail(HS_ERR_DTYPE, "unknown dtype %d", q.dtype);
   if (q.mode != HS_SAMPLE && q.mode != HS_GREEDY) return fail(HS_ERR_ARG, "unknown mode %d", q.mode);
   if (q.L < 1 || q.L > HS_MAX_TOPL || q.L > q.V)
     return fail(HS_ERR_SHAPE, "need 1 <= L <= min(V, %d) (got L=%d, V=%lld)", HS_MAX_TOPL, q.L,

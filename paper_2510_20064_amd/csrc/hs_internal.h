@@ -22,7 +22,7 @@ constexpr int kMaxTeams = 4096;        // teams resident at once (one mailbox ri
 // by a quarter of them
 constexpr int kNormCopies = 4;
 
-// Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 logits.
+// Per-storage-type 16-byte vector: 4 fp32 or 8 bf16 or fp16 logits.
 template <int DT>
 struct Vec;
 template <>
@@ -61,27 +61,38 @@ struct Vec<HS_F32> {
     }
   }
 };
-template <>
-struct Vec<HS_BF16> {
+// 8 16-bit logits per vector: bf16 (the upper half of an fp32) or fp16 (IEEE 754 binary16,
+// converted exactly by the hardware's half-to-float conversion).
+template <bool F16>
+struct Vec16 {
   static constexpr int kElems = 8;
   static constexpr int kBytes = 2;
   static constexpr int kU = kSliceElems / (kThreads * kElems);
-  __device__ static inline float lo(uint32_t w) { return __uint_as_float(w << 16); }
-  __device__ static inline float hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+  static constexpr uint32_t kNegInf = F16 ? 0xFC00u : 0xFF80u;  // -inf
+  // the value of the low (lo) or high (hi) half of a 32-bit word
+  __device__ static inline float lo(uint32_t w) {
+    if constexpr (F16) return (float)__builtin_bit_cast(_Float16, (uint16_t)w);
+    else return __uint_as_float(w << 16);
+  }
+  __device__ static inline float hi(uint32_t w) {
+    if constexpr (F16) return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+    else return __uint_as_float(w & 0xFFFF0000u);
+  }
   using Raw = uint4;
-  // raw 16-byte vector vi of a row (logits beyond V read as -inf, bf16 0xFF80)
+  // raw 16-byte vector vi of a row (logits beyond V read as -inf)
   __device__ static inline Raw load_raw(const char* rowp, int64_t vi, int64_t V) {
     if ((vi + 1) * kElems <= V) return *reinterpret_cast<const uint4*>(rowp + vi * 16);
     const uint16_t* p = reinterpret_cast<const uint16_t*>(rowp);
     uint32_t h[kElems];
 #pragma unroll
-    for (int e = 0; e < kElems; ++e) h[e] = vi * kElems + e < V ? p[vi * kElems + e] : 0xFF80u;
+    for (int e = 0; e < kElems; ++e) h[e] = vi * kElems + e < V ? p[vi * kElems + e] : kNegInf;
     return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
                       h[6] | (h[7] << 16));
   }
   __device__ static inline Raw zero_raw() { return make_uint4(0u, 0u, 0u, 0u); }
-  __device__ static inline Raw neg_raw() {  // four pairs of bf16 -inf
-    return make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+  __device__ static inline Raw neg_raw() {  // four pairs of -inf
+    constexpr uint32_t w = kNegInf | (kNegInf << 16);
+    return make_uint4(w, w, w, w);
   }
   __device__ static inline void unpack(const Raw& x, float* z) {
     z[0] = lo(x.x); z[1] = hi(x.x); z[2] = lo(x.y); z[3] = hi(x.y);
@@ -90,18 +101,21 @@ struct Vec<HS_BF16> {
   __device__ static inline void load(const char* rowp, int64_t vi, int64_t V, float* z) {
     if ((vi + 1) * kElems <= V) {
       uint4 x = *reinterpret_cast<const uint4*>(rowp + vi * 16);
-      z[0] = lo(x.x); z[1] = hi(x.x); z[2] = lo(x.y); z[3] = hi(x.y);
-      z[4] = lo(x.z); z[5] = hi(x.z); z[6] = lo(x.w); z[7] = hi(x.w);
+      unpack(x, z);
     } else {
       const uint16_t* p = reinterpret_cast<const uint16_t*>(rowp);
 #pragma unroll
       for (int e = 0; e < kElems; ++e) {
         int64_t idx = vi * kElems + e;
-        z[e] = idx < V ? __uint_as_float((uint32_t)p[idx] << 16) : -INFINITY;
+        z[e] = idx < V ? lo(p[idx]) : -INFINITY;
       }
     }
   }
 };
+template <>
+struct Vec<HS_BF16> : Vec16<false> {};
+template <>
+struct Vec<HS_F16> : Vec16<true> {};
 
 // Division of a 32-bit value by a divisor fixed for the launch, by a multiply-high and two
 // shifts (Granlund and Montgomery, "Division by invariant integers using multiplication",
@@ -151,7 +165,7 @@ inline bool team_geom(int B, int N, int K, int64_t V, int dtype, TeamGeom* g) {
   if (B < 1 || N < 1 || K < 1 || V < 1) return false;
   if (B > HS_MAX_QUERIES || N > HS_MAX_DRAFTERS || K > HS_MAX_POSITIONS || V > INT32_MAX)
     return false;
-  if (dtype != HS_F32 && dtype != HS_BF16) return false;
+  if (dtype != HS_F32 && dtype != HS_BF16 && dtype != HS_F16) return false;
   const int E = dtype == HS_F32 ? 4 : 8;
   g->B = B;
   g->N = N;

@@ -366,7 +366,7 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, 
     }
   }
   // uniform row base + 32-bit lane offset (a row holds < 2^31 logits); a global (not flat)
-  // 16-byte load. bf16 rows load nontemporal (every logit is read once; the target slice of
+  // 16-byte load. 16-bit rows load nontemporal (every logit is read once; the target slice of
   // a group's later row sets still comes from L2): 1% faster on every bf16 workload measured,
   // but 19% slower on 64 stacked fp32 tiny chains, so fp32 rows load plainly
   typedef unsigned int u4 __attribute__((ext_vector_type(4)));
@@ -376,7 +376,7 @@ __device__ __forceinline__ void fetch_item(const TeamArgs& A, const ItemPos& q, 
   for (int r = 0; r <= D; ++r) {
     const uint32_t o = r <= q.n ? off : 0u;
     typedef const __attribute__((address_space(1))) u4* gp4;
-    const u4 v = DT == HS_BF16 ? __builtin_nontemporal_load((gp4)(rb[r] + o)) : *(gp4)(rb[r] + o);
+    const u4 v = DT != HS_F32 ? __builtin_nontemporal_load((gp4)(rb[r] + o)) : *(gp4)(rb[r] + o);
     __builtin_memcpy(&dst[r], &v, 16);
   }
   if (valid && vfull < A.nvec && (int64_t)(q.s + 1) * kThreads > vfull) {  // the tail slice
@@ -1214,6 +1214,7 @@ int by_set(int D, bool ns, bool na, Args&&... args) {
 template <template <int, int, bool, bool> class F, typename... Args>
 int dispatch(const TeamGeom& g, bool ns, bool na, Args&&... args) {
   if (g.dtype == HS_F32) return by_set<F, HS_F32>(g.D, ns, na, args...);
+  if (g.dtype == HS_F16) return by_set<F, HS_F16>(g.D, ns, na, args...);
   return by_set<F, HS_BF16>(g.D, ns, na, args...);
 }
 

@@ -49,8 +49,9 @@ constexpr uint64_t kFlip64 = 0x8000000000000000ull;
 
 // ---- integer images of logits --------------------------------------------------------------
 
-// Two bf16 logits (one 32-bit word) to two int16 that order like the values, -0 as +0:
-// magnitude for a positive value, minus the magnitude for a negative one.
+// Two 16-bit sign-magnitude logits (bf16 or fp16; one 32-bit word) to two int16 that order
+// like the values, -0 as +0: magnitude for a positive value, minus the magnitude for a
+// negative one.
 __device__ inline uint32_t bf16x2_ordered(uint32_t w) {
   typedef short s2 __attribute__((ext_vector_type(2)));
   s2 x;
@@ -111,6 +112,9 @@ struct KeyOf<HS_BF16> {
     return (int64_t)((uint64_t)(int64_t)(k >> 16) << 48) | (int64_t)(0xFFFFFFFFu - (uint32_t)g);
   }
 };
+// fp16 (IEEE binary16) is sign-magnitude in 16 bits like bf16: the same keys order it.
+template <>
+struct KeyOf<HS_F16> : KeyOf<HS_BF16> {};
 template <>
 struct KeyOf<HS_F32> {
   using K = int64_t;
@@ -246,13 +250,13 @@ __device__ inline typename Vec<DT>::Raw load_vec(const char* rowp, int64_t vi, i
                                                  int64_t V, bool tail) {
   using Vt = Vec<DT>;
   if (!tail) {
-    // nontemporal for bf16 (every logit is read once): 4% faster on large_pool_stream and 7% on
-    // the single query than plain loads
+    // nontemporal for 16-bit logits (every logit is read once): 4% faster on large_pool_stream
+    // and 7% on the single query than plain loads (bf16)
     typename Vt::Raw r;
     typedef unsigned int u4 __attribute__((ext_vector_type(4)));
     typedef const __attribute__((address_space(1))) u4* gp4;
-    const u4 v = DT == HS_BF16 ? __builtin_nontemporal_load((gp4)(rowp + vi * 16))
-                               : *(gp4)(rowp + vi * 16);
+    const u4 v = DT != HS_F32 ? __builtin_nontemporal_load((gp4)(rowp + vi * 16))
+                              : *(gp4)(rowp + vi * 16);
     __builtin_memcpy(&r, &v, 16);
     return r;
   }
@@ -651,10 +655,10 @@ __global__ __launch_bounds__(kThreads) void hs_topl_merge_kernel(TopArgs A) {
   if (win) {
     const char* trow = reinterpret_cast<const char*>(A.rows.ptr[0]) +
                        ((int64_t)b * A.rows.sb[0] + (int64_t)k * A.rows.sk[0]) * Vec<DT>::kBytes;
-    if (DT == HS_BF16)
-      zt = __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(trow)[gidx] << 16);
-    else
+    if constexpr (DT == HS_F32)
       zt = reinterpret_cast<const float*>(trow)[gidx];
+    else
+      zt = Vec<DT>::lo(reinterpret_cast<const uint16_t*>(trow)[gidx]);
   }
   if (A.gamma) {
     const float e = win ? __builtin_amdgcn_exp2f(fmaf(zt, A.c, -o)) : 0.0f;
@@ -717,6 +721,7 @@ int launch_topl(const TeamGeom& g, const RowTable& rows, int L, float c, bool wa
   A.hit = hit;
   A.idx = idx;
   if (g.dtype == HS_BF16) launch_t<HS_BF16>(A, (int64_t)nrows, stream);
+  else if (g.dtype == HS_F16) launch_t<HS_F16>(A, (int64_t)nrows, stream);
   else launch_t<HS_F32>(A, (int64_t)nrows, stream);
   return hipGetLastError() == hipSuccess ? HS_OK : HS_ERR_HIP;
 }
