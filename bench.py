@@ -99,6 +99,15 @@ def measured_topl_traffic(workload: str):
     return rec["hbm_bytes_per_call"]
 
 
+def logit_type(w) -> str:
+    return ("fp32", "bf16", "fp16")[w.dtype]
+
+
+def profile_name(w, name: str) -> str:
+    """The counter summary that covers this run (the workloads' own storage types have one)."""
+    return name + "_f16" if w.dtype == 2 and not name.endswith("_f16") else name
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -112,6 +121,8 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline, two thirds on all "
                          "cores and one third on one thread (0 = skip)")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--f16", action="store_true",
+                    help="store the workload's logits as fp16 (IEEE binary16) instead")
     ap.add_argument("--greedy", action="store_true",
                     help="evaluate in greedy argmax-agreement mode (the workload's second run)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -301,15 +312,14 @@ def bench_softmax_stats(args, w, hs, torch, dev, synth):
             b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    eb = 2 if w.dtype == synth.BF16 else 4
-    nbytes = rows * w.V * eb + rows * 12
+    nbytes = rows * w.V * w.elem_bytes + rows * 12
     achieved = nbytes / (us * 1e-6) / 1e9
     line = {"metric": "softmax row statistics: rows per second + achieved HBM GB/s",
             "value": rows / (us * 1e-6), "unit": "rows/s", "n_gpus": 1,
             "steps": reps * copies, "warmup": max(1, args.warmup // copies) * copies,
             "us_per_call": us, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
             "config": {"workload": w.name, "rows": rows, "V": w.V,
-                       "logits": "bf16" if w.dtype == synth.BF16 else "f32",
+                       "logits": logit_type(w),
                        "temperature": w.temperature, "rotation_copies": copies,
                        "hip_graph": True},
             "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
@@ -404,13 +414,13 @@ def bench_topl(args, w, hs, torch, dev, np, synth):
             "ms_per_step": us * 1e-3, "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "i32 keys, f32 mass", "data": "synthetic",
             "config": {"workload": w.name, "B": w.B, "N": w.N, "K": w.K, "V": w.V, "L": L,
-                       "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
+                       "logits": logit_type(w),
                        "temperature": w.temperature, "mode": "greedy" if greedy else "sample",
                        "rotation_copies": copies, "input_bytes_per_step": w.input_bytes,
                        "hip_graph": True, "wall_s": round(wall, 4)},
             "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                         "traffic": measured_topl_traffic(w.name),
+                         "traffic": measured_topl_traffic(profile_name(w, w.name)),
                          "kernel": "hs_eval_topl = hs_topl_slice_kernel + hs_topl_merge_kernel "
                                    "(one call, both launches timed)",
                          "kernel_us": us, "algorithmic_bytes_per_launch": w.input_bytes},
@@ -438,6 +448,8 @@ def main():
         w = synth.variant(w, mode=synth.GREEDY)
     if args.stack > 1:  # R independent instances: R times the queries, each its own logits
         w = synth.variant(w, B=w.B * args.stack)
+    if args.f16:
+        w = synth.variant(w, dtype=synth.F16)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.delayed:
@@ -626,7 +638,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "N": w.N, "K": w.K, "V": w.V,
-                   "logits": "bf16" if w.dtype == synth.BF16 else "fp32",
+                   "logits": logit_type(w),
                    "temperature": w.temperature, "mode": "greedy" if greedy else "sample",
                    "loss": ("length", "accept_token", "accept_chunk")[w.loss],
                    "learners": "hedge+normalhedge", "tree": bool(w.tree),
@@ -634,7 +646,7 @@ def main():
                    "input_bytes_per_step": w.input_bytes, "hip_graph": use_graph,
                    "wall_s": round(wall, 4)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(name),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(profile_name(w, name)),
                      "kernel": "hs_eval_alpha = hs_team_kernel (one launch)",
                      "kernel_us": eval_us, "kernel_calls_timed": n_eval,
                      "algorithmic_bytes_per_launch": w.input_bytes,
