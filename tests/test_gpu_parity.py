@@ -270,7 +270,7 @@ def _bf16_bits(a: np.ndarray) -> np.ndarray:
     return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
-@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.F16])
 def test_argmax_ties_across_slices_and_workgroups(dtype):
     note("argmax ties across slice boundaries, dtype %d" % dtype)
     V = 40000
@@ -282,7 +282,7 @@ def test_argmax_ties_across_slices_and_workgroups(dtype):
     x[2, 0, 0, [5, 6]] = 9.0                    # tie inside one vector
     x[3, 0, 0, [8192]] = 9.0
     x[:, 0, 1, :] = 0.0                         # all-equal rows: argmax 0
-    xs = _bf16_bits(x) if dtype == synth.BF16 else x
+    xs = _bf16_bits(x) if dtype == synth.BF16 else x.astype(np.float16) if dtype == synth.F16 else x
     got, _ = check_eval(w, xs)
     assert got["argmax_t"][0, 0] == 7999 and list(got["argmax_d"][0, :, 0]) == [20000, 5, 8192]
     assert list(got["argmax_d"][0, :, 1]) == [0, 0, 0]

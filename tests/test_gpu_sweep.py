@@ -159,23 +159,24 @@ def test_eval_alpha_at_the_vocabulary_limit(case):
 def _dead_rows_case(B, N, K, V, dtype, dead, nan_logit=False):
     """Logits with whole rows at -inf (or, nan_logit, one NaN logit in each such row plus a
     large logit elsewhere): dead = list of (row, b, k), row 0 the target."""
-    step = 8 if dtype == synth.BF16 else 4
+    step = 4 if dtype == synth.F32 else 8
     w = synth.variant(BASE, B=B, N=N, K=K, V=V, ld=(V + step - 1) // step * step, dtype=dtype,
                       scales=[0.3 + 0.4 * j for j in range(N)], permute=False, seed=90)
     x = synth.generate(w)
     bf = dtype == synth.BF16
+    ft = np.float16 if dtype == synth.F16 else np.float32
     for j, (r, b, k) in enumerate(dead):
         if nan_logit:
-            x[r, b, k, (37 * j + 11) % V] = np.uint16(0x7FC0) if bf else np.float32(np.nan)
-            x[r, b, k, (53 * j + 5) % V] = np.uint16(0x4248) if bf else np.float32(50.0)
+            x[r, b, k, (37 * j + 11) % V] = np.uint16(0x7FC0) if bf else ft(np.nan)
+            x[r, b, k, (53 * j + 5) % V] = np.uint16(0x4248) if bf else ft(50.0)
         else:
-            x[r, b, k, :V] = np.uint16(0xFF80) if bf else np.float32(-np.inf)
+            x[r, b, k, :V] = np.uint16(0xFF80) if bf else ft(-np.inf)
     return w, x
 
 
 @pytest.mark.parametrize("nan_logit", [False, True])
 @pytest.mark.parametrize("shape", ["one item per team", "several items per team"])
-@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.F16])
 def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype, nan_logit):
     # Theorem 1 needs two distributions: a row of -inf logits has none, and neither has a row
     # holding a NaN logit. Alpha is NaN for every drafter when the target's row is such a row
@@ -210,7 +211,7 @@ def test_alpha_is_nan_where_a_row_has_no_distribution(shape, dtype, nan_logit):
     assert np.array_equal(got["argmax_d"], ref["argmax"][:, :, 1:].transpose(0, 2, 1))
 
 
-@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.F16])
 def test_softmax_stats_of_rows_without_a_distribution(dtype):
     # hs_softmax_stats on rows of -inf and rows holding a NaN: the normaliser is NaN, the max
     # and argmax skip the NaN (an all -inf row has max -inf at index 0); the other rows as usual
@@ -224,7 +225,7 @@ def test_softmax_stats_of_rows_without_a_distribution(dtype):
     z[3, 4000] = np.nan
     z[3, 77] = 30.0
     z[4, [0, 8999]] = np.nan
-    x = _bf16_bits(z) if dtype == synth.BF16 else z
+    x = _bf16_bits(z) if dtype == synth.BF16 else z.astype(np.float16) if dtype == synth.F16 else z
     t = torch.from_numpy(x)
     t = (t.view(torch.bfloat16) if dtype == synth.BF16 else t).cuda()
     for T in (1.0, 0.6):

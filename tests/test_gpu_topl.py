@@ -57,7 +57,7 @@ def check(x, L, V=None, T=1.0, mode=hs.SAMPLE, groups=None):
     return got
 
 
-@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32, synth.F16])
 @pytest.mark.parametrize("N", [1, 3, 8, 11])
 @pytest.mark.parametrize("L", [1, 10, 32])
 def test_topl_small_ragged(dtype, N, L):
@@ -96,7 +96,7 @@ def test_topl_ties_signed_zeros_and_infinities():
     z[0, :, 1, ::2] = -np.inf             # a target with masked tokens
     z[5] = z[0]                           # a copy of the target
     z[6] = -z[0]
-    for x in (z, _bf16(z)):
+    for x in (z, _bf16(z), z.astype(np.float16)):
         note("ties, zeros, infinities dtype=%s" % x.dtype)
         for L in (1, 7, 32):
             check(x, L, T=0.9)
