@@ -51,6 +51,8 @@ def _load():
         lib.or_eval.restype = I
         lib.or_topl.argtypes = [P, I, I64, I, I64, I64, I, D, I, P, P, P]
         lib.or_topl.restype = I
+        lib.or_candidate_mass.argtypes = [P, I, I64, I64, I64, I, I, P, D, P]
+        lib.or_candidate_mass.restype = I
         lib.or_hybrid_losses.argtypes = [P, I, I, I, I64, P]
         lib.or_hybrid_losses.restype = I
         lib.or_play.argtypes = [P, I, I, I, P, P]
@@ -169,6 +171,27 @@ def topl(logits: np.ndarray, L: int, V: Optional[int] = None, T: float = 1.0,
         raise ValueError("or_topl failed: %d" % rc)
     return {"gamma": gamma.reshape(gshape + (N,)), "hit": hit.reshape(gshape + (N,)),
             "idx": idx.reshape(gshape + (N, L))}
+
+
+def candidate_mass(target: np.ndarray, cand: np.ndarray, V: Optional[int] = None,
+                   T: float = 1.0) -> np.ndarray:
+    """Theorem 2 with dynamic pruning: the target's softmax mass on given candidate sets.
+
+    target: [G..][ld] stored logits (one target row per group); cand: [G..][N][C] int32 token
+    indices, negative = empty slot. Returns gamma [G..][N] (NaN where an index is >= V).
+    """
+    gshape = target.shape[:-1]
+    ld = target.shape[-1]
+    V = ld if V is None else V
+    G = int(np.prod(gshape)) if gshape else 1
+    x = np.ascontiguousarray(target).reshape(G, ld)
+    c = np.ascontiguousarray(np.asarray(cand, dtype=np.int32)).reshape(G, -1, cand.shape[-1])
+    N, C = c.shape[1], c.shape[2]
+    gamma = np.zeros((G, N))
+    rc = _load().or_candidate_mass(_p(x), _dtype_of(x), ld, G, V, N, C, _p(c), T, _p(gamma))
+    if rc != 0:
+        raise ValueError("or_candidate_mass failed: %d" % rc)
+    return gamma.reshape(gshape + (N,))
 
 
 def softmax_stats(x: np.ndarray, V: Optional[int] = None, T: float = 1.0):

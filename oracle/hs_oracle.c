@@ -25,6 +25,9 @@
  *                             enumeration of the dominating L-subset, ties and signed
  *                             zeros by index, invariance under exact rescaling of the
  *                             drafter, L = 1 greedy hit equals argmax agreement).
+ *   or_candidate_mass       : pinned (the kept children equal to Top_L reproduce or_topl's
+ *                             mass, every token gives 1, no token 0, a target built from a
+ *                             known distribution gives that distribution's mass).
  *   or_hybrid_losses        : pinned (H = 0 is the window loss, H >= T the acceptance loss,
  *                             the appendix's K = 8 example with a first chunk of 4 tokens).
  *   or_play                 : pinned (point masses, empirical frequencies on a uniform grid
@@ -238,6 +241,42 @@ int or_topl(const void* logits, int dtype, int64_t ld, int R, int64_t G, int64_t
     free(top);
   }
   return rc;
+}
+
+/*
+ * Theorem 2 with EAGLE-2's dynamic pruning: when the draft tree is pruned, the acceptance
+ * probability at a node is the target's mass on the node's kept children instead of on
+ * Top_L(q). Here the kept children are given: for group g (a query and position) and drafter
+ * i, cand[(g * N + i) * C + j], j < C, lists token indices; a negative entry is an empty slot,
+ * and each listed index counts once per listing. gamma[g * N + i] = sum over the listed v of
+ * softmax(z_t / T)_v, with z_t the target row of group g; an index >= V makes it NaN.
+ *   target : [G][ld] stored logits, one target row per group.
+ */
+int or_candidate_mass(const void* target, int dtype, int64_t ld, int64_t G, int64_t V, int N,
+                      int C, const int32_t* cand, double T, double* gamma) {
+  if (G < 1 || V < 1 || ld < V || N < 1 || C < 1 || !(T > 0.0)) return -1;
+  size_t es = (dtype == OR_F32) ? 4 : 2;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t g = 0; g < G; ++g) {
+    const char* zt = (const char*)target + (size_t)(g * ld) * es;
+    double m, lse;
+    int64_t am;
+    or_row_stats(zt, dtype, V, T, &m, &am, &lse);
+    for (int i = 0; i < N; ++i) {
+      double s = 0.0;
+      for (int j = 0; j < C; ++j) {
+        int32_t v = cand[(g * N + i) * C + j];
+        if (v < 0) continue;
+        if (v >= V) {
+          s = NAN;
+          break;
+        }
+        s += exp(or_decode(zt, dtype, v) / T - lse);
+      }
+      gamma[g * N + i] = s;
+    }
+  }
+  return 0;
 }
 
 /* Row statistics of `rows` rows of a [rows][ld] tensor (one temperature softmax each). */

@@ -798,3 +798,48 @@ def test_regret_eal_of_the_played_drafter_and_bad_indices():
     rb = oracle.Regret(1, 3)
     rb.update(np.zeros((1, 1, 3)), np.array([[3]], dtype=np.int32))
     assert np.isnan(rb.regret[0])
+
+
+# ------------------------------------------------------------------------------------------
+# Theorem 2 with dynamic pruning: the target's mass on a given candidate set
+# ------------------------------------------------------------------------------------------
+
+def test_candidate_mass_of_the_top_l_is_the_eagle_mass():
+    rng = np.random.default_rng(31)
+    x = rng.normal(0, 2, (4, 3, 2, 500)).astype(np.float32)  # [R][B][K][V]
+    for T in (1.0, 0.8):
+        t = oracle.topl(x, 7, T=T)
+        cm = oracle.candidate_mass(x[0], t["idx"], T=T)  # [B][K][N]
+        assert np.allclose(cm, t["gamma"], rtol=1e-12, atol=0)
+
+
+def test_candidate_mass_full_and_empty_sets_and_bad_indices():
+    rng = np.random.default_rng(32)
+    V = 50
+    x = rng.normal(0, 3, (2, V)).astype(np.float32)
+    full = np.tile(np.arange(V, dtype=np.int32), (2, 1, 1))  # [G][N=1][C=V]
+    assert np.allclose(oracle.candidate_mass(x, full, T=0.7), 1.0, rtol=0, atol=1e-12)
+    empty = np.full((2, 3, 5), -1, np.int32)
+    assert np.all(oracle.candidate_mass(x, empty) == 0.0)
+    bad = np.array([[[3, V, 4]], [[1, 2, -1]]], np.int32)
+    g = oracle.candidate_mass(x, bad)
+    assert np.isnan(g[0, 0]) and np.isfinite(g[1, 0])
+
+
+def test_candidate_mass_of_a_known_distribution():
+    # logits log p (+ any shift) have softmax p at T = 1, up to the fp32 rounding of log p
+    # (relative error below 1e-6 per token here)
+    rng = np.random.default_rng(33)
+    V = 40
+    p = rng.dirichlet(np.full(V, 0.5))
+    p = np.maximum(p, 1e-12)
+    p /= p.sum()
+    for shift in (0.0, 17.5):
+        z = (np.log(p) + shift).astype(np.float32)[None, :]
+        sets = [rng.choice(V, size=k, replace=False) for k in (1, 5, 13, V)]
+        for s in sets:
+            c = np.full((1, 1, V), -1, np.int32)
+            c[0, 0, :len(s)] = s
+            rng.shuffle(c[0, 0])  # empty slots anywhere in the list
+            got = oracle.candidate_mass(z, c)[0, 0]
+            assert abs(got - p[s].sum()) <= 5e-6 * p[s].sum() + 1e-15, (len(s), got, p[s].sum())
