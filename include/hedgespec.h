@@ -54,6 +54,7 @@ extern "C" {
 #define HS_MAX_POSITIONS 64 /* K (chain positions) or M (tree nodes)                */
 #define HS_MAX_QUERIES 65535
 #define HS_MAX_TOPL 32      /* L: children per draft-tree node in hs_eval_topl           */
+#define HS_MAX_CANDIDATES 1024 /* C: candidate slots per node in hs_candidate_mass       */
 /* V: at most 512 * 256 16-byte vectors per row (1048576 bf16 or fp16, or 524288 fp32
    logits), and the device must hold ceil(V / 2048) (bf16, fp16) or ceil(V / 1024) (fp32)
    evaluation workgroups at once: hs_eval_alpha returns HS_ERR_LIMIT otherwise. */
@@ -198,12 +199,33 @@ size_t hs_eval_topl_workspace_size(int B, int N, int K, int64_t V, int L, int dt
  * row: the target's softmax statistics, or a drafter's L best keys, 8 L bytes); the second
  * merges each drafter row's candidates and reads the target logits of its L winners.
  * Deterministic for a given shape.
- * Not covered: EAGLE-2's dynamic pruning, whose candidate set is the pruned subtree.
+ * EAGLE-2's dynamic pruning, whose candidate set is the pruned subtree: hs_candidate_mass.
  */
 int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int N, int B, int K,
                  int64_t V, int dtype, int L, float temperature, int mode, float* gamma,
                  uint8_t* hit, int32_t* children, void* workspace, size_t workspace_bytes,
                  void* stream);
+
+/*
+ * hs_candidate_mass - Theorem 2 with EAGLE-2's dynamic pruning: when the draft tree is pruned,
+ * the candidate set at a node is the node's kept children (the pruned set of descendants)
+ * instead of Top_L(q), and the target accepts one of them with probability
+ *   gamma[b][i][k] = sum_{j < C, cand[b][i][k][j] >= 0} p(cand[b][i][k][j]),
+ *   p = softmax(target[b][k] / T),
+ * accumulated in fp32 in a fixed order, not clamped (a listed index counts once per listing).
+ * target, B, K, V, dtype: as in hs_eval_alpha.
+ * target_lse   : [B][K] fp32 device, log sum_v exp(target[b][k][v] / T) (natural log), e.g.
+ *                hs_softmax_stats' row_lse over the target rows at the same T.
+ * cand         : [B][N][K][C] int32 device, the kept children (hs_eval_topl's `children`
+ *                after pruning); a negative entry is an empty slot. An index >= V makes that
+ *                gamma NaN.
+ * C            : slots per node, 1 <= C <= HS_MAX_CANDIDATES.
+ * gamma        : [B][N][K] fp32 device.
+ * One launch, one wave per output; it reads the C indices and the target logits they name.
+ */
+int hs_candidate_mass(const hs_view* target, int N, int B, int K, int64_t V, int dtype,
+                      float temperature, const float* target_lse, const int32_t* cand, int C,
+                      float* gamma, void* stream);
 
 /*
  * hs_accept_len - Theorem 3's one-step counterfactual acceptance-length

@@ -79,6 +79,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hs_eval_topl_workspace_size.argtypes = [I, I, I, I64, I, I]
     lib.hs_eval_topl_workspace_size.restype = SZ
     lib.hs_eval_topl.argtypes = [VP, VP, I, I, I, I64, I, I, F, I, P, P, P, P, SZ, P]
+    lib.hs_candidate_mass.argtypes = [VP, I, I, I, I64, I, F, P, P, I, P, P]
     lib.hs_play.argtypes = [P, I, I, I, P, P, P]
     lib.hs_regret_update.argtypes = [P, I, I, I, P, P, P, P, P, P, P]
     lib.hs_accept_len.argtypes = [P, P, I, I, I, I, P, P, P, P, I, P, P]
@@ -261,6 +262,31 @@ def eval_alpha_noalloc(target: torch.Tensor, drafters=None, V: Optional[int] = N
                                      _ptr(o.get("argmax_t")), _ptr(o.get("argmax_d")),
                                      _stream(stream)))
     return o
+
+
+def candidate_mass(target: torch.Tensor, lse: torch.Tensor, cand: torch.Tensor,
+                   V: Optional[int] = None, temperature: float = 1.0,
+                   out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """hs_candidate_mass (Theorem 2 with dynamic pruning): the target's mass on given candidate
+    sets. target [B][K][ld] logits, lse [B][K] f32 (natural-log normalisers at `temperature`,
+    e.g. softmax_stats' row_lse), cand [B][N][K][C] i32 (negative = empty slot).
+    Returns gamma [B][N][K] f32."""
+    lib = load_library()
+    B, K, ld = target.shape
+    V = ld if V is None else V
+    Bc, N, Kc, C = cand.shape
+    if (Bc, Kc) != (B, K) or cand.dtype != torch.int32 or not cand.is_contiguous():
+        raise ValueError("cand must be a contiguous int32 [B][N][K][C] tensor")
+    if lse.shape != (B, K) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 [B][K] tensor")
+    if out is None:
+        out = torch.empty((B, N, K), dtype=torch.float32, device=target.device)
+    elif out.shape != (B, N, K) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [B][N][K] tensor")
+    tv = _view(target)
+    _check(lib.hs_candidate_mass(ctypes.byref(tv), N, B, K, V, _dtype_code(target), temperature,
+                                 _ptr(lse), _ptr(cand), C, _ptr(out), _stream(stream)))
+    return out
 
 
 def topl_workspace_size(B: int, N: int, K: int, V: int, L: int, dtype: int) -> int:

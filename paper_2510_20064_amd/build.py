@@ -12,7 +12,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhedgespec.so")
 SOURCES = ["hs_api.hip", "hs_stats.hip", "hs_team.hip", "hs_tail.hip", "hs_delayed.hip",
-           "hs_topl.hip", "hs_play.hip", "hs_probe.hip"]
+           "hs_topl.hip", "hs_play.hip", "hs_probe.hip", "hs_cmass.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -422,6 +422,28 @@ HS_API int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int
   return ok();
 }
 
+HS_API int hs_candidate_mass(const hs_view* target, int N, int B, int K, int64_t V, int dtype,
+                             float temperature, const float* target_lse, const int32_t* cand,
+                             int C, float* gamma, void* stream) {
+  int rc = check_shape(B, N, K, V);
+  if (rc) return rc;
+  if (dtype != HS_F32 && dtype != HS_BF16 && dtype != HS_F16)
+    return fail(HS_ERR_DTYPE, "unknown dtype %d", dtype);
+  if ((rc = check_view(target, dtype, "target"))) return rc;
+  if (!target_lse || !cand || !gamma)
+    return fail(HS_ERR_NULL, "target_lse, cand and gamma are required");
+  if (C < 1 || C > HS_MAX_CANDIDATES)
+    return fail(HS_ERR_LIMIT, "C must be in [1, %d] (got %d)", HS_MAX_CANDIDATES, C);
+  if (!(isfinite(temperature) && temperature > 0.0f))
+    return fail(HS_ERR_TEMPERATURE, "temperature must be finite and > 0 (got %g)",
+                (double)temperature);
+  const float c = (float)(1.4426950408889634 / (double)temperature);
+  rc = hs::launch_candidate_mass(target->ptr, target->stride_b, target->stride_k, dtype, B, N, K,
+                                 V, C, c, target_lse, cand, gamma, (hipStream_t)stream);
+  if (rc) return fail(rc, "kernel launch failed: %s", hipGetErrorString(hipGetLastError()));
+  return ok();
+}
+
 HS_API int hs_play(const double* weights, int B, int N, int how, const double* u,
                    int32_t* choice, void* stream) {
   int rc = check_shape(B, N, 1, 1);

@@ -302,3 +302,30 @@ def test_noalloc_workspace_limit_and_validation():
     assert call(0, 8, 8, 151936) == 2  # HS_ERR_SHAPE
     assert call(1, 65, 8, 151936) == 8  # HS_ERR_LIMIT
     assert call(1, 8, 8, 151936, T=0.0) == 5  # HS_ERR_TEMPERATURE
+
+
+def _cmass(lib, **kw):
+    a = dict(target=hs.hs_view(FAKE, 8 * 151936, 151936), N=8, B=1, K=8, V=151936, dtype=1,
+             T=0.7, lse=FAKE, cand=FAKE, C=10, gamma=FAKE)
+    a.update(kw)
+    tv = a["target"]
+    return lib.hs_candidate_mass(ctypes.byref(tv) if tv is not None else None, a["N"], a["B"],
+                                 a["K"], a["V"], a["dtype"], a["T"], a["lse"], a["cand"], a["C"],
+                                 a["gamma"], None)
+
+
+def test_candidate_mass_validation_codes():
+    # every rejection happens on the host, before any HIP call (no GPU here)
+    lib = hs.load_library()
+    assert _cmass(lib, N=0) == 2
+    assert _cmass(lib, K=65) == 8
+    assert _cmass(lib, dtype=5) == 3
+    assert _cmass(lib, target=None) == 1
+    assert _cmass(lib, lse=None) == 1
+    assert _cmass(lib, cand=None) == 1
+    assert _cmass(lib, gamma=None) == 1
+    assert _cmass(lib, C=0) == 8
+    assert _cmass(lib, C=1025) == 8
+    assert _cmass(lib, T=0.0) == 5
+    assert _cmass(lib, T=float("nan")) == 5
+    assert _cmass(lib, target=hs.hs_view(FAKE + 2, 8 * 151936, 151936)) == 4

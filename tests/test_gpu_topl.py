@@ -183,3 +183,62 @@ def test_topl_fp32_full_vocabulary():
     x = synth.generate(w)
     for L in (10, 32):
         check(x, L, T=0.8)
+
+
+# ---- Theorem 2 with dynamic pruning: hs_candidate_mass ----------------------------------------
+
+def _target_lse(xd_target, V, T):
+    B, K, ld = xd_target.shape
+    _, lse, _ = hs.softmax_stats(xd_target.reshape(B * K, ld), V=V, temperature=T)
+    return lse.reshape(B, K)
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32, synth.F16])
+def test_candidate_mass_of_pruned_children(dtype):
+    # the children hs_eval_topl returns, then pruned (a seeded mask empties some slots): the
+    # unpruned sets give hs_eval_topl's own gamma, the pruned ones the oracle's mass
+    w = synth.variant(WL["qwen3_8b_single"], B=2, K=3, N=5, V=20011, ld=20016, dtype=dtype,
+                      scales=[0.3 + 0.2 * i for i in range(5)], permute=False)
+    note("candidate mass of pruned children dtype=%d" % dtype)
+    x = synth.generate(w)
+    xd = to_dev(x)
+    T, L = 0.8, 10
+    out = hs.eval_topl(xd, L=L, V=w.V, temperature=T, want_gamma=True, want_children=True)
+    lse = _target_lse(xd[0], w.V, T)
+    full = hs.candidate_mass(xd[0], lse, out["children"], V=w.V, temperature=T)
+    torch.cuda.synchronize()
+    assert np.abs(full.cpu().numpy() - out["gamma"].cpu().numpy()).max() <= GAMMA_TOL
+    cand = out["children"].cpu().numpy().copy()
+    rng = np.random.default_rng(7)
+    cand[rng.random(cand.shape) < 0.4] = -1
+    got = hs.candidate_mass(xd[0], lse, torch.from_numpy(cand).cuda(), V=w.V, temperature=T)
+    torch.cuda.synchronize()
+    ref = oracle.candidate_mass(x[0], cand.transpose(0, 2, 1, 3), V=w.V, T=T)  # [B][K][N]
+    assert np.abs(got.cpu().numpy() - ref.transpose(0, 2, 1)).max() <= GAMMA_TOL
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32, synth.F16])
+def test_candidate_mass_long_lists_duplicates_and_bad_indices(dtype):
+    # C = 150 slots (three passes of a wave), duplicates counted per listing, empty slots,
+    # whole empty sets (mass 0) and one index past V (NaN for that output only)
+    w = synth.variant(WL["qwen3_8b_single"], B=3, K=2, N=4, V=3001, ld=3008, dtype=dtype,
+                      scales=[0.3 + 0.2 * i for i in range(4)], permute=False)
+    note("candidate mass long lists dtype=%d" % dtype)
+    x = synth.generate(w)
+    xd = to_dev(x)
+    rng = np.random.default_rng(8)
+    C = 150
+    cand = rng.integers(-1, w.V, size=(w.B, w.N, w.K, C)).astype(np.int32)
+    cand[0, 1, 0, 5:9] = cand[0, 1, 0, 0]  # duplicates
+    cand[1, 2, 1, :] = -1                  # an empty set
+    cand[2, 3, 0, 77] = w.V                # past the row end
+    for T in (1.0, 0.6):
+        lse = _target_lse(xd[0], w.V, T)
+        got = hs.candidate_mass(xd[0], lse, torch.from_numpy(cand).cuda(), V=w.V,
+                                temperature=T).cpu().numpy()
+        ref = oracle.candidate_mass(x[0], cand.transpose(0, 2, 1, 3), V=w.V, T=T).transpose(0, 2, 1)
+        nan = np.isnan(ref)
+        assert nan.sum() == 1 and nan[2, 3, 0]
+        assert np.array_equal(np.isnan(got), nan)
+        assert got[1, 2, 1] == 0.0
+        assert np.abs(got[~nan] - ref[~nan]).max() <= GAMMA_TOL
