@@ -422,6 +422,13 @@ HS_API int hs_eval_topl(const hs_view* target, const hs_view* drafters_host, int
   return ok();
 }
 
+namespace hs {
+// defined next to its kernel in hs_cmass.hip
+int launch_candidate_mass(const void* tptr, int64_t sb, int64_t sk, int dtype, int B, int N,
+                          int K, int64_t V, int C, float c, const float* lse,
+                          const int32_t* cand, float* gamma, hipStream_t stream);
+}  // namespace hs
+
 HS_API int hs_candidate_mass(const hs_view* target, int N, int B, int K, int64_t V, int dtype,
                              float temperature, const float* target_lse, const int32_t* cand,
                              int C, float* gamma, void* stream) {

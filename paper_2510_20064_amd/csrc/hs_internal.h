@@ -296,9 +296,6 @@ __device__ inline void lse2_combine(float& o, float& s, float o2, float s2) {
 namespace hs {
 int launch_softmax_stats(const void* x, int dtype, int64_t rows, int64_t V, int64_t ld, float c,
                          float* row_max, float* row_lse, int32_t* row_argmax, hipStream_t stream);
-int launch_candidate_mass(const void* tptr, int64_t sb, int64_t sk, int dtype, int B, int N,
-                          int K, int64_t V, int C, float c, const float* lse,
-                          const int32_t* cand, float* gamma, hipStream_t stream);
 
 struct TailArgs {
   const float* alpha;
