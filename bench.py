@@ -121,6 +121,9 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline, two thirds on all "
                          "cores and one third on one thread (0 = skip)")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--pruned", type=float, default=0.0, metavar="KEEP",
+                    help="with --topl: also time hs_candidate_mass on the children pruned to "
+                         "a seeded KEEP fraction (Theorem 2 with dynamic pruning)")
     ap.add_argument("--f16", action="store_true",
                     help="store the workload's logits as fp16 (IEEE binary16) instead")
     ap.add_argument("--greedy", action="store_true",
@@ -329,6 +332,62 @@ def bench_softmax_stats(args, w, hs, torch, dev, synth):
     print(json.dumps(line), flush=True)
 
 
+def bench_pruned(args, w, hs, torch, np, bufs, copies, L):
+    """hs_candidate_mass after hs_eval_topl: each copy's children with a seeded (1 - KEEP)
+    share of the slots emptied, the target's lse from hs_softmax_stats; graph-replayed calls
+    over the resident copies, timed with HIP events."""
+    T = w.temperature
+    rng = np.random.default_rng(12)
+    lses, cands, outs = [], [], []
+    for i in range(copies):
+        o = hs.eval_topl(bufs[i], L=L, V=w.V, temperature=T, want_gamma=True, want_hit=False,
+                         want_children=True)
+        c = o["children"].cpu().numpy()
+        c[rng.random(c.shape) >= args.pruned] = -1
+        cands.append(torch.from_numpy(c).cuda())
+        tgt = bufs[i][0]
+        _, lse, _ = hs.softmax_stats(tgt.reshape(w.B * w.K, -1), V=w.V, temperature=T)
+        lses.append(lse.reshape(w.B, w.K))
+        outs.append(torch.empty((w.B, w.N, w.K), dtype=torch.float32, device=tgt.device))
+    stream = torch.cuda.Stream()
+
+    def call(i):
+        hs.candidate_mass(bufs[i][0], lses[i], cands[i], V=w.V, temperature=T, out=outs[i],
+                          stream=torch.cuda.current_stream())
+
+    per_graph = max(copies, 16)  # a short kernel: several calls per replay amortise its launch
+    with torch.cuda.stream(stream):
+        for i in range(copies):
+            call(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(per_graph):
+            call(i % copies)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // per_graph)
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup // per_graph)):
+            g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+    kept = float(np.mean([(c >= 0).float().mean().item() for c in cands]))
+    outputs = w.B * w.N * w.K
+    # bytes a call needs: the candidate lists, one lse per group, the kept target logits, gamma
+    nbytes = outputs * L * 4 + w.B * w.K * 4 + outputs * L * kept * w.elem_bytes + outputs * 4
+    return {"kernel": "hs_candidate_mass (one launch)", "us_per_call": us,
+            "outputs_per_s": outputs / (us * 1e-6), "keep_fraction": round(kept, 4),
+            "slots_per_output": L, "bytes_per_call": int(nbytes),
+            "achieved_GBps": nbytes / (us * 1e-6) / 1e9, "bound": "latency"}
+
+
 def bench_topl(args, w, hs, torch, dev, np, synth):
     """hs_eval_topl on distinct rounds resident in HBM (>= 512 MB, rotated), in a HIP graph.
     A call is two launches (per-slice candidates, then the merge); the roofline prices the whole
@@ -378,6 +437,7 @@ def bench_topl(args, w, hs, torch, dev, np, synth):
     wall = time.perf_counter() - t0
     us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
     achieved = w.input_bytes / (us * 1e-6) / 1e9
+    pruned = bench_pruned(args, w, hs, torch, np, bufs, copies, L) if args.pruned > 0 else None
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
@@ -425,6 +485,8 @@ def bench_topl(args, w, hs, torch, dev, np, synth):
                                    "(one call, both launches timed)",
                          "kernel_us": us, "algorithmic_bytes_per_launch": w.input_bytes},
             "cpu_baseline": cpu}
+    if pruned:
+        line["pruned_mass"] = pruned
     print(json.dumps(line), flush=True)
 
 
