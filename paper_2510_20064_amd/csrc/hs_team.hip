@@ -876,7 +876,15 @@ __global__ __launch_bounds__(kThreads, 4) void hs_team_kernel(TeamArgs A) {
   const int teams = A.teams;
   // consecutive workgroups form a team; the workgroups that share a CU (w, w + CUs, ...)
   // then belong to different teams, so that one team's waits leave the CU to the others
-  const int T = (int)fdiv(blockIdx.x, A.divS), slot = blockIdx.x - T * S;
+  const int T = (int)fdiv(blockIdx.x, A.divS);
+  // slot: the member's slice. The pipelined kernel rotates it by the team index, so that the
+  // workgroups a CU holds at once (w, w + CUs, ...) take different slices also when S divides
+  // the number of CUs (8% on 64 stacked fp32 tiny chains, S = 32; no change where it does not)
+  int slot = (int)blockIdx.x - T * S;
+  if constexpr (NEED_SUM && !SINGLE) {
+    slot += T - (int)fdiv((uint32_t)T, A.divS) * S;  // + T mod S
+    if (slot >= S) slot -= S;
+  }
   const uint32_t nsets = fdiv((uint32_t)A.items, A.divS);
   constexpr int kStatic = NEED_SUM ? 3 : 2;  // items per team with a fixed row set
   // slot 0 folds row 0 of every item, so it waits for the whole team each item: it can never
