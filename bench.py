@@ -99,13 +99,16 @@ def measured_topl_traffic(workload: str):
     return rec["hbm_bytes_per_call"]
 
 
+LOGIT_TYPES = ("fp32", "bf16", "fp16")  # by the library's dtype code (HS_F32, HS_BF16, HS_F16)
+
+
 def logit_type(w) -> str:
-    return ("fp32", "bf16", "fp16")[w.dtype]
+    return LOGIT_TYPES[w.dtype]
 
 
 def profile_name(w, name: str) -> str:
     """The counter summary that covers this run (the workloads' own storage types have one)."""
-    return name + "_f16" if w.dtype == 2 and not name.endswith("_f16") else name
+    return name + "_f16" if LOGIT_TYPES[w.dtype] == "fp16" and not name.endswith("_f16") else name
 
 
 def parse():
